@@ -1,0 +1,227 @@
+/*
+ * liveserve_kv.h — C ABI of the MI355X (gfx950) paged-KV hot path under
+ * LiveServe's interaction-aware serving (arXiv 2606.22983).
+ *
+ * The paper keeps the serving engine's paged KV block pool and its
+ * block-level allocation (§5.1, §6 "Hierarchical KV cache manager"), reuses a
+ * session's multi-turn KV so the next turn does not re-prefill history (§5),
+ * offloads idle multi-turn KV from HBM to host DRAM (§5, §5.1) and preloads it
+ * back during user speech through the HBM-DRAM offload connector's
+ * asynchronous transfer path (§5.2, §6).  This library is the data-parallel
+ * part of that: attention of the thinker/talker decoders (§2.1) over the
+ * per-session paged cache — batched single-token decode and next-turn chunked
+ * prefill over reused context — and the block stash/restore copies.
+ *
+ * Conventions for every entry point
+ *   - Ownership: the caller owns every buffer (device memory, pinned host
+ *     memory).  The library never allocates device memory; a pool handle owns
+ *     only host-side metadata.
+ *   - Asynchrony: work is enqueued on the given HIP stream (NULL = the default
+ *     stream) and the call returns without waiting for it.
+ *   - Errors: arguments are validated on the host before anything is
+ *     enqueued; any status other than LS_OK means nothing was enqueued.
+ *     ls_last_error() returns a message for the calling thread's last failure.
+ *     No C++ exception crosses this boundary.
+ *   - Device-side index arrays (block tables, lengths, block ids) are read by
+ *     the kernels, which bounds-check every block id they dereference: an id
+ *     outside [0, num_blocks) is skipped (its keys are treated as absent, its
+ *     copy is not made) and a bit is set in a device error word that
+ *     ls_device_errors() returns.  A result computed with such an id is not
+ *     meaningful.
+ *   - Concurrency: calls on different streams may run concurrently only on
+ *     disjoint sets of blocks; ordering between streams is the caller's
+ *     (events).  Blocks being restored must not be read by attention until the
+ *     restore's stream has been waited on — the same rule the paper's KV
+ *     manager follows before reusing preloaded KV (§5.2).
+ *   - Data types: K, V, Q and outputs are bfloat16 (bf16); arithmetic inside
+ *     attention accumulates in fp32.
+ *
+ * Pool layout (device memory, bf16, num_layers x num_blocks x 2 x Hkv tiles):
+ *   pool[layer][block][kv][head][tile]         kv = 0: K, kv = 1: V
+ *   K tile = [block_size tokens][head_dim]     (token-major)
+ *   V tile = [head_dim][block_size tokens]     (dim-major)
+ * Logical token t of session s lives in slot t % block_size of block
+ * block_tables[s * max_blocks_per_session + t / block_size].
+ *
+ * Staging layout of stash/restore (device or pinned host memory):
+ *   staging[i][layer][kv][head][tile]   for block ids[i], i = 0..n-1
+ * i.e. every layer's (K, V) slab of one block is contiguous, block after block.
+ */
+#ifndef LIVESERVE_KV_H
+#define LIVESERVE_KV_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    LS_OK = 0,
+    LS_EINVAL = -22,        /* invalid argument; nothing enqueued */
+    LS_ENOMEM = -12,        /* a caller-provided buffer is too small */
+    LS_EHIP = -5,           /* a HIP runtime call failed */
+    LS_EUNSUPPORTED = -95   /* valid but unsupported geometry (head_dim, group size) */
+} ls_status;
+
+/* Bits of the device error word (ls_device_errors). */
+#define LS_DEVERR_BLOCK_ID 0x1u     /* a block id outside [0, num_blocks) was skipped */
+#define LS_DEVERR_LENGTH   0x2u     /* a length exceeded its block table and was clipped */
+
+typedef struct ls_kv_pool ls_kv_pool;
+
+typedef struct {
+    int32_t num_layers;        /* >= 1 */
+    int32_t num_kv_heads;      /* Hkv >= 1 */
+    int32_t head_dim;          /* D: 64 or 128 */
+    int32_t block_size;        /* tokens per block: 16 */
+    int64_t num_blocks;        /* blocks per layer */
+    void *kv_base;             /* device, >= ls_kv_pool_bytes(...) bytes, 256-byte aligned */
+    size_t kv_bytes;
+    void *staging_ring;        /* device ring used when stash/restore staging is host memory;
+                                  may be NULL (then only device staging is accepted) */
+    size_t staging_ring_bytes; /* a multiple of one block's all-layer slab is used */
+} ls_kv_pool_desc;
+
+/* Bytes of pool memory for the given geometry (0 on overflow or bad geometry). */
+size_t ls_kv_pool_bytes(int32_t num_layers, int64_t num_blocks, int32_t num_kv_heads,
+                        int32_t head_dim, int32_t block_size);
+
+/*
+ * kv_pool_create — wrap caller-owned device memory as a paged KV block pool
+ * (the paged KV block pool of §6, block-level allocation of §5.1).  Validates
+ * the geometry (block_size 16, head_dim 64 or 128, kv_bytes large enough,
+ * 256-byte alignment), records the layout and the current HIP device, and
+ * writes an opaque handle to *out.  Launches nothing and touches no device
+ * memory.  LS_EINVAL on bad arguments, LS_EUNSUPPORTED on an unsupported
+ * head_dim or block_size.
+ */
+ls_status kv_pool_create(const ls_kv_pool_desc *desc, ls_kv_pool **out);
+
+/* Free the handle's host metadata (never the caller's memory).  NULL is OK. */
+ls_status kv_pool_destroy(ls_kv_pool *pool);
+
+/*
+ * Workspace bytes paged_attn_decode needs for this shape (split-K partial
+ * results and per-(session, KV head) arrival counters).  The workspace must be
+ * zero-filled once before its first use; every completed decode call leaves
+ * its counters at zero again, so it can be reused without clearing.
+ */
+size_t ls_decode_workspace_bytes(const ls_kv_pool *pool, int32_t num_sessions,
+                                 int32_t num_q_heads, int32_t max_blocks_per_session);
+
+/*
+ * paged_attn_decode — one batched decode step of the thinker/talker
+ * autoregressive decoders (§2.1; the engines' continuous-batching decode loop,
+ * §4 and §6) over the per-session paged KV cache.
+ *
+ *   q              device bf16 [num_sessions][num_q_heads][head_dim]: the step's query
+ *   k_new, v_new   device bf16 [num_sessions][num_kv_heads][head_dim], or both NULL.
+ *                  When given, the step's own K/V row is first written at logical
+ *                  position context_lens[s] (its block must already be in the table)
+ *                  and the query attends to context_lens[s] + 1 keys.
+ *   block_tables   device int32 [num_sessions][max_blocks_per_session]
+ *   context_lens   device int32 [num_sessions]: tokens already in the pool, >= 1
+ *                  (>= 0 with append).  A length whose keys do not fit the table
+ *                  is clipped to it and flagged (LS_DEVERR_LENGTH).
+ *   scale          softmax scale applied to q.k (normally 1/sqrt(head_dim))
+ *   out            device bf16 [num_sessions][num_q_heads][head_dim]:
+ *                  out = softmax(scale * q K^T) V over the session's keys, per query
+ *                  head h using KV head h / (num_q_heads / num_kv_heads)
+ *   workspace      device, >= ls_decode_workspace_bytes(...), zero-filled before first use
+ *
+ * Supported: num_q_heads / num_kv_heads in {1, 2, 4, 8}.  Errors: LS_EINVAL
+ * (NULL pointer, layer out of range, num_q_heads not a multiple of num_kv_heads,
+ * only one of k_new / v_new), LS_ENOMEM (workspace too small), LS_EUNSUPPORTED
+ * (group size), LS_EHIP (launch failure).
+ */
+ls_status paged_attn_decode(ls_kv_pool *pool, int32_t layer, int32_t num_sessions,
+                            int32_t num_q_heads, const void *q, const void *k_new,
+                            const void *v_new, const int32_t *block_tables,
+                            int32_t max_blocks_per_session, const int32_t *context_lens,
+                            float scale, void *out, void *workspace, size_t workspace_bytes,
+                            hipStream_t stream);
+
+/*
+ * paged_attn_prefill — next-turn (chunked) prefill over reused multi-turn
+ * context (§5: reusing LLM-stage KV avoids re-prefilling conversation history;
+ * §3: the prefetch endpoint's current-turn prefill).  Session s brings n_s new
+ * tokens; they are appended at logical positions c_s .. c_s + n_s - 1 and new
+ * row j attends causally to keys 0 .. c_s + j (bottom-right alignment).  A
+ * chunked prefill is repeated calls with c_s advanced by the previous chunk.
+ *
+ *   q              device bf16 [total_new_tokens][num_q_heads][head_dim], sessions
+ *                  back to back in cu_new_lens order
+ *   k_new, v_new   device bf16 [total_new_tokens][num_kv_heads][head_dim], or both
+ *                  NULL when the turn's K/V is already in the pool
+ *   cu_new_lens    device int32 [num_sessions + 1]: prefix sums of n_s (cu[0] = 0)
+ *   reused_lens    device int32 [num_sessions]: c_s >= 0
+ *   total_new_tokens, max_new_len   host ints: cu[S] and max_s n_s (grid sizing)
+ *   block_tables   device int32 [num_sessions][max_blocks_per_session], covering
+ *                  c_s + n_s tokens
+ *   out            device bf16 [total_new_tokens][num_q_heads][head_dim]
+ *
+ * Supported: head_dim 128 or 64, num_q_heads / num_kv_heads in {1, 2, 4, 8}.
+ * Errors as for paged_attn_decode.
+ */
+ls_status paged_attn_prefill(ls_kv_pool *pool, int32_t layer, int32_t num_sessions,
+                             int32_t num_q_heads, const void *q, const void *k_new,
+                             const void *v_new, const int32_t *cu_new_lens,
+                             const int32_t *reused_lens, int32_t total_new_tokens,
+                             int32_t max_new_len, const int32_t *block_tables,
+                             int32_t max_blocks_per_session, float scale, void *out,
+                             hipStream_t stream);
+
+/*
+ * kv_blocks_stash — offload: copy every layer's K/V slab of blocks ids[0..n-1]
+ * into staging (layout above), the HBM-to-DRAM eviction of idle multi-turn KV
+ * (§5, §5.1; eviction stays block-level, suffix blocks first — the order is
+ * the caller's).  The pool is left unchanged; freeing the ids is the caller's
+ * decision once the stream has passed this call.
+ *
+ *   block_ids       device int32 [n]: distinct ids in [0, num_blocks)
+ *   block_ids_host  optional host copy of the same ids; when given, range and
+ *                   distinctness are checked on the host (LS_EINVAL)
+ *   staging         device memory, or pinned host memory when staging_on_host != 0
+ *                   (then the copy runs through the pool's staging_ring in whole-block
+ *                   chunks: gather kernel, then a device-to-host DMA, per chunk)
+ * Bit-exact byte copy.  n == 0 is a no-op.
+ */
+ls_status kv_blocks_stash(ls_kv_pool *pool, int32_t n, const int32_t *block_ids,
+                          const int32_t *block_ids_host, void *staging,
+                          int32_t staging_on_host, hipStream_t stream);
+
+/*
+ * kv_blocks_restore — reload / speech-triggered preload: copy staging (layout
+ * above) back into pool blocks ids[0..n-1] (§5.2; the offload connector's
+ * asynchronous transfer path, §6).  Blocks are written in id order, so a
+ * restore cut short by the caller (a cancelled preload) leaves a complete
+ * prefix, and restoring the remaining ids afterwards (the synchronous
+ * fallback of §5.2) gives the same pool as one full restore.
+ * Arguments as for kv_blocks_stash; with staging_on_host != 0 each chunk is a
+ * host-to-device DMA into the staging ring followed by the scatter kernel.
+ * Bit-exact byte copy.  n == 0 is a no-op.
+ */
+ls_status kv_blocks_restore(ls_kv_pool *pool, int32_t n, const int32_t *block_ids,
+                            const int32_t *block_ids_host, const void *staging,
+                            int32_t staging_on_host, hipStream_t stream);
+
+/*
+ * Wait for `stream`, then return (and clear) the device error word of the
+ * current device in *bits (LS_DEVERR_* bits; 0 when no kernel met a bad index).
+ */
+ls_status ls_device_errors(uint32_t *bits, hipStream_t stream);
+
+/* Message of the calling thread's most recent non-OK status ("" if none). */
+const char *ls_last_error(void);
+
+/* Library version string. */
+const char *ls_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LIVESERVE_KV_H */

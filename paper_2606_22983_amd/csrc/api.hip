@@ -1,0 +1,304 @@
+// C-ABI entry points: argument validation, pool bookkeeping and kernel
+// launches.  Every check happens before anything is enqueued, so a non-OK
+// status means the stream is untouched.
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <vector>
+
+#include "common.h"
+
+struct ls_kv_pool {
+    ls::PoolGeom geom;
+};
+
+namespace ls {
+
+namespace {
+// One error word per device, in the library's own code object.
+__device__ unsigned int g_device_errors = 0;
+}  // namespace
+
+unsigned int *device_error_word() {
+    static std::mutex mu;
+    static unsigned int *addr[64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(g_device_errors)) == hipSuccess)
+            addr[dev] = static_cast<unsigned int *>(p);
+    }
+    return addr[dev];
+}
+
+namespace {
+
+thread_local char t_last_error[512] = "";
+
+ls_status fail(ls_status st, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(t_last_error, sizeof t_last_error, fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+ls_status hip_fail(hipError_t e, const char *what) {
+    return fail(LS_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool supported_head_dim(int32_t d) { return d == 64 || d == 128; }
+bool supported_group(int32_t g) { return g == 1 || g == 2 || g == 4 || g == 8; }
+
+ls_status check_pool(const ls_kv_pool *pool) {
+    if (!pool) return fail(LS_EINVAL, "pool handle is NULL");
+    return LS_OK;
+}
+
+ls_status check_heads(const PoolGeom &p, int32_t num_q_heads) {
+    if (num_q_heads <= 0 || num_q_heads % p.num_kv_heads != 0)
+        return fail(LS_EINVAL, "num_q_heads (%d) must be a positive multiple of num_kv_heads (%d)",
+                    num_q_heads, p.num_kv_heads);
+    if (!supported_group(num_q_heads / p.num_kv_heads))
+        return fail(LS_EUNSUPPORTED, "query heads per KV head must be 1, 2, 4 or 8 (got %d)",
+                    num_q_heads / p.num_kv_heads);
+    return LS_OK;
+}
+
+// Host check of a restore/stash id list: range and distinctness.
+ls_status check_ids_host(const PoolGeom &p, int32_t n, const int32_t *ids) {
+    std::vector<unsigned char> seen((size_t)p.num_blocks, 0);
+    for (int32_t i = 0; i < n; ++i) {
+        const int32_t b = ids[i];
+        if (b < 0 || b >= p.num_blocks)
+            return fail(LS_EINVAL, "block id %d at position %d is outside [0, %lld)", b, i,
+                        (long long)p.num_blocks);
+        if (seen[(size_t)b]) return fail(LS_EINVAL, "block id %d appears twice", b);
+        seen[(size_t)b] = 1;
+    }
+    return LS_OK;
+}
+
+ls_status copy_blocks(ls_kv_pool *pool, int32_t n, const int32_t *block_ids,
+                      const int32_t *block_ids_host, void *staging, int32_t staging_on_host,
+                      bool to_pool, hipStream_t stream) {
+    if (ls_status st = check_pool(pool)) return st;
+    const PoolGeom &p = pool->geom;
+    if (n < 0) return fail(LS_EINVAL, "n must be >= 0");
+    if (n == 0) return LS_OK;
+    if (!block_ids || !staging) return fail(LS_EINVAL, "block_ids and staging must not be NULL");
+    if (n > p.num_blocks) return fail(LS_EINVAL, "n (%d) exceeds num_blocks", n);
+    if (block_ids_host)
+        if (ls_status st = check_ids_host(p, n, block_ids_host)) return st;
+    const size_t per_block = p.slab_bytes() * (size_t)p.num_layers;
+    if (staging_on_host && (!p.ring || p.ring_bytes < per_block))
+        return fail(LS_ENOMEM, "host staging needs a device staging ring of at least %zu bytes",
+                    per_block);
+    unsigned int *err = device_error_word();
+    if (!err) return fail(LS_EHIP, "cannot resolve the device error word");
+    if (!staging_on_host) {
+        hipError_t e = launch_block_copy(p, n, block_ids, static_cast<uint8_t *>(staging), to_pool, err, stream);
+        return e == hipSuccess ? LS_OK : hip_fail(e, "block copy launch");
+    }
+    // Whole blocks per chunk, in id order, all on the caller's stream.
+    const int32_t chunk = (int32_t)(p.ring_bytes / per_block);
+    uint8_t *host = static_cast<uint8_t *>(staging);
+    for (int32_t i0 = 0; i0 < n; i0 += chunk) {
+        const int32_t cnt = (n - i0) < chunk ? (n - i0) : chunk;
+        const size_t bytes = per_block * (size_t)cnt;
+        hipError_t e;
+        if (to_pool) {
+            e = hipMemcpyAsync(p.ring, host + per_block * (size_t)i0, bytes, hipMemcpyHostToDevice, stream);
+            if (e != hipSuccess) return hip_fail(e, "restore host-to-device copy");
+            e = launch_block_copy(p, cnt, block_ids + i0, p.ring, true, err, stream);
+            if (e != hipSuccess) return hip_fail(e, "restore scatter launch");
+        } else {
+            e = launch_block_copy(p, cnt, block_ids + i0, p.ring, false, err, stream);
+            if (e != hipSuccess) return hip_fail(e, "stash gather launch");
+            e = hipMemcpyAsync(host + per_block * (size_t)i0, p.ring, bytes, hipMemcpyDeviceToHost, stream);
+            if (e != hipSuccess) return hip_fail(e, "stash device-to-host copy");
+        }
+    }
+    return LS_OK;
+}
+
+}  // namespace
+}  // namespace ls
+
+using namespace ls;
+
+extern "C" {
+
+size_t ls_kv_pool_bytes(int32_t num_layers, int64_t num_blocks, int32_t num_kv_heads,
+                        int32_t head_dim, int32_t block_size) {
+    if (num_layers <= 0 || num_blocks <= 0 || num_kv_heads <= 0 || head_dim <= 0 || block_size <= 0)
+        return 0;
+    const unsigned __int128 bytes = (unsigned __int128)num_layers * (unsigned __int128)num_blocks *
+                                    2u * (unsigned)num_kv_heads * (unsigned)block_size *
+                                    (unsigned)head_dim * 2u;
+    if (bytes > (unsigned __int128)SIZE_MAX) return 0;
+    return (size_t)bytes;
+}
+
+ls_status kv_pool_create(const ls_kv_pool_desc *desc, ls_kv_pool **out) {
+    if (!desc || !out) return fail(LS_EINVAL, "desc and out must not be NULL");
+    *out = nullptr;
+    if (desc->num_layers <= 0 || desc->num_kv_heads <= 0 || desc->num_blocks <= 0)
+        return fail(LS_EINVAL, "num_layers, num_kv_heads and num_blocks must be positive");
+    if (desc->block_size != kBlock)
+        return fail(LS_EUNSUPPORTED, "block_size must be %d (got %d)", kBlock, desc->block_size);
+    if (!supported_head_dim(desc->head_dim))
+        return fail(LS_EUNSUPPORTED, "head_dim must be 64 or 128 (got %d)", desc->head_dim);
+    if (desc->num_blocks > INT32_MAX)
+        return fail(LS_EINVAL, "num_blocks must fit in int32 (block ids are int32)");
+    if (!desc->kv_base) return fail(LS_EINVAL, "kv_base must not be NULL");
+    if (reinterpret_cast<uintptr_t>(desc->kv_base) % 256 != 0)
+        return fail(LS_EINVAL, "kv_base must be 256-byte aligned");
+    const size_t need = ls_kv_pool_bytes(desc->num_layers, desc->num_blocks, desc->num_kv_heads,
+                                         desc->head_dim, desc->block_size);
+    if (need == 0) return fail(LS_EINVAL, "pool size overflows");
+    if (desc->kv_bytes < need)
+        return fail(LS_ENOMEM, "kv_bytes (%zu) is smaller than the layout needs (%zu)",
+                    desc->kv_bytes, need);
+    if (desc->staging_ring && reinterpret_cast<uintptr_t>(desc->staging_ring) % 16 != 0)
+        return fail(LS_EINVAL, "staging_ring must be 16-byte aligned");
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) dev = -1;
+    ls_kv_pool *pool = new (std::nothrow) ls_kv_pool;
+    if (!pool) return fail(LS_ENOMEM, "out of host memory");
+    pool->geom.num_layers = desc->num_layers;
+    pool->geom.num_kv_heads = desc->num_kv_heads;
+    pool->geom.head_dim = desc->head_dim;
+    pool->geom.num_blocks = desc->num_blocks;
+    pool->geom.base = static_cast<uint16_t *>(desc->kv_base);
+    pool->geom.ring = static_cast<uint8_t *>(desc->staging_ring);
+    pool->geom.ring_bytes = desc->staging_ring ? desc->staging_ring_bytes : 0;
+    pool->geom.device = dev;
+    *out = pool;
+    return LS_OK;
+}
+
+ls_status kv_pool_destroy(ls_kv_pool *pool) {
+    delete pool;
+    return LS_OK;
+}
+
+size_t ls_decode_workspace_bytes(const ls_kv_pool *pool, int32_t num_sessions,
+                                 int32_t num_q_heads, int32_t max_blocks_per_session) {
+    if (!pool || num_sessions <= 0 || max_blocks_per_session <= 0 || num_q_heads <= 0) return 0;
+    return plan_decode(pool->geom, num_sessions, num_q_heads, max_blocks_per_session).total();
+}
+
+ls_status paged_attn_decode(ls_kv_pool *pool, int32_t layer, int32_t num_sessions,
+                            int32_t num_q_heads, const void *q, const void *k_new,
+                            const void *v_new, const int32_t *block_tables,
+                            int32_t max_blocks_per_session, const int32_t *context_lens,
+                            float scale, void *out, void *workspace, size_t workspace_bytes,
+                            hipStream_t stream) {
+    if (ls_status st = check_pool(pool)) return st;
+    const PoolGeom &p = pool->geom;
+    if (layer < 0 || layer >= p.num_layers)
+        return fail(LS_EINVAL, "layer %d outside [0, %d)", layer, p.num_layers);
+    if (num_sessions < 0) return fail(LS_EINVAL, "num_sessions must be >= 0");
+    if (ls_status st = check_heads(p, num_q_heads)) return st;
+    if (num_sessions == 0) return LS_OK;
+    if (!q || !block_tables || !context_lens || !out || !workspace)
+        return fail(LS_EINVAL, "q, block_tables, context_lens, out and workspace must not be NULL");
+    if ((k_new == nullptr) != (v_new == nullptr))
+        return fail(LS_EINVAL, "k_new and v_new must both be given or both be NULL");
+    if (max_blocks_per_session <= 0) return fail(LS_EINVAL, "max_blocks_per_session must be > 0");
+    if (!(scale > 0.f) || scale != scale) return fail(LS_EINVAL, "scale must be a positive number");
+    const DecodePlan plan = plan_decode(p, num_sessions, num_q_heads, max_blocks_per_session);
+    if (workspace_bytes < plan.total())
+        return fail(LS_ENOMEM, "workspace_bytes (%zu) < required (%zu)", workspace_bytes, plan.total());
+    unsigned int *err = device_error_word();
+    if (!err) return fail(LS_EHIP, "cannot resolve the device error word");
+    if (k_new) {
+        hipError_t e = launch_append_decode(p, layer, num_sessions, static_cast<const uint16_t *>(k_new),
+                                            static_cast<const uint16_t *>(v_new), block_tables,
+                                            max_blocks_per_session, context_lens, err, stream);
+        if (e != hipSuccess) return hip_fail(e, "append launch");
+    }
+    hipError_t e = launch_decode(p, layer, num_sessions, num_q_heads, static_cast<const uint16_t *>(q),
+                                 k_new != nullptr, block_tables, max_blocks_per_session, context_lens,
+                                 scale, static_cast<uint16_t *>(out), workspace, plan, err, stream);
+    return e == hipSuccess ? LS_OK : hip_fail(e, "decode launch");
+}
+
+ls_status paged_attn_prefill(ls_kv_pool *pool, int32_t layer, int32_t num_sessions,
+                             int32_t num_q_heads, const void *q, const void *k_new,
+                             const void *v_new, const int32_t *cu_new_lens,
+                             const int32_t *reused_lens, int32_t total_new_tokens,
+                             int32_t max_new_len, const int32_t *block_tables,
+                             int32_t max_blocks_per_session, float scale, void *out,
+                             hipStream_t stream) {
+    if (ls_status st = check_pool(pool)) return st;
+    const PoolGeom &p = pool->geom;
+    if (layer < 0 || layer >= p.num_layers)
+        return fail(LS_EINVAL, "layer %d outside [0, %d)", layer, p.num_layers);
+    if (num_sessions < 0 || total_new_tokens < 0 || max_new_len < 0)
+        return fail(LS_EINVAL, "num_sessions, total_new_tokens and max_new_len must be >= 0");
+    if (ls_status st = check_heads(p, num_q_heads)) return st;
+    if (num_sessions == 0 || total_new_tokens == 0) return LS_OK;
+    if (!q || !cu_new_lens || !reused_lens || !block_tables || !out)
+        return fail(LS_EINVAL, "q, cu_new_lens, reused_lens, block_tables and out must not be NULL");
+    if ((k_new == nullptr) != (v_new == nullptr))
+        return fail(LS_EINVAL, "k_new and v_new must both be given or both be NULL");
+    if (max_blocks_per_session <= 0) return fail(LS_EINVAL, "max_blocks_per_session must be > 0");
+    if (max_new_len > total_new_tokens)
+        return fail(LS_EINVAL, "max_new_len (%d) exceeds total_new_tokens (%d)", max_new_len,
+                    total_new_tokens);
+    if (!(scale > 0.f) || scale != scale) return fail(LS_EINVAL, "scale must be a positive number");
+    unsigned int *err = device_error_word();
+    if (!err) return fail(LS_EHIP, "cannot resolve the device error word");
+    if (k_new) {
+        hipError_t e = launch_append_prefill(p, layer, num_sessions, total_new_tokens,
+                                             static_cast<const uint16_t *>(k_new),
+                                             static_cast<const uint16_t *>(v_new), cu_new_lens,
+                                             reused_lens, block_tables, max_blocks_per_session, err,
+                                             stream);
+        if (e != hipSuccess) return hip_fail(e, "append launch");
+    }
+    hipError_t e = launch_prefill(p, layer, num_sessions, num_q_heads, static_cast<const uint16_t *>(q),
+                                  cu_new_lens, reused_lens, max_new_len, block_tables,
+                                  max_blocks_per_session, scale, static_cast<uint16_t *>(out), err, stream);
+    return e == hipSuccess ? LS_OK : hip_fail(e, "prefill launch");
+}
+
+ls_status kv_blocks_stash(ls_kv_pool *pool, int32_t n, const int32_t *block_ids,
+                          const int32_t *block_ids_host, void *staging, int32_t staging_on_host,
+                          hipStream_t stream) {
+    return copy_blocks(pool, n, block_ids, block_ids_host, staging, staging_on_host, false, stream);
+}
+
+ls_status kv_blocks_restore(ls_kv_pool *pool, int32_t n, const int32_t *block_ids,
+                            const int32_t *block_ids_host, const void *staging,
+                            int32_t staging_on_host, hipStream_t stream) {
+    return copy_blocks(pool, n, block_ids, block_ids_host, const_cast<void *>(staging),
+                       staging_on_host, true, stream);
+}
+
+ls_status ls_device_errors(uint32_t *bits, hipStream_t stream) {
+    if (!bits) return fail(LS_EINVAL, "bits must not be NULL");
+    hipError_t e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return hip_fail(e, "stream synchronize");
+    unsigned int *word = device_error_word();
+    if (!word) return fail(LS_EHIP, "cannot resolve the device error word");
+    unsigned int v = 0, zero = 0;
+    e = hipMemcpy(&v, word, sizeof v, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "read device error word");
+    e = hipMemcpy(word, &zero, sizeof zero, hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "clear device error word");
+    *bits = v;
+    return LS_OK;
+}
+
+const char *ls_last_error(void) { return t_last_error; }
+
+const char *ls_version(void) { return "liveserve_kv 0.1.0 (gfx950)"; }
+
+}  // extern "C"

@@ -1,0 +1,247 @@
+"""Python binding of ``libliveserve_kv.so`` — argument marshalling only.
+
+Every function here has the name of the C entry point it calls and passes
+device pointers of torch tensors (PyTorch provides device memory and streams)
+plus the current HIP stream.  All work runs in the library's HIP kernels; there
+is no fallback.  Importing this module raises ``ImportError`` when the library
+has not been built (``python -m paper_2606_22983_amd.build``).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libliveserve_kv.so")
+if not os.path.exists(LIB_PATH):
+    raise ImportError("libliveserve_kv.so is not built; run `python -m paper_2606_22983_amd.build`")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+_p, _i32, _i64, _sz, _f32 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t,
+                             ctypes.c_float)
+
+
+class _PoolDesc(ctypes.Structure):
+    _fields_ = [("num_layers", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("block_size", ctypes.c_int32),
+                ("num_blocks", ctypes.c_int64), ("kv_base", ctypes.c_void_p),
+                ("kv_bytes", ctypes.c_size_t), ("staging_ring", ctypes.c_void_p),
+                ("staging_ring_bytes", ctypes.c_size_t)]
+
+
+_lib.ls_kv_pool_bytes.argtypes = [_i32, _i64, _i32, _i32, _i32]
+_lib.ls_kv_pool_bytes.restype = _sz
+_lib.kv_pool_create.argtypes = [ctypes.POINTER(_PoolDesc), ctypes.POINTER(_p)]
+_lib.kv_pool_destroy.argtypes = [_p]
+_lib.ls_decode_workspace_bytes.argtypes = [_p, _i32, _i32, _i32]
+_lib.ls_decode_workspace_bytes.restype = _sz
+_lib.paged_attn_decode.argtypes = [_p, _i32, _i32, _i32, _p, _p, _p, _p, _i32, _p, _f32, _p, _p,
+                                   _sz, _p]
+_lib.paged_attn_prefill.argtypes = [_p, _i32, _i32, _i32, _p, _p, _p, _p, _p, _i32, _i32, _p,
+                                    _i32, _f32, _p, _p]
+_lib.kv_blocks_stash.argtypes = [_p, _i32, _p, _p, _p, _i32, _p]
+_lib.kv_blocks_restore.argtypes = [_p, _i32, _p, _p, _p, _i32, _p]
+_lib.ls_device_errors.argtypes = [ctypes.POINTER(ctypes.c_uint32), _p]
+_lib.ls_last_error.restype = ctypes.c_char_p
+_lib.ls_version.restype = ctypes.c_char_p
+for _f in (_lib.kv_pool_create, _lib.kv_pool_destroy, _lib.paged_attn_decode,
+           _lib.paged_attn_prefill, _lib.kv_blocks_stash, _lib.kv_blocks_restore,
+           _lib.ls_device_errors):
+    _f.restype = ctypes.c_int
+
+LS_OK, LS_EINVAL, LS_ENOMEM, LS_EHIP, LS_EUNSUPPORTED = 0, -22, -12, -5, -95
+LS_DEVERR_BLOCK_ID, LS_DEVERR_LENGTH = 0x1, 0x2
+
+
+class LiveServeError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        msg = _lib.ls_last_error().decode(errors="replace")
+        super().__init__("%s failed with status %d: %s" % (where, status, msg))
+
+
+def _check(status: int, where: str):
+    if status != LS_OK:
+        raise LiveServeError(status, where)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dev(t: torch.Tensor, name: str, dtype=None):
+    if not t.is_cuda:
+        raise ValueError("%s must be a device tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if dtype is not None and t.dtype not in (dtype if isinstance(dtype, tuple) else (dtype,)):
+        raise ValueError("%s must have dtype %s (got %s)" % (name, dtype, t.dtype))
+    return t
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+_BF16 = (torch.bfloat16, torch.int16)
+
+
+def version() -> str:
+    return _lib.ls_version().decode()
+
+
+def ls_kv_pool_bytes(num_layers, num_blocks, num_kv_heads, head_dim, block_size=16) -> int:
+    return int(_lib.ls_kv_pool_bytes(num_layers, num_blocks, num_kv_heads, head_dim, block_size))
+
+
+class KVPool:
+    """Handle of a pool created by :func:`kv_pool_create` (keeps its tensors alive)."""
+
+    def __init__(self, handle, kv, ring, num_layers, num_blocks, num_kv_heads, head_dim,
+                 block_size):
+        self.handle = handle
+        self.kv = kv
+        self.ring = ring
+        self.num_layers = num_layers
+        self.num_blocks = num_blocks
+        self.num_kv_heads = num_kv_heads
+        self.head_dim = head_dim
+        self.block_size = block_size
+
+    @property
+    def slab_bytes(self) -> int:
+        return 2 * self.num_kv_heads * self.block_size * self.head_dim * 2
+
+    def close(self):
+        if self.handle:
+            _lib.kv_pool_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def kv_pool_create(kv: torch.Tensor, num_layers: int, num_blocks: int, num_kv_heads: int,
+                   head_dim: int, block_size: int = 16,
+                   staging_ring: Optional[torch.Tensor] = None) -> KVPool:
+    """Wrap ``kv`` (device memory of at least ``ls_kv_pool_bytes`` bytes) as a pool."""
+    _dev(kv, "kv")
+    if staging_ring is not None:
+        _dev(staging_ring, "staging_ring")
+    desc = _PoolDesc(num_layers, num_kv_heads, head_dim, block_size, num_blocks,
+                     kv.data_ptr(), kv.numel() * kv.element_size(),
+                     None if staging_ring is None else staging_ring.data_ptr(),
+                     0 if staging_ring is None else staging_ring.numel() * staging_ring.element_size())
+    handle = ctypes.c_void_p()
+    _check(_lib.kv_pool_create(ctypes.byref(desc), ctypes.byref(handle)), "kv_pool_create")
+    return KVPool(handle, kv, staging_ring, num_layers, num_blocks, num_kv_heads, head_dim,
+                  block_size)
+
+
+def decode_workspace_bytes(pool: KVPool, num_sessions: int, num_q_heads: int,
+                           max_blocks_per_session: int) -> int:
+    return int(_lib.ls_decode_workspace_bytes(pool.handle, num_sessions, num_q_heads,
+                                              max_blocks_per_session))
+
+
+def paged_attn_decode(pool: KVPool, layer: int, q: torch.Tensor, block_tables: torch.Tensor,
+                      context_lens: torch.Tensor, scale: float, out: torch.Tensor,
+                      workspace: torch.Tensor, k_new: Optional[torch.Tensor] = None,
+                      v_new: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """q/out: [S][Hq][D] bf16; block_tables int32 [S][maxb]; context_lens int32 [S]."""
+    _dev(q, "q", _BF16)
+    _dev(out, "out", _BF16)
+    _dev(block_tables, "block_tables", torch.int32)
+    _dev(context_lens, "context_lens", torch.int32)
+    _dev(workspace, "workspace")
+    if k_new is not None:
+        _dev(k_new, "k_new", _BF16)
+    if v_new is not None:
+        _dev(v_new, "v_new", _BF16)
+    s, hq = q.shape[0], q.shape[1]
+    _check(_lib.paged_attn_decode(pool.handle, layer, s, hq, _ptr(q), _ptr(k_new), _ptr(v_new),
+                                  _ptr(block_tables), block_tables.shape[1], _ptr(context_lens),
+                                  float(scale), _ptr(out), _ptr(workspace),
+                                  workspace.numel() * workspace.element_size(), _stream(stream)),
+           "paged_attn_decode")
+    return out
+
+
+def paged_attn_prefill(pool: KVPool, layer: int, q: torch.Tensor, cu_new_lens: torch.Tensor,
+                       reused_lens: torch.Tensor, max_new_len: int, block_tables: torch.Tensor,
+                       scale: float, out: torch.Tensor, k_new: Optional[torch.Tensor] = None,
+                       v_new: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """q/out: [T][Hq][D] bf16; cu_new_lens int32 [S+1]; reused_lens int32 [S]."""
+    _dev(q, "q", _BF16)
+    _dev(out, "out", _BF16)
+    _dev(cu_new_lens, "cu_new_lens", torch.int32)
+    _dev(reused_lens, "reused_lens", torch.int32)
+    _dev(block_tables, "block_tables", torch.int32)
+    if k_new is not None:
+        _dev(k_new, "k_new", _BF16)
+    if v_new is not None:
+        _dev(v_new, "v_new", _BF16)
+    s = reused_lens.shape[0]
+    _check(_lib.paged_attn_prefill(pool.handle, layer, s, q.shape[1], _ptr(q), _ptr(k_new),
+                                   _ptr(v_new), _ptr(cu_new_lens), _ptr(reused_lens), q.shape[0],
+                                   int(max_new_len), _ptr(block_tables), block_tables.shape[1],
+                                   float(scale), _ptr(out), _stream(stream)),
+           "paged_attn_prefill")
+    return out
+
+
+def _host_ids(ids):
+    if ids is None:
+        return None, None
+    arr = (ctypes.c_int32 * len(ids))(*[int(x) for x in ids])
+    return arr, ctypes.cast(arr, ctypes.c_void_p)
+
+
+def kv_blocks_stash(pool: KVPool, block_ids: torch.Tensor, staging: torch.Tensor,
+                    block_ids_host=None, stream=None) -> torch.Tensor:
+    """Copy every layer's slab of ``block_ids`` into ``staging`` (device or pinned host)."""
+    _dev(block_ids, "block_ids", torch.int32)
+    on_host = not staging.is_cuda
+    if on_host and not staging.is_pinned():
+        raise ValueError("host staging must be pinned memory")
+    keep, hp = _host_ids(block_ids_host)
+    _check(_lib.kv_blocks_stash(pool.handle, block_ids.numel(), _ptr(block_ids), hp,
+                                _ptr(staging), 1 if on_host else 0, _stream(stream)),
+           "kv_blocks_stash")
+    del keep
+    return staging
+
+
+def kv_blocks_restore(pool: KVPool, block_ids: torch.Tensor, staging: torch.Tensor,
+                      block_ids_host=None, stream=None):
+    """Copy ``staging`` (device or pinned host) back into pool blocks ``block_ids``."""
+    _dev(block_ids, "block_ids", torch.int32)
+    on_host = not staging.is_cuda
+    if on_host and not staging.is_pinned():
+        raise ValueError("host staging must be pinned memory")
+    keep, hp = _host_ids(block_ids_host)
+    _check(_lib.kv_blocks_restore(pool.handle, block_ids.numel(), _ptr(block_ids), hp,
+                                  _ptr(staging), 1 if on_host else 0, _stream(stream)),
+           "kv_blocks_restore")
+    del keep
+
+
+def ls_device_errors(stream=None) -> int:
+    """Wait for the stream, then read and clear the device error word."""
+    bits = ctypes.c_uint32()
+    _check(_lib.ls_device_errors(ctypes.byref(bits), _stream(stream)), "ls_device_errors")
+    return int(bits.value)
+
+
+def raw_library():
+    """The ctypes handle of the C library (tests call entry points through it)."""
+    return _lib

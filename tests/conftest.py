@@ -18,3 +18,12 @@ def oracle_lib():
     import oracle
     oracle.build(force=False)
     return oracle
+
+
+@pytest.fixture(scope="session")
+def built_lib():
+    """Path of libliveserve_kv.so, building it first if it is missing."""
+    from paper_2606_22983_amd import build as b
+    if not os.path.exists(b.LIB):
+        b.build(verbose=False)
+    return b.LIB

@@ -1,0 +1,75 @@
+"""Helpers shared by the GPU tests: upload seeded host arrays, compare with the
+oracle under the stated tolerance, and run the library entry points."""
+import math
+import sys
+
+import numpy as np
+import torch
+
+ATOL, RTOL, RMS_GATE = 2e-2, 1e-2, 5e-3
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def bf16_dev(a: np.ndarray) -> torch.Tensor:
+    """uint16 bf16 bit patterns -> device bf16 tensor (same bits)."""
+    t = torch.from_numpy(np.ascontiguousarray(a).view(np.int16))
+    return t.cuda().view(torch.bfloat16)
+
+
+def i32_dev(a) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
+
+
+def host_bits(t: torch.Tensor) -> np.ndarray:
+    return t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def assert_attn_close(gpu: torch.Tensor, ref: np.ndarray, what: str):
+    """Elementwise |gpu - ref| <= ATOL + RTOL*|ref| and RMS-relative error <= RMS_GATE."""
+    g = gpu.float().cpu().numpy().astype(np.float64).reshape(ref.shape)
+    assert np.isfinite(g).all(), "%s: non-finite GPU output" % what
+    err = np.abs(g - ref)
+    tol = ATOL + RTOL * np.abs(ref)
+    rms = math.sqrt(float(np.mean((g - ref) ** 2)))
+    rms_ref = math.sqrt(float(np.mean(ref ** 2))) or 1.0
+    log("%s: max|err| %.3e  max rel %.3e  rms-rel %.3e  (%d values)" % (
+        what, err.max(), (err / np.maximum(np.abs(ref), 1e-6)).max(), rms / rms_ref, ref.size))
+    bad = err > tol
+    assert not bad.any(), "%s: %d of %d values outside tolerance, worst err %.3e at %s" % (
+        what, int(bad.sum()), ref.size, err.max(), np.unravel_index(np.argmax(err - tol), err.shape))
+    assert rms / rms_ref <= RMS_GATE, "%s: rms-relative error %.3e > %.1e" % (what, rms / rms_ref,
+                                                                              RMS_GATE)
+
+
+class DevicePool:
+    """A pool uploaded to the GPU and wrapped by kv_pool_create."""
+
+    def __init__(self, kv_mod, pool_host: np.ndarray, head_dim: int, ring_blocks: int = 0):
+        nl, nb, _, hkv, _ = pool_host.shape
+        self.kv_mod = kv_mod
+        self.data = bf16_dev(pool_host)
+        self.ring = None
+        if ring_blocks:
+            per_block = nl * 2 * hkv * 16 * head_dim * 2
+            self.ring = torch.empty(ring_blocks * per_block, dtype=torch.uint8, device="cuda")
+        self.pool = kv_mod.kv_pool_create(self.data, nl, nb, hkv, head_dim, 16, self.ring)
+        self.shape = pool_host.shape
+
+    def host(self) -> np.ndarray:
+        torch.cuda.synchronize()
+        return host_bits(self.data).reshape(self.shape)
+
+
+def run_decode(kv_mod, dp: DevicePool, q, tables, lens, scale, k_new=None, v_new=None,
+               layer=0, workspace=None):
+    s, hq, d = q.shape
+    out = torch.empty((s, hq, d), dtype=torch.bfloat16, device="cuda")
+    if workspace is None:
+        nbytes = kv_mod.decode_workspace_bytes(dp.pool, s, hq, tables.shape[1])
+        workspace = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
+    kv_mod.paged_attn_decode(dp.pool, layer, q, tables, lens, scale, out, workspace, k_new, v_new)
+    return out, workspace

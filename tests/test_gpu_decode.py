@@ -1,0 +1,162 @@
+"""GPU parity of paged_attn_decode (through the C ABI) against the CPU oracle."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2606_22983_amd import workloads as W
+from tests.gpu_util import (DevicePool, assert_attn_close, bf16_dev, host_bits, i32_dev, log,
+                            run_decode)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def kv():
+    from paper_2606_22983_amd import kv as kv_mod
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return kv_mod
+
+
+def _decode_case(kv, oracle_lib, case, step=0, append=False, label=""):
+    dp = DevicePool(kv, case.pool.data, case.pool.head_dim)
+    lens = case.lens_at(step)
+    q = bf16_dev(case.q[step])
+    tables = i32_dev(case.block_tables)
+    kn = bf16_dev(case.k_new[step]) if append else None
+    vn = bf16_dev(case.v_new[step]) if append else None
+    out, _ = run_decode(kv, dp, q, tables, i32_dev(lens), case.scale, kn, vn)
+    ref, ref_pool = oracle_lib.decode(case.pool.data, 16, case.pool.head_dim, 0, case.q[step],
+                                      case.block_tables, lens, case.scale,
+                                      k_new=case.k_new[step] if append else None,
+                                      v_new=case.v_new[step] if append else None, pool_out=True)
+    assert_attn_close(out, ref, label or case.name)
+    if append:
+        assert np.array_equal(dp.host(), ref_pool), "appended pool differs from the oracle's"
+    assert kv.ls_device_errors() == 0
+    return out
+
+
+@pytest.mark.parametrize("append", [False, True])
+def test_tiny_decode(kv, oracle_lib, append):
+    _decode_case(kv, oracle_lib, W.tiny_decode(append=append), append=append,
+                 label="tiny decode append=%s" % append)
+
+
+def _synthetic(rng, lens, hq, hkv, d, append, spare=5):
+    """Random paged case with given lengths (block ids shuffled, tails NaN)."""
+    lens = np.asarray(lens, dtype=np.int64)
+    final = lens + (1 if append else 0)
+    need = np.maximum((final + 15) // 16, 1)
+    nb = int(need.sum()) + spare
+    perm = rng.permutation(nb).astype(np.int32)
+    tables = np.full((len(lens), int(need.max())), -1, np.int32)
+    pos = 0
+    for s, k in enumerate(need):
+        tables[s, :k] = perm[pos:pos + k]
+        pos += k
+    pool = W.normal_bf16(rng, (1, nb, 2, hkv, 16 * d))
+    W._poison(pool, d, tables, lens, int(need.sum()))
+    q = W.normal_bf16(rng, (len(lens), hq, d))
+    kn = W.normal_bf16(rng, (len(lens), hkv, d)) if append else None
+    vn = W.normal_bf16(rng, (len(lens), hkv, d)) if append else None
+    return pool, tables, q, kn, vn
+
+
+@pytest.mark.parametrize("d,hq,hkv", [(128, 32, 4), (128, 16, 2), (64, 8, 2), (128, 8, 8),
+                                      (64, 4, 2), (128, 4, 4)])
+@pytest.mark.parametrize("append", [False, True])
+def test_decode_lengths_and_groups(kv, oracle_lib, d, hq, hkv, append):
+    """Ragged lengths around block and split boundaries, every supported group size."""
+    rng = np.random.default_rng(hq * 7 + d + append)
+    lens = [1, 2, 15, 16, 17, 63, 64, 65, 127, 128, 129, 255, 256, 257, 511, 512, 513, 1023, 1024,
+            1025, 2047, 3001]
+    if append:
+        lens = [0] + lens
+    pool, tables, q, kn, vn = _synthetic(rng, lens, hq, hkv, d, append)
+    dp = DevicePool(kv, pool, d)
+    out, _ = run_decode(kv, dp, bf16_dev(q), i32_dev(tables), i32_dev(lens), 1 / math.sqrt(d),
+                        None if kn is None else bf16_dev(kn), None if vn is None else bf16_dev(vn))
+    ref, ref_pool = oracle_lib.decode(pool, 16, d, 0, q, tables, np.array(lens), 1 / math.sqrt(d),
+                                      k_new=kn, v_new=vn, pool_out=True)
+    assert_attn_close(out, ref, "decode D=%d G=%d append=%s" % (d, hq // hkv, append))
+    if append:
+        assert np.array_equal(dp.host(), ref_pool)
+    assert kv.ls_device_errors() == 0
+
+
+def test_one_key_returns_v_bit_exactly(kv):
+    rng = np.random.default_rng(3)
+    pool, tables, q, _, _ = _synthetic(rng, [1, 1, 1, 1], 32, 4, 128, False)
+    dp = DevicePool(kv, pool, 128)
+    out, _ = run_decode(kv, dp, bf16_dev(q), i32_dev(tables), i32_dev([1] * 4), 0.0884)
+    got = host_bits(out)
+    for s in range(4):
+        vt = pool[0, tables[s, 0], 1].reshape(4, 128, 16)[:, :, 0]     # V of token 0, per KV head
+        for h in range(32):
+            assert np.array_equal(got[s, h], vt[h // 8]), (s, h)
+
+
+def test_thinker_decode_full(kv, oracle_lib):
+    case = W.thinker_decode()
+    log("thinker decode: %d sessions, %d tokens, pool %.2f GB" % (
+        case.num_sessions, int(case.context_lens.sum()), case.pool.nbytes / 1e9))
+    _decode_case(kv, oracle_lib, case, label="thinker decode (64 sessions, full)")
+
+
+def test_talker_decode_32_steps(kv, oracle_lib):
+    case = W.talker_decode()
+    log("talker decode: %d sessions, %d steps, pool %.2f GB" % (
+        case.num_sessions, case.steps, case.pool.nbytes / 1e9))
+    dp = DevicePool(kv, case.pool.data, 128)
+    tables = i32_dev(case.block_tables)
+    ws = None
+    ref_pool = case.pool.data.copy()
+    checked = {0, 1, 15, 16, 31}
+    for t in range(case.steps):
+        lens = case.lens_at(t)
+        out, ws = run_decode(kv, dp, bf16_dev(case.q[t]), tables, i32_dev(lens), case.scale,
+                             bf16_dev(case.k_new[t]), bf16_dev(case.v_new[t]), workspace=ws)
+        if t in checked:
+            ref, ref_pool = oracle_lib.decode(ref_pool, 16, 128, 0, case.q[t], case.block_tables,
+                                              lens, case.scale, k_new=case.k_new[t],
+                                              v_new=case.v_new[t], pool_out=True)
+            assert_attn_close(out, ref, "talker step %d" % t)
+        else:
+            oracle_lib.append(ref_pool, 16, 128, 0, case.block_tables,
+                              np.arange(case.num_sessions), lens, case.k_new[t], case.v_new[t])
+    assert np.array_equal(dp.host(), ref_pool), "pool after 32 appends differs"
+    assert kv.ls_device_errors() == 0
+
+
+def test_decode_bitwise_deterministic_and_block_permutation_invariant(kv):
+    case = W.tiny_decode()
+    pool = case.pool.data
+    dp = DevicePool(kv, pool, 64)
+    q = bf16_dev(case.q[0])
+    lens = i32_dev(case.context_lens)
+    a, ws = run_decode(kv, dp, q, i32_dev(case.block_tables), lens, case.scale)
+    b, _ = run_decode(kv, dp, q, i32_dev(case.block_tables), lens, case.scale, workspace=ws)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    rng = np.random.default_rng(9)
+    sigma = rng.permutation(pool.shape[1])
+    moved = np.empty_like(pool)
+    moved[:, sigma] = pool
+    tables = np.where(case.block_tables >= 0, sigma[np.maximum(case.block_tables, 0)], -1)
+    dp2 = DevicePool(kv, moved, 64)
+    c, _ = run_decode(kv, dp2, q, i32_dev(tables), lens, case.scale)
+    assert torch.equal(a.view(torch.int16), c.view(torch.int16))
+
+
+def test_out_of_range_block_id_is_flagged_not_read(kv):
+    rng = np.random.default_rng(4)
+    pool, tables, q, _, _ = _synthetic(rng, [100, 40], 8, 2, 64, False)
+    bad = tables.copy()
+    bad[0, 2] = pool.shape[1] + 1000          # outside the pool
+    bad[1, 0] = -7
+    dp = DevicePool(kv, pool, 64)
+    kv.ls_device_errors()
+    out, _ = run_decode(kv, dp, bf16_dev(q), i32_dev(bad), i32_dev([100, 40]), 0.125)
+    assert kv.ls_device_errors() & kv.LS_DEVERR_BLOCK_ID
+    torch.cuda.synchronize()

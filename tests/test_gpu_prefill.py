@@ -1,0 +1,104 @@
+"""GPU parity of paged_attn_prefill (next-turn prefill over reused context)."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2606_22983_amd import workloads as W
+from tests.gpu_util import DevicePool, assert_attn_close, bf16_dev, i32_dev, log
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def kv():
+    from paper_2606_22983_amd import kv as kv_mod
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return kv_mod
+
+
+def _case(rng, n, c, hq, hkv, d, spare=3):
+    n = np.asarray(n, np.int64)
+    c = np.asarray(c, np.int64)
+    need = (c + n + 15) // 16
+    nb = int(need.sum()) + spare
+    perm = rng.permutation(nb).astype(np.int32)
+    tables = np.full((len(n), int(need.max())), -1, np.int32)
+    pos = 0
+    for s, k in enumerate(need):
+        tables[s, :k] = perm[pos:pos + k]
+        pos += k
+    pool = W.normal_bf16(rng, (1, nb, 2, hkv, 16 * d))
+    W._poison(pool, d, tables, c, int(need.sum()))
+    total = int(n.sum())
+    q = W.normal_bf16(rng, (total, hq, d))
+    kn = W.normal_bf16(rng, (total, hkv, d))
+    vn = W.normal_bf16(rng, (total, hkv, d))
+    return pool, tables, q, kn, vn
+
+
+def _run(kv, dp, q, kn, vn, n, c, tables, scale):
+    cu = np.concatenate([[0], np.cumsum(n)]).astype(np.int32)
+    out = torch.empty((q.shape[0], q.shape[1], q.shape[2]), dtype=torch.bfloat16, device="cuda")
+    kv.paged_attn_prefill(dp.pool, 0, bf16_dev(q), i32_dev(cu), i32_dev(c), int(np.max(n)),
+                          i32_dev(tables), scale, out, bf16_dev(kn), bf16_dev(vn))
+    return out, cu
+
+
+@pytest.mark.parametrize("d,hq,hkv", [(128, 32, 4), (64, 8, 2), (128, 8, 8), (128, 16, 8),
+                                      (64, 4, 1)])
+def test_prefill_ragged(kv, oracle_lib, d, hq, hkv):
+    """Turn lengths and contexts around tile and block boundaries, c = 0 included."""
+    rng = np.random.default_rng(d + hq * 3 + hkv)
+    n = [1, 17, 16, 130, 37, 255, 64]
+    c = [0, 5, 300, 0, 1000, 77, 16]
+    pool, tables, q, kn, vn = _case(rng, n, c, hq, hkv, d)
+    dp = DevicePool(kv, pool, d)
+    out, cu = _run(kv, dp, q, kn, vn, np.array(n), np.array(c), tables, 1 / math.sqrt(d))
+    ref, ref_pool = oracle_lib.prefill(pool, 16, d, 0, q, kn, vn, cu, c, tables, 1 / math.sqrt(d),
+                                       pool_out=True)
+    assert_attn_close(out, ref, "prefill D=%d G=%d" % (d, hq // hkv))
+    assert np.array_equal(dp.host(), ref_pool), "appended pool differs from the oracle's"
+    assert kv.ls_device_errors() == 0
+
+
+def test_prefill_chunked_equals_whole_turn(kv):
+    """Two chunks (c advanced by the first) give the same rows as one call."""
+    rng = np.random.default_rng(12)
+    d, hq, hkv = 128, 32, 4
+    n, c, n1 = 300, 517, 133
+    pool, tables, q, kn, vn = _case(rng, [n], [c], hq, hkv, d)
+    dp1 = DevicePool(kv, pool, d)
+    whole, _ = _run(kv, dp1, q, kn, vn, np.array([n]), np.array([c]), tables, 0.0884)
+    dp2 = DevicePool(kv, pool, d)
+    a, _ = _run(kv, dp2, q[:n1], kn[:n1], vn[:n1], np.array([n1]), np.array([c]), tables, 0.0884)
+    b, _ = _run(kv, dp2, q[n1:], kn[n1:], vn[n1:], np.array([n - n1]), np.array([c + n1]), tables,
+                0.0884)
+    assert torch.equal(torch.cat([a, b]).view(torch.int16), whole.view(torch.int16))
+    assert np.array_equal(dp1.host(), dp2.host())
+
+
+def test_next_turn_prefill_full_sampled(kv, oracle_lib):
+    case = W.next_turn_prefill()
+    n = case.new_lens.astype(np.int64)
+    log("next-turn prefill: %d sessions, %d new tokens, %d reused, pool %.2f GB" % (
+        case.num_sessions, int(n.sum()), int(case.reused_lens.sum()), case.pool.nbytes / 1e9))
+    dp = DevicePool(kv, case.pool.data, 128)
+    out, cu = _run(kv, dp, case.q, case.k_new, case.v_new, n, case.reused_lens, case.block_tables,
+                   case.scale)
+    torch.cuda.synchronize()
+    # Sampled rows: first and last token of every session, tile edges of session 0,
+    # and random rows.
+    rng = np.random.default_rng(33)
+    rows = set()
+    for s in range(case.num_sessions):
+        rows.update([int(cu[s]), int(cu[s + 1] - 1)])
+    rows.update(int(cu[0]) + j for j in (15, 16, 17, 127, 128))
+    rows.update(rng.integers(0, int(cu[-1]), size=40).tolist())
+    rows = np.array(sorted(rows))
+    ref = oracle_lib.prefill(case.pool.data, 16, 128, 0, case.q, case.k_new, case.v_new, cu,
+                             case.reused_lens, case.block_tables, case.scale, rows=rows)
+    assert_attn_close(out[torch.from_numpy(rows).cuda()], ref,
+                      "next-turn prefill (%d sampled rows)" % len(rows))
+    assert kv.ls_device_errors() == 0
