@@ -1,0 +1,430 @@
+#!/usr/bin/env python3
+"""Benchmark of the paged-KV hot path on one MI355X.
+
+Headline (the JSON line's ``value``): thinker-shaped batched decode — 64
+sessions, lognormal context lengths (median 4096, clipped to [512, 16384]),
+32 query / 4 KV heads, head_dim 128, 16-token blocks in a shuffled pool —
+reported as algorithmic KV bytes per second (GB/s) against the 8 TB/s HBM peak.
+
+Alongside it (``legs``): next-turn chunked prefill (32 sessions, TFLOP/s vs the
+2.5 PFLOP/s dense bf16 MFMA peak), 32-step talker decode with append (GB/s),
+and the KV-block restore/stash scatter legs (48 layers x 4 KV heads x 128 dims,
+128 sessions x 8192 tokens = 96 GiB) alone and overlapped with decode on a
+side stream.  Inputs are seeded synthetic sessions, resident in HBM before the
+timed region starts.  ``cpu_baseline`` is the CPU oracle timed on this host.
+
+Usage: python bench.py [--steps K] [--warmup W] [--legs decode,prefill,talker,restore]
+"""
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+PCIE_PEAK_GBS = 64.0
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--legs", default="decode,prefill,talker,restore")
+    ap.add_argument("--prefill-reps", type=int, default=5)
+    ap.add_argument("--restore-reps", type=int, default=5)
+    ap.add_argument("--restore-sessions", type=int, default=128)
+    ap.add_argument("--host-leg-gib", type=float, default=4.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def source_digest(*names):
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2606_22983_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel_key, digest):
+    """HBM bytes per launch from committed rocprofv3 PMC runs, if they were taken
+    on the current kernel source (else None)."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        table = json.load(f)
+    e = table.get(kernel_key)
+    if not e or e.get("source_digest") != digest:
+        return None
+    return e.get("hbm_bytes_per_launch")
+
+
+class Timer:
+    """HIP events recorded on the stream the library launches on."""
+
+    def __init__(self, torch, stream):
+        self.torch = torch
+        self.stream = stream
+        self.pairs = []
+
+    def start(self):
+        e = self.torch.cuda.Event(enable_timing=True)
+        e.record(self.stream)
+        return e
+
+    def stop(self, s):
+        e = self.torch.cuda.Event(enable_timing=True)
+        e.record(self.stream)
+        self.pairs.append((s, e))
+
+    def mean_ms(self):
+        return float(np.mean([a.elapsed_time(b) for a, b in self.pairs]))
+
+
+def dev16(torch, a):
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda().view(torch.bfloat16)
+
+
+def dev32(torch, a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
+
+
+# ---------------------------------------------------------------------------
+def decode_leg(torch, kv, W, args):
+    case = W.thinker_decode()
+    hkv, d, hq = case.pool.num_kv_heads, case.pool.head_dim, case.num_q_heads
+    lens = case.context_lens.astype(np.int64)
+    kv_bytes = int(lens.sum()) * hkv * d * 2 * 2
+    io_bytes = 2 * case.num_sessions * hq * d * 2
+    alg_bytes = kv_bytes + io_bytes
+    log("decode: %d sessions, %d tokens, %.1f MB algorithmic per step" % (
+        case.num_sessions, int(lens.sum()), alg_bytes / 1e6))
+    # Three copies of the pool (each ~0.9 GB) rotate so that consecutive steps
+    # cannot be served from the 256 MB Infinity Cache.
+    base = dev16(torch, case.pool.data)
+    copies = [base] + [base.clone() for _ in range(2)]
+    pools = [kv.kv_pool_create(t, 1, case.pool.num_blocks, hkv, d) for t in copies]
+    q = dev16(torch, case.q[0])
+    tables = dev32(torch, case.block_tables)
+    lens_d = dev32(torch, case.context_lens)
+    out = torch.empty((case.num_sessions, hq, d), dtype=torch.bfloat16, device="cuda")
+    ws = torch.zeros(kv.decode_workspace_bytes(pools[0], case.num_sessions, hq,
+                                               case.block_tables.shape[1]),
+                     dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    for i in range(args.warmup):
+        kv.paged_attn_decode(pools[i % 3], 0, q, tables, lens_d, case.scale, out, ws)
+    timer = Timer(torch, stream)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        e = timer.start()
+        kv.paged_attn_decode(pools[i % 3], 0, q, tables, lens_d, case.scale, out, ws)
+        timer.stop(e)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    assert kv.ls_device_errors() == 0
+    kernel_ms = timer.mean_ms()
+    res = dict(case=case, pools=pools, copies=copies, q=q, tables=tables, lens=lens_d, out=out,
+               ws=ws, alg_bytes=alg_bytes, kv_bytes=kv_bytes, wall_s=wall, kernel_ms=kernel_ms,
+               ms_per_step=wall * 1e3 / args.steps)
+    log("decode: %.1f us/step wall, %.1f us/launch (events), %.0f GB/s" % (
+        res["ms_per_step"] * 1e3, kernel_ms * 1e3, alg_bytes / (kernel_ms * 1e-3) / 1e9))
+    return res
+
+
+def cpu_baseline(dec, W):
+    import oracle
+    case = dec["case"]
+    threads = oracle.num_threads()
+    os.environ.setdefault("OMP_NUM_THREADS", str(threads))
+    total, reps = 0.0, 0
+    while reps < 5 and (total < 10.0 or reps == 0):
+        _, t = oracle.timed(oracle.decode, case.pool.data, 16, case.pool.head_dim, 0, case.q[0],
+                            case.block_tables, case.context_lens, case.scale)
+        total += t
+        reps += 1
+    per = total / reps
+    log("cpu oracle: %.2f s per decode step on %d threads (%d reps)" % (per, threads, reps))
+    return {"value": round(dec["alg_bytes"] / per / 1e9, 4), "unit": "GB/s", "cores": threads,
+            "kind": "oracle",
+            "sample": "full thinker-shaped decode step (64 sessions, %d tokens), fp64, %d rep(s), "
+                      "%.2f s each" % (int(case.context_lens.sum()), reps, per)}
+
+
+def prefill_leg(torch, kv, W, args):
+    case = W.next_turn_prefill()
+    n = case.new_lens.astype(np.int64)
+    c = case.reused_lens.astype(np.int64)
+    hq, d = case.num_q_heads, case.pool.head_dim
+    flops = 4.0 * d * hq * float(np.sum(n * c + n * (n + 1) / 2))
+    log("prefill: %d sessions, %d new tokens, %d reused, %.2f TFLOP" % (
+        case.num_sessions, int(n.sum()), int(c.sum()), flops / 1e12))
+    pool_t = dev16(torch, case.pool.data)
+    pool = kv.kv_pool_create(pool_t, 1, case.pool.num_blocks, case.pool.num_kv_heads, d)
+    q = dev16(torch, case.q)
+    kn, vn = dev16(torch, case.k_new), dev16(torch, case.v_new)
+    cu = dev32(torch, case.cu_new_lens)
+    ctx = dev32(torch, case.reused_lens)
+    tables = dev32(torch, case.block_tables)
+    out = torch.empty(q.shape, dtype=torch.bfloat16, device="cuda")
+    maxn = int(n.max())
+    # The first call appends the turn's K/V; timed calls run attention only.
+    kv.paged_attn_prefill(pool, 0, q, cu, ctx, maxn, tables, case.scale, out, kn, vn)
+    kv.paged_attn_prefill(pool, 0, q, cu, ctx, maxn, tables, case.scale, out)
+    timer = Timer(torch, torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.prefill_reps):
+        e = timer.start()
+        kv.paged_attn_prefill(pool, 0, q, cu, ctx, maxn, tables, case.scale, out)
+        timer.stop(e)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    assert kv.ls_device_errors() == 0
+    ms = timer.mean_ms()
+    tflops = flops / (ms * 1e-3) / 1e12
+    log("prefill: %.2f ms/launch, %.1f TFLOP/s" % (ms, tflops))
+    return {"workload": "next-turn prefill: 32 sessions, n~U[256,2048] new tokens over "
+                        "c~U[2048,32768] reused context, 32/4 heads, D=128, bf16, fp32 accumulate",
+            "tflop": round(flops / 1e12, 4), "ms_per_launch": round(ms, 4),
+            "wall_ms_per_launch": round(wall * 1e3 / args.prefill_reps, 4),
+            "value": round(tflops, 2), "unit": "TFLOP/s",
+            "roofline": {"bound": "mfma", "achieved": round(tflops, 2),
+                         "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                         "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+                         "traffic": measured_traffic("prefill", source_digest("prefill.hip"))}}
+
+
+def talker_leg(torch, kv, W, args):
+    case = W.talker_decode()
+    hkv, d, hq, S = case.pool.num_kv_heads, case.pool.head_dim, case.num_q_heads, case.num_sessions
+    step_bytes = [int((case.context_lens.astype(np.int64) + t + 1).sum()) * hkv * d * 4 +
+                  2 * S * hkv * d * 2 + 2 * S * hq * d * 2 for t in range(case.steps)]
+    total_bytes = float(sum(step_bytes))
+    pool_t = dev16(torch, case.pool.data)
+    pool = kv.kv_pool_create(pool_t, 1, case.pool.num_blocks, hkv, d)
+    tables = dev32(torch, case.block_tables)
+    qs = [dev16(torch, case.q[t]) for t in range(case.steps)]
+    kns = [dev16(torch, case.k_new[t]) for t in range(case.steps)]
+    vns = [dev16(torch, case.v_new[t]) for t in range(case.steps)]
+    lens = [dev32(torch, case.lens_at(t)) for t in range(case.steps)]
+    out = torch.empty((S, hq, d), dtype=torch.bfloat16, device="cuda")
+    ws = torch.zeros(kv.decode_workspace_bytes(pool, S, hq, case.block_tables.shape[1]),
+                     dtype=torch.uint8, device="cuda")
+
+    def run32():
+        for t in range(case.steps):
+            kv.paged_attn_decode(pool, 0, qs[t], tables, lens[t], case.scale, out, ws, kns[t],
+                                 vns[t])
+
+    run32()
+    timer = Timer(torch, torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    reps = 3
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        e = timer.start()
+        run32()
+        timer.stop(e)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    assert kv.ls_device_errors() == 0
+    ms32 = timer.mean_ms()
+    gbs = total_bytes / (ms32 * 1e-3) / 1e9
+    log("talker: %.1f us/step, %.0f GB/s" % (ms32 * 1e3 / case.steps, gbs))
+    return {"workload": "talker-shaped decode: 256 sessions, L0~U[512,4096], 16/2 heads, D=128, "
+                        "32 consecutive steps appending one token per session",
+            "us_per_step": round(ms32 * 1e3 / case.steps, 2),
+            "wall_us_per_step": round(wall * 1e6 / (reps * case.steps), 2),
+            "mb_per_step": round(total_bytes / case.steps / 1e6, 1),
+            "value": round(gbs, 1), "unit": "GB/s", "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)}
+
+
+def restore_leg(torch, kv, W, args, dec):
+    rc = W.restore_case(num_sessions=args.restore_sessions)
+    nl, hkv, d, nb = rc.num_layers, rc.num_kv_heads, rc.head_dim, rc.num_blocks
+    n = len(rc.stash_ids)
+    per_block = nl * rc.slab_bytes
+    payload = n * per_block
+    log("restore: %d blocks x %d layers, payload %.1f GiB; pool and staging on device" % (
+        n, nl, payload / 2 ** 30))
+    pool_t = torch.empty(nl * nb * 2 * hkv * 16 * d, dtype=torch.int16, device="cuda")
+    staging = torch.empty(n * nl * 2 * hkv * 16 * d, dtype=torch.int16, device="cuda")
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(rc.seed)
+    pool_t.random_(-32768, 32767, generator=gen)
+    ring = torch.empty(128 * per_block, dtype=torch.uint8, device="cuda")
+    pool = kv.kv_pool_create(pool_t, nl, nb, hkv, d, 16, ring)
+    a = dev32(torch, rc.stash_ids)
+    b = dev32(torch, rc.restore_ids)
+    stream = torch.cuda.current_stream()
+
+    # stash A (gather) and check sampled slabs against the oracle's byte copy
+    kv.kv_blocks_stash(pool, a, staging)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(rc.seed)
+    sample = rng.choice(n, size=16, replace=False)
+    pview = pool_t.view(nl, nb, -1)
+    sview = staging.view(n, nl, -1)
+    for i in sample:
+        assert torch.equal(sview[i], pview[:, int(rc.stash_ids[i])]), "stash sample %d" % i
+
+    def timed(fn, reps):
+        timer = Timer(torch, stream)
+        for _ in range(reps):
+            e = timer.start()
+            fn()
+            timer.stop(e)
+        torch.cuda.synchronize()
+        return timer.mean_ms()
+
+    stash_ms = timed(lambda: kv.kv_blocks_stash(pool, a, staging), args.restore_reps)
+    restore_ms = timed(lambda: kv.kv_blocks_restore(pool, b, staging), args.restore_reps)
+    for i in sample:
+        assert torch.equal(pview[:, int(rc.restore_ids[i])], sview[i]), "restore sample %d" % i
+    assert kv.ls_device_errors() == 0
+    scatter_gbs = 2.0 * payload / (restore_ms * 1e-3) / 1e9
+    gather_gbs = 2.0 * payload / (stash_ms * 1e-3) / 1e9
+    log("restore scatter: %.2f ms, %.0f GB/s (2N); stash gather: %.2f ms, %.0f GB/s" % (
+        restore_ms, scatter_gbs, stash_ms, gather_gbs))
+
+    # restore on a side stream while the thinker decode repeats on the main stream
+    side = torch.cuda.Stream()
+    dec_alone_ms = dec["kernel_ms"]
+    n_dec = 0
+    dtimer = Timer(torch, stream)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev_side_start = torch.cuda.Event(enable_timing=True)
+    ev_side_end = torch.cuda.Event(enable_timing=True)
+    ev_side_start.record(side)
+    with torch.cuda.stream(side):
+        kv.kv_blocks_restore(pool, b, staging, stream=side)
+    ev_side_end.record(side)
+    while not ev_side_end.query() and n_dec < 2000:
+        e = dtimer.start()
+        kv.paged_attn_decode(dec["pools"][n_dec % 3], 0, dec["q"], dec["tables"], dec["lens"],
+                             dec["case"].scale, dec["out"], dec["ws"])
+        dtimer.stop(e)
+        n_dec += 1
+        if n_dec % 16 == 0:
+            stream.synchronize()
+    torch.cuda.synchronize()
+    makespan = time.perf_counter() - t0
+    side_ms = ev_side_start.elapsed_time(ev_side_end)
+    dec_conc_ms = dtimer.mean_ms() if n_dec else float("nan")
+    agg = (2.0 * payload + n_dec * dec["alg_bytes"]) / makespan / 1e9
+    log("overlap: restore %.2f ms on the side stream, %d decode steps at %.1f us (alone %.1f us)" % (
+        side_ms, n_dec, dec_conc_ms * 1e3, dec_alone_ms * 1e3))
+
+    # host leg: pinned host staging -> device ring -> scatter, through the same call
+    host = {}
+    hb = min(n, int(args.host_leg_gib * 2 ** 30 // per_block))
+    if hb > 0:
+        hbuf = torch.empty(hb * per_block // 2, dtype=torch.int16, pin_memory=True)
+        ids_h = b[:hb]
+        kv.kv_blocks_stash(pool, ids_h, hbuf)
+        torch.cuda.synchronize()
+        h2d = timed(lambda: kv.kv_blocks_restore(pool, ids_h, hbuf), 2)
+        d2h = timed(lambda: kv.kv_blocks_stash(pool, ids_h, hbuf), 2)
+        host = {"blocks": hb, "gib": round(hb * per_block / 2 ** 30, 2),
+                "restore_gbs": round(hb * per_block / (h2d * 1e-3) / 1e9, 2),
+                "stash_gbs": round(hb * per_block / (d2h * 1e-3) / 1e9, 2),
+                "pcie_peak_gbs": PCIE_PEAK_GBS}
+        log("host leg: restore %.1f GB/s, stash %.1f GB/s over %.1f GiB" % (
+            host["restore_gbs"], host["stash_gbs"], host["gib"]))
+        del hbuf
+    assert kv.ls_device_errors() == 0
+    del pool_t, staging, ring
+    torch.cuda.empty_cache()
+    return {"workload": "KV restore/stash: 48 layers x 4 KV heads x D=128 bf16, %d sessions x 8192 "
+                        "tokens = %d blocks (%.1f GiB), device staging -> scattered pool slots" % (
+                            args.restore_sessions, n, payload / 2 ** 30),
+            "payload_gib": round(payload / 2 ** 30, 2),
+            "restore_ms": round(restore_ms, 3), "value": round(scatter_gbs, 1), "unit": "GB/s",
+            "frac_hbm_peak": round(scatter_gbs / HBM_PEAK_GBS, 4),
+            "stash_ms": round(stash_ms, 3), "stash_gbs": round(gather_gbs, 1),
+            "roofline": {"bound": "hbm", "achieved": round(scatter_gbs, 1), "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": round(scatter_gbs / HBM_PEAK_GBS, 4),
+                         "traffic": measured_traffic("block_copy", source_digest("blockcopy.hip"))},
+            "overlap": {"restore_side_stream_ms": round(side_ms, 3), "decode_steps": n_dec,
+                        "decode_us_alone": round(dec_alone_ms * 1e3, 2),
+                        "decode_us_concurrent": round(dec_conc_ms * 1e3, 2),
+                        "decode_slowdown_pct": round(100 * (dec_conc_ms / dec_alone_ms - 1), 1),
+                        "aggregate_gbs": round(agg, 1)},
+            "host_leg": host}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (sessions would be "
+              "sharded across GPUs with no exchange inside attention); run with --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2606_22983_amd import kv
+    from paper_2606_22983_amd import workloads as W
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    legs = set(args.legs.split(","))
+    log("device:", torch.cuda.get_device_name(0), "| library:", kv.version())
+
+    dec = decode_leg(torch, kv, W, args)
+    dec_gbs = dec["alg_bytes"] / (dec["kernel_ms"] * 1e-3) / 1e9
+    wall_gbs = dec["alg_bytes"] * args.steps / dec["wall_s"] / 1e9
+    extra = {}
+    if "prefill" in legs:
+        extra["prefill"] = prefill_leg(torch, kv, W, args)
+        torch.cuda.empty_cache()
+    if "talker" in legs:
+        extra["talker"] = talker_leg(torch, kv, W, args)
+        torch.cuda.empty_cache()
+    if "restore" in legs:
+        extra["restore"] = restore_leg(torch, kv, W, args, dec)
+    cpu = None if args.no_cpu_baseline else cpu_baseline(dec, W)
+
+    line = {
+        "metric": "paged decode KV GB/s (% HBM peak); prefill TFLOP/s; restore GB/s on 1 MI355X",
+        "value": round(wall_gbs, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(dec["ms_per_step"], 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded multi-turn speech sessions; see workloads.py)",
+        "config": {"workload": "thinker-shaped batched decode: 64 sessions, lognormal context "
+                               "(median 4096, sigma 1, clipped [512,16384]), 32/4 heads GQA, "
+                               "head_dim 128, 16-token blocks, shuffled pool 1.25x",
+                   "sessions": 64, "tokens": int(dec["case"].context_lens.sum()),
+                   "algorithmic_mb_per_step": round(dec["alg_bytes"] / 1e6, 2)},
+        "roofline": {"bound": "hbm", "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic("decode", source_digest("decode.hip"))},
+        "cpu_baseline": cpu,
+        "legs": extra,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -104,10 +104,10 @@ ls_status kv_pool_create(const ls_kv_pool_desc *desc, ls_kv_pool **out);
 ls_status kv_pool_destroy(ls_kv_pool *pool);
 
 /*
- * Workspace bytes paged_attn_decode needs for this shape (split-K partial
- * results and per-(session, KV head) arrival counters).  The workspace must be
- * zero-filled once before its first use; every completed decode call leaves
- * its counters at zero again, so it can be reused without clearing.
+ * Workspace bytes paged_attn_decode needs for this shape: the split-K partial
+ * results (running max, running sum and unnormalised output per split, fp32).
+ * No initialisation is needed; calls on one stream may reuse the same
+ * workspace, concurrent calls need their own.  Returns 0 for invalid arguments.
  */
 size_t ls_decode_workspace_bytes(const ls_kv_pool *pool, int32_t num_sessions,
                                  int32_t num_q_heads, int32_t max_blocks_per_session);
@@ -130,7 +130,7 @@ size_t ls_decode_workspace_bytes(const ls_kv_pool *pool, int32_t num_sessions,
  *   out            device bf16 [num_sessions][num_q_heads][head_dim]:
  *                  out = softmax(scale * q K^T) V over the session's keys, per query
  *                  head h using KV head h / (num_q_heads / num_kv_heads)
- *   workspace      device, >= ls_decode_workspace_bytes(...), zero-filled before first use
+ *   workspace      device, >= ls_decode_workspace_bytes(...) bytes
  *
  * Supported: num_q_heads / num_kv_heads in {1, 2, 4, 8}.  Errors: LS_EINVAL
  * (NULL pointer, layer out of range, num_q_heads not a multiple of num_kv_heads,

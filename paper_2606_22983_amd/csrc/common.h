@@ -41,10 +41,9 @@ unsigned int *device_error_word();
 struct DecodePlan {
     int split_tokens;               // tokens per split (multiple of 64)
     int max_splits;                 // splits of the longest possible session
-    size_t counters_bytes;          // int32 [S][Hkv], padded
     size_t ml_bytes;                // fp32 [S][Hkv][max_splits][G][2]
     size_t acc_bytes;               // fp32 [S][Hkv][max_splits][G][D]
-    size_t total() const { return counters_bytes + ml_bytes + acc_bytes; }
+    size_t total() const { return ml_bytes + acc_bytes; }
 };
 DecodePlan plan_decode(const PoolGeom &p, int32_t num_sessions, int32_t num_q_heads,
                        int32_t max_blocks_per_session);

@@ -25,8 +25,10 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kPreThreads = 256;
+constexpr int kBufferDword3P = 0x00020000;   // raw buffer, 32-bit data format
 constexpr int kPreRows = 128;            // query rows per workgroup
 constexpr int kKeyTile = 64;             // keys per staged tile (4 blocks)
 constexpr float kLog2eP = 1.4426950408889634f;
@@ -58,78 +60,77 @@ __device__ __forceinline__ float xsum16_32(float x) {
 template <int D>
 struct TileRegs {
     static constexpr int kChunks = (2 * kKeyTile * D * 2) / (16 * kPreThreads);  // 16-byte chunks per thread
-    uint4 c[kChunks];
+    u32x4 c[kChunks];
 };
 
-// Load one key tile (K then V of 4 blocks) into registers.  Chunks of blocks
-// beyond the session's keys, and slots at or past its last key, become zero.
+// Issue the loads of one key tile (K then V of 4 blocks) into registers.  Blocks
+// past the session's keys (or with an id outside the pool) are read through a
+// zero-size buffer descriptor: no memory traffic, zeros returned.
 template <int D>
 __device__ __forceinline__ void load_tile(TileRegs<D> &r, const PrefillArgs &a, const int32_t *table,
-                                          int nblk_valid, int kv_len, int g, int kt, int tid) {
+                                          int nblk_valid, int g, int kt, int tid) {
     constexpr int kChunksPerTile = kBlock * D * 2 / 16;      // 16-byte chunks in a K (or V) tile
     constexpr int kPerKV = 4 * kChunksPerTile;               // chunks of 4 K tiles
-    const int64_t tile = (int64_t)kBlock * D;
+    constexpr int kTileElems = kBlock * D;
 #pragma unroll
     for (int u = 0; u < TileRegs<D>::kChunks; ++u) {
         const int c = tid + u * kPreThreads;
-        const bool is_v = c >= kPerKV;
-        const int cc = is_v ? c - kPerKV : c;
-        const int bi = cc / kChunksPerTile;
+        const int is_v = __builtin_amdgcn_readfirstlane(c >= kPerKV ? 1 : 0);
+        const int cc = c - is_v * kPerKV;
+        const int bi = __builtin_amdgcn_readfirstlane(cc / kChunksPerTile);   // uniform per wave
         const int within = cc % kChunksPerTile;
         const int jb = kt * 4 + bi;
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (jb < nblk_valid) {
-            const int32_t b = table[jb];
-            if (b >= 0 && b < a.num_blocks) {
-                const uint16_t *base = a.pool + (((int64_t)b * 2 + (is_v ? 1 : 0)) * a.num_kv_heads + g) * tile;
-                v = *reinterpret_cast<const uint4 *>(base + within * 8);
-                const int tok0 = jb * kBlock;
-                if (tok0 + kBlock > kv_len) {
-                    if (!is_v) {
-                        const int token = within / (D / 8);
-                        if (tok0 + token >= kv_len) v = make_uint4(0, 0, 0, 0);
-                    } else {
-                        // V chunk: 8 consecutive tokens of one dim
-                        const int t8 = (within & 1) * 8;
-                        uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            const int t = tok0 + t8 + 2 * e;
-                            const uint32_t mask = t + 1 < kv_len ? 0xFFFFFFFFu : (t < kv_len ? 0x0000FFFFu : 0u);
-                            w[e] &= mask;
-                        }
-                        v = make_uint4(w[0], w[1], w[2], w[3]);
-                    }
-                }
-            }
-        }
-        r.c[u] = v;
+        int32_t b = jb < nblk_valid ? table[jb] : -1;
+        const bool valid = b >= 0 && b < a.num_blocks;
+        const uint16_t *base = a.pool + (((int64_t)(valid ? b : 0) * 2 + is_v) * a.num_kv_heads + g) * kTileElems;
+        const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint16_t *>(base), 0, valid ? kTileElems * 2 : 0, kBufferDword3P);
+        r.c[u] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, within * 16, 0, 0);
     }
 }
 
+// Write a loaded tile to LDS.  Slots at or past the session's last key (kv_len)
+// are zeroed here so that masked keys contribute exact zeros (never NaN) to PV.
 template <int D>
-__device__ __forceinline__ void store_tile(const TileRegs<D> &r, uint8_t *lds_k, uint8_t *lds_v, int tid) {
+__device__ __forceinline__ void store_tile(TileRegs<D> &r, uint8_t *lds_k, uint8_t *lds_v, int tid,
+                                           int kt, int kv_len) {
     constexpr int kChunksPerTile = kBlock * D * 2 / 16;
     constexpr int kPerKV = 4 * kChunksPerTile;
     constexpr int kRowChunks = D / 8;
+    const bool tail = (kt + 1) * kKeyTile > kv_len;
 #pragma unroll
     for (int u = 0; u < TileRegs<D>::kChunks; ++u) {
         const int c = tid + u * kPreThreads;
+        u32x4 v = r.c[u];
         if (c < kPerKV) {
             const int bi = c / kChunksPerTile;
             const int within = c % kChunksPerTile;
             const int token = within / kRowChunks;
             const int ch = within % kRowChunks;
+            if (tail && kt * kKeyTile + bi * kBlock + token >= kv_len) v = u32x4{0u, 0u, 0u, 0u};
             const int slot = ch ^ (token & (kRowChunks - 1));
-            *reinterpret_cast<uint4 *>(lds_k + bi * (kBlock * D * 2) + token * (D * 2) + slot * 16) = r.c[u];
+            *reinterpret_cast<u32x4 *>(lds_k + bi * (kBlock * D * 2) + token * (D * 2) + slot * 16) = v;
         } else {
-            *reinterpret_cast<uint4 *>(lds_v + (c - kPerKV) * 16) = r.c[u];
+            const int cv = c - kPerKV;
+            if (tail) {
+                // V chunk: 8 consecutive tokens of one dim
+                const int bi = cv / kChunksPerTile;
+                const int t0 = kt * kKeyTile + bi * kBlock + (cv & 1) * 8;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int t = t0 + 2 * e;
+                    const uint32_t mask = t + 1 < kv_len ? 0xFFFFFFFFu : (t < kv_len ? 0x0000FFFFu : 0u);
+                    v[e] &= mask;
+                }
+            }
+            *reinterpret_cast<u32x4 *>(lds_v + cv * 16) = v;
         }
     }
 }
 
 template <int D>
-__global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(kPreThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void prefill_kernel(PrefillArgs a) {
     constexpr int KS = D / 32;           // 32-dim k-steps of QK
     constexpr int NDT = D / 16;          // 16-dim output tiles
     constexpr int kRowChunks = D / 8;
@@ -194,14 +195,14 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
 
     const int32_t *table = a.block_tables + (int64_t)s * a.max_blocks;
     TileRegs<D> regs;
-    load_tile<D>(regs, a, table, nblk_valid, kv_len, g, 0, tid);
+    load_tile<D>(regs, a, table, nblk_valid, g, 0, tid);
 
     for (int kt = 0; kt < ntiles; ++kt) {
         uint8_t *lk = lds[kt & 1][0];
         uint8_t *lv = lds[kt & 1][1];
-        store_tile<D>(regs, lk, lv, tid);
+        store_tile<D>(regs, lk, lv, tid, kt, kv_len);
         __syncthreads();
-        if (kt + 1 < ntiles) load_tile<D>(regs, a, table, nblk_valid, kv_len, g, kt + 1, tid);
+        load_tile<D>(regs, a, table, kt + 1 < ntiles ? nblk_valid : 0, g, kt + 1, tid);
 
         // ---- S^T = K Q^T for 4 key sub-tiles x 2 row tiles
         f32x4 sacc[2][4];
