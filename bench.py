@@ -13,7 +13,9 @@ and the KV-block restore/stash scatter legs (48 layers x 4 KV heads x 128 dims,
 side stream.  Inputs are seeded synthetic sessions, resident in HBM before the
 timed region starts.  ``cpu_baseline`` is the CPU oracle timed on this host.
 
-Usage: python bench.py [--steps K] [--warmup W] [--legs decode,prefill,talker,restore]
+Usage: python bench.py [--steps K] [--warmup W] [--legs decode,prefill,talker,restore,calib]
+(decode always runs; "calib" adds a 1 GiB plain device copy used to scale the
+rocprofv3 HBM-traffic counters.)
 """
 import argparse
 import hashlib
@@ -370,6 +372,26 @@ def restore_leg(torch, kv, W, args, dec):
             "host_leg": host}
 
 
+def calib_leg(torch, args):
+    """A plain device copy of known size, the reference for HBM traffic counters
+    (FETCH_SIZE / WRITE_SIZE of this kernel per launch should read 1 GiB each)."""
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty(n, dtype=torch.uint8, device="cuda")
+    src.fill_(1)
+    torch.cuda.synchronize()
+    timer = Timer(torch, torch.cuda.current_stream())
+    for _ in range(5):
+        e = timer.start()
+        torch.bitwise_not(src, out=dst)      # an elementwise kernel of its own name
+        timer.stop(e)
+    torch.cuda.synchronize()
+    ms = timer.mean_ms()
+    log("calibration copy: 1 GiB in %.3f ms, %.0f GB/s (read + write)" % (ms, 2 * n / ms / 1e6))
+    del src, dst
+    return {"bytes_each_way": n, "ms": round(ms, 4), "gbs_read_plus_write": round(2 * n / ms / 1e6, 1)}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -385,6 +407,7 @@ def main():
     legs = set(args.legs.split(","))
     log("device:", torch.cuda.get_device_name(0), "| library:", kv.version())
 
+    calib = calib_leg(torch, args) if "calib" in legs else None
     dec = decode_leg(torch, kv, W, args)
     dec_gbs = dec["alg_bytes"] / (dec["kernel_ms"] * 1e-3) / 1e9
     wall_gbs = dec["alg_bytes"] * args.steps / dec["wall_s"] / 1e9
@@ -397,6 +420,8 @@ def main():
         torch.cuda.empty_cache()
     if "restore" in legs:
         extra["restore"] = restore_leg(torch, kv, W, args, dec)
+    if calib:
+        extra["calibration_copy"] = calib
     cpu = None if args.no_cpu_baseline else cpu_baseline(dec, W)
 
     line = {

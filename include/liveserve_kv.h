@@ -69,6 +69,7 @@ typedef enum {
 /* Bits of the device error word (ls_device_errors). */
 #define LS_DEVERR_BLOCK_ID 0x1u     /* a block id outside [0, num_blocks) was skipped */
 #define LS_DEVERR_LENGTH   0x2u     /* a length exceeded its block table and was clipped */
+#define LS_DEVERR_INTERNAL 0x4u     /* an internal bounded wait expired (a library bug) */
 
 typedef struct ls_kv_pool ls_kv_pool;
 

@@ -166,8 +166,10 @@ ls_status kv_pool_create(const ls_kv_pool_desc *desc, ls_kv_pool **out) {
                     desc->kv_bytes, need);
     if (desc->staging_ring && reinterpret_cast<uintptr_t>(desc->staging_ring) % 16 != 0)
         return fail(LS_EINVAL, "staging_ring must be 16-byte aligned");
-    int dev = 0;
+    int dev = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess) dev = -1;
+    if (dev >= 0 && hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        cus = 0;
     ls_kv_pool *pool = new (std::nothrow) ls_kv_pool;
     if (!pool) return fail(LS_ENOMEM, "out of host memory");
     pool->geom.num_layers = desc->num_layers;
@@ -178,6 +180,7 @@ ls_status kv_pool_create(const ls_kv_pool_desc *desc, ls_kv_pool **out) {
     pool->geom.ring = static_cast<uint8_t *>(desc->staging_ring);
     pool->geom.ring_bytes = desc->staging_ring ? desc->staging_ring_bytes : 0;
     pool->geom.device = dev;
+    pool->geom.num_cus = cus;
     *out = pool;
     return LS_OK;
 }
@@ -213,6 +216,9 @@ ls_status paged_attn_decode(ls_kv_pool *pool, int32_t layer, int32_t num_session
     if (max_blocks_per_session <= 0) return fail(LS_EINVAL, "max_blocks_per_session must be > 0");
     if (!(scale > 0.f) || scale != scale) return fail(LS_EINVAL, "scale must be a positive number");
     const DecodePlan plan = plan_decode(p, num_sessions, num_q_heads, max_blocks_per_session);
+    if (!plan.supported)
+        return fail(LS_EUNSUPPORTED, "batch of %d sessions with %d blocks each exceeds the decode "
+                    "limits (2048 sessions, 131072 tokens)", num_sessions, max_blocks_per_session);
     if (workspace_bytes < plan.total())
         return fail(LS_ENOMEM, "workspace_bytes (%zu) < required (%zu)", workspace_bytes, plan.total());
     unsigned int *err = device_error_word();

@@ -23,6 +23,7 @@ struct PoolGeom {
     uint8_t *ring;                  // device staging ring (may be null)
     size_t ring_bytes;
     int device;
+    int num_cus;                    // compute units of that device (0 if unknown)
 
     // Elements of one (kv, head) tile and of one (layer, block) slab.
     int64_t tile_elems() const { return (int64_t)kBlock * head_dim; }
@@ -41,6 +42,8 @@ unsigned int *device_error_word();
 struct DecodePlan {
     int split_tokens;               // tokens per split (multiple of 64)
     int max_splits;                 // splits of the longest possible session
+    bool supported;                 // false when a session could need too many splits
+    int resident_workgroups;        // persistent grid size
     size_t ml_bytes;                // fp32 [S][Hkv][max_splits][G][2]
     size_t acc_bytes;               // fp32 [S][Hkv][max_splits][G][D]
     size_t total() const { return ml_bytes + acc_bytes; }

@@ -24,6 +24,8 @@
 // stream never waits on an index fetch; a block that does not exist is loaded
 // through a zero-size buffer descriptor (no memory traffic, no branch).  Heads
 // beyond G in the 16-wide tile carry q = 0 and are never written.
+#include <algorithm>
+
 #include "common.h"
 
 namespace ls {
@@ -38,8 +40,11 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kDecThreads = 256;
 constexpr int kDecWaves = kDecThreads / kWave;
-constexpr int kMaxSplitTokens = 512;
-constexpr int kMaxPerWave = kMaxSplitTokens / (kDecWaves * kBlock);   // blocks per wave per split
+constexpr int kMaxSplitTokens = 512;         // 8 blocks per wave (the unrolled sequence)
+constexpr int kMaxSplits = 256;              // combine kernel's LDS capacity
+constexpr int kMaxBatch = 2048;              // sessions per decode call (LDS prefix sums)
+constexpr int kMaxGroup = 8;                 // query heads per KV head
+constexpr int kSpinLimit = 1 << 22;          // bound of the merge-slot wait (~0.1 s)
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kBufferDword3 = 0x00020000;   // raw buffer, 32-bit data format
 constexpr float kMaxFloor = -1.0e30f;       // initial running max (finite, below any score)
@@ -56,11 +61,12 @@ struct DecodeArgs {
     const int32_t *lens;           // tokens already in the pool
     int32_t appended;              // 1: the step's own token was appended at lens[s]
     float scale_log2;              // scale * log2(e)
-    int32_t split_tokens;          // multiple of 64, at most kMaxSplitTokens
+    int32_t split_tokens;          // kPerWave * 64 of the instantiation launched
     int32_t max_splits;
     float *part_ml;                // [S][Hkv][max_splits][G][2]
     float *part_acc;               // [S][Hkv][max_splits][G][D]
     unsigned int *err;             // device error word
+    int32_t num_sessions;
 };
 
 template <int D>
@@ -157,144 +163,290 @@ __device__ __forceinline__ void process_block(BlockRegs<D> &r, const bf16x8 (&qo
                                                           o[dt], 0, 0, 0);
 }
 
-template <int D, int kDepth>
+// Block-wide exclusive scan of one int per thread (kDecThreads threads).
+__device__ __forceinline__ int block_exclusive_scan(int v, int *sm_wave_tot, int &total) {
+    const int lane = threadIdx.x % kWave;
+    const int wave = threadIdx.x / kWave;
+    int x = v;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int y = __shfl_up(x, off);
+        if (lane >= off) x += y;
+    }
+    if (lane == kWave - 1) sm_wave_tot[wave] = x;
+    __syncthreads();
+    int before = 0;
+    total = 0;
+#pragma unroll
+    for (int w = 0; w < kDecWaves; ++w) {
+        const int t = sm_wave_tot[w];
+        if (w < wave) before += t;
+        total += t;
+    }
+    return before + x - v;
+}
+
+// Persistent decode: a fixed grid (about two workgroups per CU) walks the work
+// items (session s, split k, KV head g) round-robin.  Each workgroup first
+// computes, in LDS, how many splits every session needs (a prefix sum over the
+// batch), so no workgroup is launched for a split that does not exist, and it
+// fetches the next item's block ids while it works on the current one.
+template <int D, int kDepth, int kMaxPerWave>
 __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
-    const int split = blockIdx.x;
-    const int g = blockIdx.y;
-    const int s = blockIdx.z;
+    __shared__ int sm_cum[kMaxBatch + 1];       // first work row of each session
+    __shared__ int sm_len[kMaxBatch];           // attended length of each session
+    __shared__ int sm_wave_tot[kDecWaves];
+    // Per-item merge slots (double-buffered): each wave leaves its (m, l, O) of
+    // the group's heads, the last wave to arrive merges them.
+    __shared__ float sm_m[2][kDecWaves][kMaxGroup];
+    __shared__ float sm_l[2][kDecWaves][kMaxGroup];
+    __shared__ __attribute__((aligned(16))) float sm_o[2][kDecWaves][kMaxGroup][D];
+    __shared__ int sm_arrived[2];               // waves that have filled the slot
+    __shared__ int sm_merged[2];                // merges completed on the slot
+
     const int tid = threadIdx.x;
     const int G = a.group;
     const int hq_total = a.num_kv_heads * G;
+    const int S = a.num_sessions;
+    const int T = a.split_tokens;
 
-    const int L = attended_len(a, s, split == 0 && tid == 0 && g == 0);
-    if (L <= 0) {
-        // Softmax over no key is undefined: write zeros and flag the length.
-        if (split == 0) {
-            if (tid == 0 && g == 0) flag_error(a.err, LS_DEVERR_LENGTH);
-            for (int idx = tid; idx < G * D; idx += kDecThreads)
-                a.out[((int64_t)s * hq_total + g * G) * D + idx] = 0;
-        }
-        return;
+    if (tid < 2) {
+        sm_arrived[tid] = 0;
+        sm_merged[tid] = 0;
     }
-    const int t0 = split * a.split_tokens;
-    if (t0 >= L) return;
-    const int t1 = min(L, t0 + a.split_tokens);
-    const int nsplit = (L + a.split_tokens - 1) / a.split_tokens;
-    const int blk0 = t0 / kBlock;
-    const int nblk = (t1 + kBlock - 1) / kBlock - blk0;     // <= kMaxSplitTokens / 16
+    // ---- splits per session and their prefix sum
+    const int per_thread = (S + kDecThreads - 1) / kDecThreads;
+    const int s_begin = min(S, tid * per_thread);
+    const int s_end = min(S, s_begin + per_thread);
+    int mine = 0;
+    for (int s = s_begin; s < s_end; ++s) {
+        const int L = attended_len(a, s, blockIdx.x == 0);
+        sm_len[s] = L;
+        mine += L > 0 ? (L + T - 1) / T : 1;        // an empty session still owns one row
+    }
+    int total_rows = 0;
+    int run = block_exclusive_scan(mine, sm_wave_tot, total_rows);
+    for (int s = s_begin; s < s_end; ++s) {
+        sm_cum[s] = run;
+        run += sm_len[s] > 0 ? (sm_len[s] + T - 1) / T : 1;
+    }
+    if (tid == 0) sm_cum[S] = total_rows;
+    __syncthreads();
+    const int total_items = total_rows * a.num_kv_heads;
 
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
     const int lane = tid % kWave;
     const int c16 = lane & 15;
     const int g4 = lane >> 4;
-
-    // Block ids of the split, one per lane; out-of-range ids become -1.
-    int id_lane = -1;
-    if (lane < nblk) {
-        const int32_t b = a.block_tables[(int64_t)s * a.max_blocks + blk0 + lane];
-        if (b >= 0 && b < a.num_blocks) {
-            id_lane = b;
-        } else if (wave == 0) {
-            flag_error(a.err, LS_DEVERR_BLOCK_ID);
-        }
-    }
-    const int my_n = wave < nblk ? (nblk - wave + kDecWaves - 1) / kDecWaves : 0;
-    auto bid = [&](int it) -> int {
-        const int idx = wave + it * kDecWaves;
-        return idx < nblk ? __builtin_amdgcn_readlane(id_lane, idx) : -1;
-    };
-
-    // Q^T operand: column = query head c16 of the group (zero beyond G).
-    bf16x8 qop[D / 32];
-    {
-        const bool active = c16 < G;
-        const uint16_t *qrow = a.q + ((int64_t)s * hq_total + g * G + (active ? c16 : 0)) * D;
-#pragma unroll
-        for (int ks = 0; ks < D / 32; ++ks) {
-            uint4 v = *reinterpret_cast<const uint4 *>(qrow + ks * 32 + g4 * 8);
-            if (!active) v = make_uint4(0, 0, 0, 0);
-            qop[ks] = __builtin_bit_cast(bf16x8, v);
-        }
-    }
     int koff[D / 32], voff[D / 16];
 #pragma unroll
     for (int ks = 0; ks < D / 32; ++ks) koff[ks] = (c16 * D + ks * 32 + g4 * 8) * 2;
 #pragma unroll
     for (int dt = 0; dt < D / 16; ++dt) voff[dt] = ((dt * 16 + c16) * kBlock + g4 * 4) * 2;
 
-    // The running max starts at a finite floor: a block whose keys are all
-    // masked then leaves (m, l, O) unchanged instead of producing NaN.
-    float m = kMaxFloor, lsum = 0.f;
-    f32x4 o[D / 16];
-#pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // (session, split) of work row r: largest s with sm_cum[s] <= r.
+    auto locate = [&](int row, int &s_out, int &split_out) {
+        int lo = 0, hi = S - 1;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (sm_cum[mid] <= row) lo = mid; else hi = mid - 1;
+        }
+        s_out = lo;
+        split_out = row - sm_cum[lo];
+    };
+    // Raw block ids of a split, one per lane.  The load is unconditional (its
+    // index clamped into the table row) and the id is validated only when it is
+    // used, so nothing waits for this load until the item is processed.
+    auto fetch_ids = [&](int s_, int split_) -> int {
+        const int j = min(split_ * (T / kBlock) + lane, a.max_blocks - 1);
+        return a.block_tables[(int64_t)s_ * a.max_blocks + j];
+    };
+    // Validated id (or -1) of entry idx of a fetched id register.
+    auto checked_id = [&](int ids, int idx, int nb) -> int {
+        if (idx >= nb) return -1;
+        const int b = __builtin_amdgcn_readlane(ids, idx);
+        if (b >= 0 && b < a.num_blocks) return b;
+        if (lane == 0) flag_error(a.err, LS_DEVERR_BLOCK_ID);
+        return -1;
+    };
 
-    // kDepth blocks in flight per wave.  The per-wave block sequence is fully
-    // unrolled (at most kMaxPerWave blocks) with forward-only exits, so the
-    // compiler sees straight-line code and waits only for the block it is about
-    // to use.  A block with a bad id is processed as fully masked (0 keys).
+    // Q^T operand of an item: column = query head c16 of the group (zero beyond G).
+    auto load_q = [&](int s_, int g_, bf16x8 (&qo)[D / 32]) {
+        const bool active = c16 < G;
+        const uint16_t *qrow = a.q + ((int64_t)s_ * hq_total + g_ * G + (active ? c16 : 0)) * D;
+#pragma unroll
+        for (int ks = 0; ks < D / 32; ++ks) {
+            uint4 v = *reinterpret_cast<const uint4 *>(qrow + ks * 32 + g4 * 8);
+            if (!active) v = make_uint4(0, 0, 0, 0);
+            qo[ks] = __builtin_bit_cast(bf16x8, v);
+        }
+    };
+    // Block count of a split and this wave's it-th block id within it.
+    auto split_blocks = [&](int s_, int split_) -> int {
+        const int L = sm_len[s_];
+        const int t0 = split_ * T;
+        return L > t0 ? (min(L, t0 + T) + kBlock - 1) / kBlock - t0 / kBlock : 0;
+    };
+
+    // kDepth blocks in flight per wave, carried across items: the next item's
+    // first blocks (and its q) are requested before the current item's merge.
     BlockRegs<D> r[kDepth];
     int bb[kDepth];
+    bf16x8 qop[D / 32];
+    // Each wave keeps the fetched block ids of the current and the next item in
+    // its own LDS slots (double-buffered; read back with readlane), so no value
+    // loaded from memory is carried around the item loop.
+    __shared__ int sm_ids[kDecWaves][2][kMaxSplitTokens / kBlock];
+    int item = blockIdx.x;
+    int s = 0, split = 0;
+    if (item < total_items) {
+        locate(item / a.num_kv_heads, s, split);
+        const int ids0 = fetch_ids(s, split);
+        if (lane < kMaxSplitTokens / kBlock) sm_ids[wave][0][lane] = ids0;
+        load_q(s, item % a.num_kv_heads, qop);
+        const int nb = split_blocks(s, split);
 #pragma unroll
-    for (int j = 0; j < kDepth; ++j) {
-        bb[j] = bid(j);
-        load_block<D>(r[j], a.pool, a.num_kv_heads, g, bb[j], koff, voff);
-    }
-#pragma unroll
-    for (int i = 0; i < kMaxPerWave; ++i) {
-        if (i >= my_n) break;
-        const int j = i % kDepth;
-        const int tb = (blk0 + wave + i * kDecWaves) * kBlock;
-        process_block<D>(r[j], qop, tb, bb[j] >= 0 ? L : 0, a.scale_log2, g4, m, lsum, o);
-        if (i + kDepth < kMaxPerWave) {
-            bb[j] = bid(i + kDepth);
-            load_block<D>(r[j], a.pool, a.num_kv_heads, g, bb[j], koff, voff);
+        for (int j = 0; j < kDepth; ++j) {
+            bb[j] = checked_id(ids0, wave + j * kDecWaves, nb);
+            load_block<D>(r[j], a.pool, a.num_kv_heads, item % a.num_kv_heads, bb[j], koff, voff);
         }
     }
-    lsum = wave_sum_xor_16_32(lsum);
-
-    // Merge the 4 waves through LDS.
-    __shared__ float sm_m[kDecWaves][16];
-    __shared__ float sm_l[kDecWaves][16];
-    __shared__ float sm_o[kDecWaves][16][D];
-#pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) sm_o[wave][c16][dt * 16 + g4 * 4 + i] = o[dt][i];
-    if (g4 == 0) {
-        sm_m[wave][c16] = m;
-        sm_l[wave][c16] = lsum;
-    }
-    __syncthreads();
-
-    const int64_t part = ((int64_t)s * a.num_kv_heads + g) * a.max_splits + split;
-    for (int idx = tid; idx < G * D; idx += kDecThreads) {
-        const int h = idx / D, d = idx % D;
-        float M = sm_m[0][h];
-#pragma unroll
-        for (int w = 1; w < kDecWaves; ++w) M = fmaxf(M, sm_m[w][h]);
-        float wsum = 0.f, acc = 0.f;
-#pragma unroll
-        for (int w = 0; w < kDecWaves; ++w) {
-            const float e = __builtin_amdgcn_exp2f(sm_m[w][h] - M);
-            wsum += e * sm_l[w][h];
-            acc += e * sm_o[w][h][d];
+    for (int k = 0; item < total_items; item += gridDim.x, ++k) {
+        const int g = item % a.num_kv_heads;
+        const int L = sm_len[s];
+        const int cur_s = s, cur_split = split;
+        const int cur_ids = lane < kMaxSplitTokens / kBlock ? sm_ids[wave][k & 1][lane] : -1;
+        // Next item: its (session, split) and block ids, fetched now.
+        const int next = item + gridDim.x;
+        const bool has_next = next < total_items;
+        int next_ids = -1;
+        if (has_next) {
+            locate(next / a.num_kv_heads, s, split);
+            next_ids = fetch_ids(s, split);
         }
-        if (nsplit == 1) {
-            a.out[((int64_t)s * hq_total + g * G + h) * D + d] = (uint16_t)f32_to_bf16_bits(acc / wsum);
-        } else {
-            a.part_acc[(part * G + h) * D + d] = acc;
-            if (d == 0) {
-                a.part_ml[(part * G + h) * 2 + 0] = M;
-                a.part_ml[(part * G + h) * 2 + 1] = wsum;
+        const int t0 = cur_split * T;
+        const int nsplit = L > 0 ? (L + T - 1) / T : 1;
+        const int blk0 = t0 / kBlock;
+        const int nblk = split_blocks(cur_s, cur_split);
+        const int my_n = wave < nblk ? (nblk - wave + kDecWaves - 1) / kDecWaves : 0;
+        auto bid = [&](int it) -> int { return checked_id(cur_ids, wave + it * kDecWaves, nblk); };
+
+        // The running max starts at a finite floor: a block whose keys are all
+        // masked then leaves (m, l, O) unchanged instead of producing NaN.
+        float m = kMaxFloor, lsum = 0.f;
+        f32x4 o[D / 16];
+#pragma unroll
+        for (int dt = 0; dt < D / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+        // The per-wave block sequence is fully unrolled (at most kMaxPerWave
+        // blocks) with forward-only exits, so the compiler sees straight-line
+        // code and waits only for the block it is about to use.  A block with a
+        // bad id is processed as fully masked.
+#pragma unroll
+        for (int i = 0; i < kMaxPerWave; ++i) {
+            if (i >= my_n) break;
+            const int j = i % kDepth;
+            const int tb = (blk0 + wave + i * kDecWaves) * kBlock;
+            process_block<D>(r[j], qop, tb, bb[j] >= 0 ? L : 0, a.scale_log2, g4, m, lsum, o);
+            if (i + kDepth < kMaxPerWave) {
+                bb[j] = bid(i + kDepth);
+                load_block<D>(r[j], a.pool, a.num_kv_heads, g, bb[j], koff, voff);
+            }
+        }
+        // Request the next item's first blocks and q before merging this one.
+        if (has_next) {
+            if (lane < kMaxSplitTokens / kBlock) sm_ids[wave][(k + 1) & 1][lane] = next_ids;
+            const int g_next = next % a.num_kv_heads;
+            const int nb = split_blocks(s, split);
+            load_q(s, g_next, qop);
+#pragma unroll
+            for (int j = 0; j < kDepth; ++j) {
+                bb[j] = checked_id(next_ids, wave + j * kDecWaves, nb);
+                load_block<D>(r[j], a.pool, a.num_kv_heads, g_next, bb[j], koff, voff);
+            }
+        }
+        lsum = wave_sum_xor_16_32(lsum);
+
+        // ---- asynchronous merge of the 4 waves: no workgroup barrier.
+        const int slot = k & 1;
+        // The slot is free once the merge of the item two steps back is done.
+        // (Bounded: a wait that never ends would be a bug; it is flagged, not hung on.)
+        for (int spin = 0; __hip_atomic_load(&sm_merged[slot], __ATOMIC_ACQUIRE,
+                                             __HIP_MEMORY_SCOPE_WORKGROUP) != (k >> 1); ++spin) {
+            if (spin == kSpinLimit) {
+                if (lane == 0) flag_error(a.err, LS_DEVERR_INTERNAL);
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+        if (c16 < G) {
+#pragma unroll
+            for (int dt = 0; dt < D / 16; ++dt)
+                *reinterpret_cast<f32x4 *>(&sm_o[slot][wave][c16][dt * 16 + g4 * 4]) = o[dt];
+            if (g4 == 0) {
+                sm_m[slot][wave][c16] = m;
+                sm_l[slot][wave][c16] = lsum;
+            }
+        }
+        // One arrival per wave (lane 0), broadcast to the whole wave.
+        int before = 0;
+        if (lane == 0)
+            before = __hip_atomic_fetch_add(&sm_arrived[slot], 1, __ATOMIC_ACQ_REL,
+                                            __HIP_MEMORY_SCOPE_WORKGROUP);
+        before = __builtin_amdgcn_readfirstlane(before);
+        if (before == kDecWaves - 1) {
+            // Last wave in: merge the item (4 consecutive outputs per lane per step).
+            const int64_t part = ((int64_t)cur_s * a.num_kv_heads + g) * a.max_splits + cur_split;
+            for (int base = lane * 4; base < G * D && L <= 0; base += kWave * 4)
+                // Softmax over no key is undefined: the output is zero (length flagged).
+                *reinterpret_cast<uint2 *>(a.out + ((int64_t)cur_s * hq_total + g * G) * D + base) =
+                    make_uint2(0u, 0u);
+            for (int base = lane * 4; base < G * D && L > 0; base += kWave * 4) {
+                const int h = base / D, d = base % D;
+                float M = sm_m[slot][0][h];
+#pragma unroll
+                for (int w = 1; w < kDecWaves; ++w) M = fmaxf(M, sm_m[slot][w][h]);
+                float wsum = 0.f;
+                f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int w = 0; w < kDecWaves; ++w) {
+                    const float e = __builtin_amdgcn_exp2f(sm_m[slot][w][h] - M);
+                    wsum += e * sm_l[slot][w][h];
+                    acc += e * *reinterpret_cast<const f32x4 *>(&sm_o[slot][w][h][d]);
+                }
+                if (nsplit == 1) {
+                    const float inv = 1.f / wsum;
+                    *reinterpret_cast<uint2 *>(a.out + ((int64_t)cur_s * hq_total + g * G + h) * D + d) =
+                        make_uint2(pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv));
+                } else {
+                    *reinterpret_cast<f32x4 *>(a.part_acc + (part * G + h) * D + d) = acc;
+                    if (d == 0) {
+                        a.part_ml[(part * G + h) * 2 + 0] = M;
+                        a.part_ml[(part * G + h) * 2 + 1] = wsum;
+                    }
+                }
+            }
+            if (lane == 0) {
+                __hip_atomic_store(&sm_arrived[slot], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                __hip_atomic_fetch_add(&sm_merged[slot], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
             }
         }
     }
 }
 
-// Log-sum-exp merge of the splits of every (session, KV head) with more than one.
+// Log-sum-exp merge of the splits of every (session, KV head) with more than
+// one.  1024 threads per (session, KV head): each wave reduces one head's split
+// statistics with shuffles, then four groups of 256 threads each sum a quarter
+// of the splits for 4 consecutive outputs (their loads issued together) and the
+// groups are added through LDS.
+constexpr int kCombThreads = 1024;
+constexpr int kCombParts = kCombThreads / 256;
+
 template <int D>
-__global__ __launch_bounds__(kDecThreads) void decode_combine_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(kCombThreads) void decode_combine_kernel(DecodeArgs a) {
+    __shared__ float sm_e[kMaxSplits][kMaxGroup];          // exp2(m_k - M) per split and head
+    __shared__ float sm_inv[kMaxGroup];                     // 1 / sum_k exp2(m_k - M) l_k
+    __shared__ __attribute__((aligned(16))) float sm_acc[kCombParts - 1][256][4];
     const int g = blockIdx.x;
     const int s = blockIdx.y;
     const int L = attended_len(a, s, false);
@@ -304,17 +456,55 @@ __global__ __launch_bounds__(kDecThreads) void decode_combine_kernel(DecodeArgs 
     const int G = a.group;
     const int hq_total = a.num_kv_heads * G;
     const int64_t part = ((int64_t)s * a.num_kv_heads + g) * a.max_splits;
-    for (int idx = threadIdx.x; idx < G * D; idx += kDecThreads) {
-        const int h = idx / D, d = idx % D;
+    const int tid = threadIdx.x;
+    const int wave = tid / kWave, lane = tid % kWave;
+
+    if (wave < G) {
+        const int h = wave;
         float M = -INFINITY;
-        for (int k = 0; k < nsplit; ++k) M = fmaxf(M, a.part_ml[((part + k) * G + h) * 2]);
-        float wsum = 0.f, acc = 0.f;
-        for (int k = 0; k < nsplit; ++k) {
+        for (int k = lane; k < nsplit; k += kWave) M = fmaxf(M, a.part_ml[((part + k) * G + h) * 2]);
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
+        float wsum = 0.f;
+        for (int k = lane; k < nsplit; k += kWave) {
             const float e = __builtin_amdgcn_exp2f(a.part_ml[((part + k) * G + h) * 2] - M);
+            sm_e[k][h] = e;
             wsum += e * a.part_ml[((part + k) * G + h) * 2 + 1];
-            acc += e * a.part_acc[((part + k) * G + h) * D + d];
         }
-        a.out[((int64_t)s * hq_total + g * G + h) * D + d] = (uint16_t)f32_to_bf16_bits(acc / wsum);
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) wsum += __shfl_xor(wsum, off);
+        if (lane == 0) sm_inv[h] = 1.f / wsum;
+    }
+    __syncthreads();
+
+    const int c = tid % 256;                 // 4 consecutive outputs: base = 4c
+    const int pidx = tid / 256;              // this thread sums splits pidx, pidx + 4, ...
+    const int base = c * 4;
+    const bool active = base < G * D;
+    const int h = active ? base / D : 0;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    if (active) {
+        const float *src = a.part_acc + (part * G) * D + base;
+        int k = pidx;
+        for (; k + 3 * kCombParts < nsplit; k += 4 * kCombParts) {
+            const f32x4 v0 = *reinterpret_cast<const f32x4 *>(src + (int64_t)k * G * D);
+            const f32x4 v1 = *reinterpret_cast<const f32x4 *>(src + (int64_t)(k + kCombParts) * G * D);
+            const f32x4 v2 = *reinterpret_cast<const f32x4 *>(src + (int64_t)(k + 2 * kCombParts) * G * D);
+            const f32x4 v3 = *reinterpret_cast<const f32x4 *>(src + (int64_t)(k + 3 * kCombParts) * G * D);
+            acc += sm_e[k][h] * v0 + sm_e[k + kCombParts][h] * v1 + sm_e[k + 2 * kCombParts][h] * v2 +
+                   sm_e[k + 3 * kCombParts][h] * v3;
+        }
+        for (; k < nsplit; k += kCombParts)
+            acc += sm_e[k][h] * *reinterpret_cast<const f32x4 *>(src + (int64_t)k * G * D);
+    }
+    if (pidx > 0) *reinterpret_cast<f32x4 *>(sm_acc[pidx - 1][c]) = acc;
+    __syncthreads();
+    if (pidx == 0 && active) {
+#pragma unroll
+        for (int q2 = 0; q2 < kCombParts - 1; ++q2) acc += *reinterpret_cast<const f32x4 *>(sm_acc[q2][c]);
+        const float inv = sm_inv[h];
+        *reinterpret_cast<uint2 *>(a.out + ((int64_t)s * hq_total + g * G) * D + base) =
+            make_uint2(pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv));
     }
 }
 
@@ -325,14 +515,18 @@ DecodePlan plan_decode(const PoolGeom &p, int32_t num_sessions, int32_t num_q_he
     DecodePlan plan{};
     const int64_t max_tokens = (int64_t)max_blocks_per_session * kBlock;
     const int64_t work = (int64_t)num_sessions * p.num_kv_heads * max_tokens;
-    // Aim for several workgroups per CU (256 CUs x 2 resident) when the batch is
-    // large, smaller splits when it is not.
+    // Splits of 256 or 512 tokens: long enough to amortise a workgroup's start-up,
+    // short enough to give several workgroups per CU on a large batch.
     int T = 512;
     if (work < 256LL * 2 * 4 * 512) T = 256;
-    if (work < 256LL * 2 * 4 * 128) T = 128;
+    while (T < kMaxSplitTokens && (max_tokens + T - 1) / T > kMaxSplits) T *= 2;
     plan.split_tokens = T;
     plan.max_splits = (int)((max_tokens + T - 1) / T);
     if (plan.max_splits < 1) plan.max_splits = 1;
+    plan.supported = plan.max_splits <= kMaxSplits && num_sessions <= kMaxBatch;
+    // Persistent grid: as many workgroups as the CUs hold at this kernel's
+    // occupancy (two 256-thread workgroups per CU).
+    plan.resident_workgroups = 2 * (p.num_cus > 0 ? p.num_cus : 256);
     const int G = p.num_kv_heads > 0 ? num_q_heads / p.num_kv_heads : 0;
     const int64_t sg = (int64_t)num_sessions * p.num_kv_heads;
     auto pad = [](size_t b) { return (b + 255) & ~(size_t)255; };
@@ -364,18 +558,27 @@ hipError_t launch_decode(const PoolGeom &p, int layer, int32_t num_sessions, int
     uint8_t *ws = static_cast<uint8_t *>(workspace);
     a.part_ml = reinterpret_cast<float *>(ws);
     a.part_acc = reinterpret_cast<float *>(ws + plan.ml_bytes);
-    dim3 grid(plan.max_splits, p.num_kv_heads, num_sessions);
-    if (p.head_dim == 128)
-        hipLaunchKernelGGL((decode_kernel<128, 2>), grid, dim3(kDecThreads), 0, stream, a);
-    else
-        hipLaunchKernelGGL((decode_kernel<64, 2>), grid, dim3(kDecThreads), 0, stream, a);
+    a.num_sessions = num_sessions;
+    const int64_t upper = (int64_t)num_sessions * p.num_kv_heads * plan.max_splits;
+    dim3 grid((unsigned)std::min<int64_t>(upper, (int64_t)plan.resident_workgroups));
+#define LS_DECODE(DD, PW) \
+    hipLaunchKernelGGL((decode_kernel<DD, 2, PW>), grid, dim3(kDecThreads), 0, stream, a)
+    const int per_wave = plan.split_tokens / (kDecWaves * kBlock);
+    if (p.head_dim == 128) {
+        if (per_wave == 4) LS_DECODE(128, 4);
+        else LS_DECODE(128, 8);
+    } else {
+        if (per_wave == 4) LS_DECODE(64, 4);
+        else LS_DECODE(64, 8);
+    }
+#undef LS_DECODE
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || plan.max_splits == 1) return e;
     dim3 cgrid(p.num_kv_heads, num_sessions);
     if (p.head_dim == 128)
-        hipLaunchKernelGGL(decode_combine_kernel<128>, cgrid, dim3(kDecThreads), 0, stream, a);
+        hipLaunchKernelGGL(decode_combine_kernel<128>, cgrid, dim3(kCombThreads), 0, stream, a);
     else
-        hipLaunchKernelGGL(decode_combine_kernel<64>, cgrid, dim3(kDecThreads), 0, stream, a);
+        hipLaunchKernelGGL(decode_combine_kernel<64>, cgrid, dim3(kCombThreads), 0, stream, a);
     return hipGetLastError();
 }
 

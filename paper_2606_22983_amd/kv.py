@@ -54,7 +54,7 @@ for _f in (_lib.kv_pool_create, _lib.kv_pool_destroy, _lib.paged_attn_decode,
     _f.restype = ctypes.c_int
 
 LS_OK, LS_EINVAL, LS_ENOMEM, LS_EHIP, LS_EUNSUPPORTED = 0, -22, -12, -5, -95
-LS_DEVERR_BLOCK_ID, LS_DEVERR_LENGTH = 0x1, 0x2
+LS_DEVERR_BLOCK_ID, LS_DEVERR_LENGTH, LS_DEVERR_INTERNAL = 0x1, 0x2, 0x4
 
 
 class LiveServeError(RuntimeError):
