@@ -5,18 +5,25 @@
 // 0 .. c_s + j (bottom-right causal alignment); the turn's K/V has already been
 // appended to the pool, so every key is read through the block table.
 //
-// Workgroup = (q-tile, KV head g, session s).  The tile packs the GQA group into
-// the row dimension: 128 rows = (128 / G) new tokens x G query heads sharing
-// KV head g, so each K/V tile staged in LDS feeds 128 query rows.  Four
-// wavefronts own 32 rows each (two 16-row MFMA tiles).  Keys stream in tiles
-// of 64 (four 16-token blocks): global -> registers -> LDS (double buffered,
-// one barrier per tile), K token-major with an XOR swizzle, V dim-major.
+// Workgroup = (session, KV head g, query tile).  The tile packs the GQA group
+// into the row dimension: 256 rows = (256 / G) new tokens x G query heads
+// sharing KV head g, so each K/V tile staged in LDS feeds 256 query rows.
+// Eight wavefronts own 32 rows each (two 16-row MFMA tiles).  Keys stream in
+// tiles of 64 (four 16-token blocks): buffer loads into registers two tiles
+// ahead, then LDS (double buffered, one barrier per tile).
 //
 //   S^T[16 keys x 16 rows] = K[16 x D] . Q^T          (MFMA 16x16x32 bf16)
 //   O^T[16 dims x 16 rows] += V^T[16 x 32 keys] . P^T  (MFMA 16x16x32 bf16)
 // The S^T accumulator layout (lane: row = lane%16, keys 4*(lane/16)+i) is the
-// B-operand layout of the PV product, so P stays in registers (rounded to bf16);
-// softmax statistics stay in fp32.
+// B-operand layout of the PV product, so P stays in registers (rounded to
+// bf16); softmax statistics stay in fp32.  A row's running max is raised (and its O and l
+// rescaled) only when a tile's max exceeds it by more than 2^8, which keeps
+// every probability at most 256 and makes rescales rare.
+//
+// Workgroups run longest session first and, within a session, latest query
+// tile first (longest-processing-time order against the tail).  Consecutive
+// query tiles of one (session, KV head) are placed on the same XCD so that
+// they share its L2.
 #include "common.h"
 
 namespace ls {
@@ -25,19 +32,26 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kPreThreads = 256;
-constexpr int kBufferDword3P = 0x00020000;   // raw buffer, 32-bit data format
-constexpr int kPreRows = 128;            // query rows per workgroup
+constexpr int kPreThreads = 512;
+constexpr int kPreRows = 256;            // query rows per workgroup
 constexpr int kKeyTile = 64;             // keys per staged tile (4 blocks)
+constexpr int kBufferDword3P = 0x00020000;   // raw buffer, 32-bit data format
 constexpr float kLog2eP = 1.4426950408889634f;
+constexpr float kRescaleSlack = 8.0f;    // log2 units a row max may lag behind
+constexpr int kXcds = 8;                 // workgroups are dispatched round-robin over XCDs
+constexpr int kXcdChunk = 8;             // consecutive items kept on one XCD
+constexpr int kMaxSortSessions = 128;    // larger batches run in index order
 
 struct PrefillArgs {
     const uint16_t *pool;          // layer base
     int64_t num_blocks;
     int32_t num_kv_heads;
     int32_t group;
+    int32_t num_sessions;
+    int32_t qtiles;                // query tiles of the longest turn
     const uint16_t *q;             // [T][Hq][D]
     uint16_t *out;                 // [T][Hq][D]
     const int32_t *cu;             // [S+1]
@@ -52,96 +66,196 @@ __device__ __forceinline__ float xmax16_32(float x) {
     x = fmaxf(x, __shfl_xor(x, 16));
     return fmaxf(x, __shfl_xor(x, 32));
 }
-__device__ __forceinline__ float xsum16_32(float x) {
-    x += __shfl_xor(x, 16);
-    return x + __shfl_xor(x, 32);
-}
+
+// Thread -> 16-byte chunk assignment of one 64-key tile (4 blocks of K, then
+// 4 blocks of V).  K: chunk c = tid + u * threads, block c / kCpt, the chunk's
+// bytes are token-major (token = within / (D/8)).  V tiles are dim-major
+// ([D][16 tokens], two chunks per dim): each wave covers 32 dims, lanes 0..31
+// the first 8 tokens, lanes 32..63 the last 8.  With two V chunks per thread
+// (D = 128) a thread holds the same (dim, half) of blocks 2*k2 and 2*k2+1.
+template <int D>
+struct TileCfg {
+    static constexpr int kTileBytes = kBlock * D * 2;                  // one block's K (or V)
+    static constexpr int kCpt = kTileBytes / 16;                       // chunks per block tile
+    static constexpr int kPerThread = 2 * 4 * kCpt / kPreThreads;      // 4 (D=128) or 2 (D=64)
+    static constexpr int kKPer = kPerThread / 2;
+    static constexpr int kVPer = kPerThread / 2;
+    static_assert(kCpt % 64 == 0, "a wave's chunks must stay inside one block tile");
+    static_assert(kVPer == 1 || 4 * kCpt == 2 * kPreThreads, "V pairing needs 2 chunks per thread");
+};
 
 template <int D>
 struct TileRegs {
-    static constexpr int kChunks = (2 * kKeyTile * D * 2) / (16 * kPreThreads);  // 16-byte chunks per thread
-    u32x4 c[kChunks];
+    u32x4 c[TileCfg<D>::kPerThread];
 };
 
-// Issue the loads of one key tile (K then V of 4 blocks) into registers.  Blocks
-// past the session's keys (or with an id outside the pool) are read through a
-// zero-size buffer descriptor: no memory traffic, zeros returned.
+template <int D>
+__device__ __forceinline__ void v_chunk_coords(int tid, int e, int &bi, int &dim, int &h) {
+    using C = TileCfg<D>;
+    int within;
+    if constexpr (C::kVPer == 2) {
+        bi = 2 * (tid / C::kCpt) + e;
+        within = tid % C::kCpt;
+    } else {
+        bi = tid / C::kCpt;
+        within = tid % C::kCpt;
+    }
+    dim = (within >> 6) * 32 + (within & 31);
+    h = (within >> 5) & 1;
+}
+
+// Entry jb of a session's block table, or -1 at or past nv entries.  The table
+// does not change during a launch, so it is read through the constant address
+// space: a scalar load, whose wait does not also wait for the tile loads in
+// flight.  The clamped index keeps the read inside the table row.
+__device__ __forceinline__ int32_t table_entry(const int32_t *table, int jb, int nv) {
+    typedef const __attribute__((address_space(4))) int32_t const_i32;
+    const int jc = max(min(jb, nv - 1), 0);
+    const int32_t b = ((const_i32 *)table)[jc];
+    return jb < nv ? b : -1;
+}
+
+// Issue the loads of one key tile into registers.  Blocks past the session's
+// keys (or with an id outside the pool) are read through a zero-size buffer
+// descriptor: no memory traffic, zeros returned.  Every call issues the same
+// loads, so outstanding loads can be counted across iterations.
 template <int D>
 __device__ __forceinline__ void load_tile(TileRegs<D> &r, const PrefillArgs &a, const int32_t *table,
                                           int nblk_valid, int g, int kt, int tid) {
-    constexpr int kChunksPerTile = kBlock * D * 2 / 16;      // 16-byte chunks in a K (or V) tile
-    constexpr int kPerKV = 4 * kChunksPerTile;               // chunks of 4 K tiles
-    constexpr int kTileElems = kBlock * D;
+    using C = TileCfg<D>;
 #pragma unroll
-    for (int u = 0; u < TileRegs<D>::kChunks; ++u) {
-        const int c = tid + u * kPreThreads;
-        const int is_v = __builtin_amdgcn_readfirstlane(c >= kPerKV ? 1 : 0);
-        const int cc = c - is_v * kPerKV;
-        const int bi = __builtin_amdgcn_readfirstlane(cc / kChunksPerTile);   // uniform per wave
-        const int within = cc % kChunksPerTile;
+    for (int u = 0; u < C::kPerThread; ++u) {
+        int bi, off, is_v;
+        if (u < C::kKPer) {
+            const int c = tid + u * kPreThreads;
+            bi = c / C::kCpt;
+            off = (c % C::kCpt) * 16;
+            is_v = 0;
+        } else {
+            int dim, h;
+            v_chunk_coords<D>(tid, u - C::kKPer, bi, dim, h);
+            off = (dim * 2 + h) * 16;
+            is_v = 1;
+        }
+        bi = __builtin_amdgcn_readfirstlane(bi);   // uniform per wave by construction
         const int jb = kt * 4 + bi;
-        int32_t b = jb < nblk_valid ? table[jb] : -1;
+        const int32_t b = table_entry(table, jb, nblk_valid);
         const bool valid = b >= 0 && b < a.num_blocks;
-        const uint16_t *base = a.pool + (((int64_t)(valid ? b : 0) * 2 + is_v) * a.num_kv_heads + g) * kTileElems;
+        const uint16_t *base =
+            a.pool + (((int64_t)(valid ? b : 0) * 2 + is_v) * a.num_kv_heads + g) * (kBlock * D);
         const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<uint16_t *>(base), 0, valid ? kTileElems * 2 : 0, kBufferDword3P);
-        r.c[u] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, within * 16, 0, 0);
+            const_cast<uint16_t *>(base), 0, valid ? C::kTileBytes : 0, kBufferDword3P);
+        r.c[u] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, 0);
     }
 }
 
-// Write a loaded tile to LDS.  Slots at or past the session's last key (kv_len)
-// are zeroed here so that masked keys contribute exact zeros (never NaN) to PV.
+// LDS layouts of a staged key tile:
+//   K: [block 4][token 16][D/8 chunks of 16 B], chunk index XOR (token % (D/8)).
+//   V: [k2 2][g4 4][dim D] groups of 16 B = {block 2*k2, tokens 4*g4..4*g4+3;
+//      block 2*k2+1, the same tokens}: the 8 keys one lane feeds the PV MFMA.
+// Slots at or past the session's last key (kv_len) are zeroed here, so masked
+// keys contribute exact zeros (never NaN) to PV.
 template <int D>
-__device__ __forceinline__ void store_tile(TileRegs<D> &r, uint8_t *lds_k, uint8_t *lds_v, int tid,
-                                           int kt, int kv_len) {
-    constexpr int kChunksPerTile = kBlock * D * 2 / 16;
-    constexpr int kPerKV = 4 * kChunksPerTile;
+__device__ __forceinline__ void store_tile(const TileRegs<D> &r, uint8_t *lds_k, uint8_t *lds_v,
+                                           int tid, int kt, int kv_len) {
+    using C = TileCfg<D>;
     constexpr int kRowChunks = D / 8;
     const bool tail = (kt + 1) * kKeyTile > kv_len;
+    u32x4 v[C::kVPer];
+    int bi_v[C::kVPer], dim = 0, h = 0;
 #pragma unroll
-    for (int u = 0; u < TileRegs<D>::kChunks; ++u) {
-        const int c = tid + u * kPreThreads;
-        u32x4 v = r.c[u];
-        if (c < kPerKV) {
-            const int bi = c / kChunksPerTile;
-            const int within = c % kChunksPerTile;
+    for (int u = 0; u < C::kPerThread; ++u) {
+        if (u < C::kKPer) {
+            const int c = tid + u * kPreThreads;
+            const int bi = c / C::kCpt;
+            const int within = c % C::kCpt;
             const int token = within / kRowChunks;
             const int ch = within % kRowChunks;
-            if (tail && kt * kKeyTile + bi * kBlock + token >= kv_len) v = u32x4{0u, 0u, 0u, 0u};
+            u32x4 x = r.c[u];
+            if (tail && kt * kKeyTile + bi * kBlock + token >= kv_len) x = u32x4{0u, 0u, 0u, 0u};
             const int slot = ch ^ (token & (kRowChunks - 1));
-            *reinterpret_cast<u32x4 *>(lds_k + bi * (kBlock * D * 2) + token * (D * 2) + slot * 16) = v;
+            *reinterpret_cast<u32x4 *>(lds_k + bi * C::kTileBytes + token * (D * 2) + slot * 16) = x;
         } else {
-            const int cv = c - kPerKV;
+            const int e = u - C::kKPer;
+            v_chunk_coords<D>(tid, e, bi_v[e], dim, h);
+            v[e] = r.c[u];
             if (tail) {
-                // V chunk: 8 consecutive tokens of one dim
-                const int bi = cv / kChunksPerTile;
-                const int t0 = kt * kKeyTile + bi * kBlock + (cv & 1) * 8;
+                const int t0 = kt * kKeyTile + bi_v[e] * kBlock + h * 8;
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int t = t0 + 2 * e;
+                for (int w = 0; w < 4; ++w) {
+                    const int t = t0 + 2 * w;
                     const uint32_t mask = t + 1 < kv_len ? 0xFFFFFFFFu : (t < kv_len ? 0x0000FFFFu : 0u);
-                    v[e] &= mask;
+                    v[e][w] &= mask;
                 }
             }
-            *reinterpret_cast<u32x4 *>(lds_v + cv * 16) = v;
         }
+    }
+    // chunk words 0,1 hold tokens 8h..8h+3 (group g4 = 2h), words 2,3 the next four
+    if constexpr (C::kVPer == 2) {
+        const int k2 = bi_v[0] >> 1;
+        uint8_t *g0 = lds_v + ((k2 * 4 + 2 * h) * D + dim) * 16;
+        uint8_t *g1 = lds_v + ((k2 * 4 + 2 * h + 1) * D + dim) * 16;
+        *reinterpret_cast<u32x4 *>(g0) = u32x4{v[0][0], v[0][1], v[1][0], v[1][1]};
+        *reinterpret_cast<u32x4 *>(g1) = u32x4{v[0][2], v[0][3], v[1][2], v[1][3]};
+    } else {
+        const int k2 = bi_v[0] >> 1, half = bi_v[0] & 1;
+        uint8_t *g0 = lds_v + ((k2 * 4 + 2 * h) * D + dim) * 16 + half * 8;
+        uint8_t *g1 = lds_v + ((k2 * 4 + 2 * h + 1) * D + dim) * 16 + half * 8;
+        *reinterpret_cast<u32x2 *>(g0) = u32x2{v[0][0], v[0][1]};
+        *reinterpret_cast<u32x2 *>(g1) = u32x2{v[0][2], v[0][3]};
     }
 }
 
 template <int D>
-__global__ __launch_bounds__(kPreThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void prefill_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
+    using C = TileCfg<D>;
     constexpr int KS = D / 32;           // 32-dim k-steps of QK
     constexpr int NDT = D / 16;          // 16-dim output tiles
     constexpr int kRowChunks = D / 8;
-    constexpr int kTileBytes = kBlock * D * 2;
-    __shared__ __attribute__((aligned(16))) uint8_t lds[2][2][4 * kTileBytes];
+    __shared__ __attribute__((aligned(16))) uint8_t lds_k[2][4 * C::kTileBytes];
+    __shared__ __attribute__((aligned(16))) uint8_t lds_v[2][4 * C::kTileBytes];
+    __shared__ int64_t sm_work[kMaxSortSessions];
+    __shared__ int sm_order[kMaxSortSessions];
 
-    const int qt = blockIdx.x;
-    const int g = blockIdx.y;
-    const int s = blockIdx.z;
+    const int tid = threadIdx.x;
+    const int S = a.num_sessions;
     const int G = a.group;
-    const int qtok = kPreRows / G;       // new tokens per tile
+    const int qtok = kPreRows / G;       // new tokens per query tile
+    const int QT = a.qtiles;
+    const int Hkv = a.num_kv_heads;
+
+    // ---- XCD-aware placement: each XCD takes kXcdChunk consecutive items
+    const int64_t total = (int64_t)S * Hkv * QT;
+    const int64_t hw = blockIdx.x;
+    const int64_t slot = hw / kXcds;
+    const int64_t logical =
+        (slot / kXcdChunk) * (kXcds * kXcdChunk) + (hw % kXcds) * kXcdChunk + slot % kXcdChunk;
+    if (logical >= total) return;
+    const int qt = QT - 1 - (int)(logical % QT);
+    const int g = (int)((logical / QT) % Hkv);
+    const int rank = (int)(logical / ((int64_t)QT * Hkv));
+
+    // ---- session of this rank: longest (query tiles x keys) first, ties by index
+    int s = rank;
+    if (S <= kMaxSortSessions) {
+        if (tid < S) {
+            const int nt = a.cu[tid + 1] - a.cu[tid];
+            sm_work[tid] = (int64_t)((nt + qtok - 1) / qtok) * (a.ctx[tid] + nt);
+        }
+        __syncthreads();
+        if (tid < S) {
+            const int64_t w = sm_work[tid];
+            int r = 0;
+            for (int t = 0; t < S; ++t) {
+                const int64_t wt = sm_work[t];
+                r += (wt > w) || (wt == w && t < tid);
+            }
+            sm_order[r] = tid;
+        }
+        __syncthreads();
+        s = sm_order[rank];
+    }
+
     const int n = a.cu[s + 1] - a.cu[s];
     const int j0 = qt * qtok;
     if (j0 >= n) return;
@@ -151,17 +265,16 @@ void prefill_kernel(PrefillArgs a) {
     int nblk_valid = (kv_len + kBlock - 1) / kBlock;
     if (nblk_valid > a.max_blocks) {
         nblk_valid = a.max_blocks;
-        if (threadIdx.x == 0) flag_error(a.err, LS_DEVERR_LENGTH);
+        if (tid == 0) flag_error(a.err, LS_DEVERR_LENGTH);
     }
     const int kv_end = c + j_last + 1;                    // keys this tile can see
     const int ntiles = (kv_end + kKeyTile - 1) / kKeyTile;
 
-    const int tid = threadIdx.x;
-    const int wave = tid / kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
     const int lane = tid % kWave;
     const int c16 = lane & 15;
     const int g4 = lane >> 4;
-    const int hq_total = a.num_kv_heads * G;
+    const int hq_total = Hkv * G;
 
     // Rows of this lane (one per 16-row tile): r = wave*32 + rt*16 + c16.
     int row_lim[2];
@@ -181,12 +294,16 @@ void prefill_kernel(PrefillArgs a) {
         const uint16_t *qrow = a.q + row_out[rt];
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
-            qop[rt][ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(qrow + ks * 32 + g4 * 8));
+            qop[rt][ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(qrow + ks * 32 + g4 * 8));
     }
+    // Wait for q here, before the first tile loads are issued, so that no wait
+    // for q remains inside the key loop (vmcnt(0), other counters untouched).
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    // smallest causal limit among this wave's rows: key tiles past it need masking
     const int wave_lim_min = c + min(j0 + (wave * 32) / G, n - 1);
 
     float m[2] = {-INFINITY, -INFINITY};
-    float lsum[2] = {0.f, 0.f};
+    float lsum[2] = {0.f, 0.f};          // this lane's partial row sums
     f32x4 o[2][NDT];
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt)
@@ -194,104 +311,116 @@ void prefill_kernel(PrefillArgs a) {
         for (int dt = 0; dt < NDT; ++dt) o[rt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     const int32_t *table = a.block_tables + (int64_t)s * a.max_blocks;
-    TileRegs<D> regs;
-    load_tile<D>(regs, a, table, nblk_valid, g, 0, tid);
+    const float sl2 = a.scale_log2;
 
-    for (int kt = 0; kt < ntiles; ++kt) {
-        uint8_t *lk = lds[kt & 1][0];
-        uint8_t *lv = lds[kt & 1][1];
-        store_tile<D>(regs, lk, lv, tid, kt, kv_len);
+    // One 64-key tile, in two halves of 32 keys (one PV k-step each), so that
+    // only 32 keys' scores per row tile are live at once.
+    auto compute_tile = [&](int kt, const uint8_t *lk, const uint8_t *lv) {
+#pragma unroll
+        for (int k2 = 0; k2 < 2; ++k2) {
+            // ---- S^T = K Q^T for 2 key sub-tiles x 2 row tiles
+            f32x4 sacc[2][2];
+#pragma unroll
+            for (int sb = 0; sb < 2; ++sb) {
+                const int sub = 2 * k2 + sb;
+                sacc[0][sb] = f32x4{0.f, 0.f, 0.f, 0.f};
+                sacc[1][sb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) {
+                    const int ch = ks * 4 + g4;
+                    const int sl = ch ^ (c16 & (kRowChunks - 1));
+                    const bf16x8 kop = __builtin_bit_cast(
+                        bf16x8, *reinterpret_cast<const u32x4 *>(lk + sub * C::kTileBytes + c16 * (D * 2) + sl * 16));
+                    sacc[0][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[0][ks], sacc[0][sb], 0, 0, 0);
+                    sacc[1][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[1][ks], sacc[1][sb], 0, 0, 0);
+                }
+            }
+            // ---- online softmax per row, in log2 units (score * scale * log2 e);
+            // scale > 0 is checked on the host, so masking before scaling is exact.
+            const int key0 = kt * kKeyTile + k2 * 32;
+            const bool diag = key0 + 31 > wave_lim_min;
+            bf16x8 pop[2];
+#pragma unroll
+            for (int rt = 0; rt < 2; ++rt) {
+                if (diag) {
+#pragma unroll
+                    for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i)
+                            if (key0 + sb * 16 + g4 * 4 + i > row_lim[rt]) sacc[rt][sb][i] = -INFINITY;
+                }
+                float bm = fmaxf(fmaxf(fmaxf(sacc[rt][0][0], sacc[rt][0][1]), fmaxf(sacc[rt][0][2], sacc[rt][0][3])),
+                                 fmaxf(fmaxf(sacc[rt][1][0], sacc[rt][1][1]), fmaxf(sacc[rt][1][2], sacc[rt][1][3])));
+                bm = xmax16_32(bm) * sl2;
+                if (__any(bm > m[rt] + kRescaleSlack)) {
+                    const float m_new = fmaxf(m[rt], bm);
+                    const float alpha = __builtin_amdgcn_exp2f(m[rt] - m_new);
+                    lsum[rt] *= alpha;
+#pragma unroll
+                    for (int dt = 0; dt < NDT; ++dt) o[rt][dt] *= alpha;
+                    m[rt] = m_new;
+                }
+                const float nm = -m[rt];
+                float p[2][4];
+                float ps = 0.f;
+#pragma unroll
+                for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        p[sb][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[rt][sb][i], sl2, nm));
+                        ps += p[sb][i];
+                    }
+                lsum[rt] += ps;
+                pop[rt] = __builtin_bit_cast(bf16x8, u32x4{pack_bf16x2(p[0][0], p[0][1]), pack_bf16x2(p[0][2], p[0][3]),
+                                                           pack_bf16x2(p[1][0], p[1][1]), pack_bf16x2(p[1][2], p[1][3])});
+            }
+            // ---- O^T += V^T P^T
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) {
+                const bf16x8 vop = __builtin_bit_cast(
+                    bf16x8, *reinterpret_cast<const u32x4 *>(lv + ((k2 * 4 + g4) * D + dt * 16 + c16) * 16));
+                o[0][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[0], o[0][dt], 0, 0, 0);
+                o[1][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[1], o[1][dt], 0, 0, 0);
+            }
+        }
+    };
+
+    // ---- pipeline: while tile kt is computed from LDS, tile kt+1 waits in one
+    // register set and tile kt+2 is in flight into the other.
+    auto nvalid = [&](int kt) { return kt < ntiles ? nblk_valid : 0; };
+    TileRegs<D> ra, rb;
+    load_tile<D>(ra, a, table, nvalid(0), g, 0, tid);
+    load_tile<D>(rb, a, table, nvalid(1), g, 1, tid);
+    store_tile<D>(ra, lds_k[0], lds_v[0], tid, 0, kv_len);
+    load_tile<D>(ra, a, table, nvalid(2), g, 2, tid);
+    __syncthreads();
+    // Both halves of the body issue the same loads on every path (only the
+    // second compute is conditional), so outstanding loads are counted exactly.
+    for (int kt = 0; kt < ntiles; kt += 2) {
+        compute_tile(kt, lds_k[0], lds_v[0]);
+        store_tile<D>(rb, lds_k[1], lds_v[1], tid, kt + 1, kv_len);
+        load_tile<D>(rb, a, table, nvalid(kt + 3), g, kt + 3, tid);
         __syncthreads();
-        load_tile<D>(regs, a, table, kt + 1 < ntiles ? nblk_valid : 0, g, kt + 1, tid);
-
-        // ---- S^T = K Q^T for 4 key sub-tiles x 2 row tiles
-        f32x4 sacc[2][4];
-#pragma unroll
-        for (int sub = 0; sub < 4; ++sub) {
-            sacc[0][sub] = f32x4{0.f, 0.f, 0.f, 0.f};
-            sacc[1][sub] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const int ch = ks * 4 + g4;
-                const int slot = ch ^ (c16 & (kRowChunks - 1));
-                const bf16x8 kop = __builtin_bit_cast(
-                    bf16x8, *reinterpret_cast<const uint4 *>(lk + sub * kTileBytes + c16 * (D * 2) + slot * 16));
-                sacc[0][sub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[0][ks], sacc[0][sub], 0, 0, 0);
-                sacc[1][sub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[1][ks], sacc[1][sub], 0, 0, 0);
-            }
-        }
-
-        // ---- online softmax per row
-        const int key0 = kt * kKeyTile;
-        const bool diag = key0 + kKeyTile - 1 > wave_lim_min;
-        bf16x8 pop[2][2];
-#pragma unroll
-        for (int rt = 0; rt < 2; ++rt) {
-            float x[4][4];
-            float bm = -INFINITY;
-#pragma unroll
-            for (int sub = 0; sub < 4; ++sub)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    float v = sacc[rt][sub][i] * a.scale_log2;
-                    if (diag && key0 + sub * 16 + g4 * 4 + i > row_lim[rt]) v = -INFINITY;
-                    x[sub][i] = v;
-                    bm = fmaxf(bm, v);
-                }
-            bm = xmax16_32(bm);
-            const float m_new = fmaxf(m[rt], bm);
-            if (__any(m_new > m[rt])) {
-                const float alpha = __builtin_amdgcn_exp2f(m[rt] - m_new);
-                lsum[rt] *= alpha;
-#pragma unroll
-                for (int dt = 0; dt < NDT; ++dt) o[rt][dt] *= alpha;
-                m[rt] = m_new;
-            }
-            float ps = 0.f;
-            float p[4][4];
-#pragma unroll
-            for (int sub = 0; sub < 4; ++sub)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    p[sub][i] = __builtin_amdgcn_exp2f(x[sub][i] - m[rt]);
-                    ps += p[sub][i];
-                }
-            lsum[rt] += ps;
-#pragma unroll
-            for (int k2 = 0; k2 < 2; ++k2) {
-                const uint4 w = make_uint4(pack_bf16x2(p[2 * k2][0], p[2 * k2][1]),
-                                           pack_bf16x2(p[2 * k2][2], p[2 * k2][3]),
-                                           pack_bf16x2(p[2 * k2 + 1][0], p[2 * k2 + 1][1]),
-                                           pack_bf16x2(p[2 * k2 + 1][2], p[2 * k2 + 1][3]));
-                pop[rt][k2] = __builtin_bit_cast(bf16x8, w);
-            }
-        }
-
-        // ---- O^T += V^T P^T
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) {
-#pragma unroll
-            for (int k2 = 0; k2 < 2; ++k2) {
-                const uint2 va = *reinterpret_cast<const uint2 *>(lv + (2 * k2) * kTileBytes + (dt * 16 + c16) * 32 + g4 * 8);
-                const uint2 vb = *reinterpret_cast<const uint2 *>(lv + (2 * k2 + 1) * kTileBytes + (dt * 16 + c16) * 32 + g4 * 8);
-                const bf16x8 vop = __builtin_bit_cast(bf16x8, make_uint4(va.x, va.y, vb.x, vb.y));
-                o[0][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[0][k2], o[0][dt], 0, 0, 0);
-                o[1][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[1][k2], o[1][dt], 0, 0, 0);
-            }
-        }
+        if (kt + 1 < ntiles) compute_tile(kt + 1, lds_k[1], lds_v[1]);
+        store_tile<D>(ra, lds_k[0], lds_v[0], tid, kt + 2, kv_len);
+        load_tile<D>(ra, a, table, nvalid(kt + 4), g, kt + 4, tid);
+        __syncthreads();
     }
 
     // ---- normalise and write
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
-        const float inv = 1.f / xsum16_32(lsum[rt]);
+        float l = lsum[rt];
+        l += __shfl_xor(l, 16);
+        l += __shfl_xor(l, 32);
+        const float inv = 1.f / l;
         if (!row_ok[rt]) continue;
         uint16_t *orow = a.out + row_out[rt];
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) {
-            const uint2 w = make_uint2(pack_bf16x2(o[rt][dt][0] * inv, o[rt][dt][1] * inv),
-                                       pack_bf16x2(o[rt][dt][2] * inv, o[rt][dt][3] * inv));
-            *reinterpret_cast<uint2 *>(orow + dt * 16 + g4 * 4) = w;
+            const u32x2 w = u32x2{pack_bf16x2(o[rt][dt][0] * inv, o[rt][dt][1] * inv),
+                                  pack_bf16x2(o[rt][dt][2] * inv, o[rt][dt][3] * inv)};
+            *reinterpret_cast<u32x2 *>(orow + dt * 16 + g4 * 4) = w;
         }
     }
 }
@@ -309,6 +438,7 @@ hipError_t launch_prefill(const PoolGeom &p, int layer, int32_t num_sessions, in
     a.num_blocks = p.num_blocks;
     a.num_kv_heads = p.num_kv_heads;
     a.group = num_q_heads / p.num_kv_heads;
+    a.num_sessions = num_sessions;
     a.q = q;
     a.out = out;
     a.cu = cu_new_lens;
@@ -318,11 +448,17 @@ hipError_t launch_prefill(const PoolGeom &p, int layer, int32_t num_sessions, in
     a.scale_log2 = scale * kLog2eP;
     a.err = err;
     const int qtok = kPreRows / a.group;
-    dim3 grid((max_new_len + qtok - 1) / qtok, p.num_kv_heads, num_sessions);
+    a.qtiles = (max_new_len + qtok - 1) / qtok;
+    const int64_t items = (int64_t)num_sessions * p.num_kv_heads * a.qtiles;
+    // Whole groups of kXcds * kXcdChunk workgroups keep the placement map a
+    // bijection onto [0, grid); workgroups past the item count exit at once.
+    const int64_t per_group = (int64_t)kXcds * kXcdChunk;
+    const int64_t grid = (items + per_group - 1) / per_group * per_group;
+    if (grid > 0x7FFFFFFFLL) return hipErrorInvalidConfiguration;
     if (p.head_dim == 128)
-        hipLaunchKernelGGL(prefill_kernel<128>, grid, dim3(kPreThreads), 0, stream, a);
+        hipLaunchKernelGGL(prefill_kernel<128>, dim3((unsigned)grid), dim3(kPreThreads), 0, stream, a);
     else
-        hipLaunchKernelGGL(prefill_kernel<64>, grid, dim3(kPreThreads), 0, stream, a);
+        hipLaunchKernelGGL(prefill_kernel<64>, dim3((unsigned)grid), dim3(kPreThreads), 0, stream, a);
     return hipGetLastError();
 }
 

@@ -63,6 +63,22 @@ def test_prefill_ragged(kv, oracle_lib, d, hq, hkv):
     assert kv.ls_device_errors() == 0
 
 
+def test_prefill_many_sessions(kv, oracle_lib):
+    """More sessions than the in-kernel longest-first ordering handles (index
+    order), with empty turns mixed in."""
+    rng = np.random.default_rng(140)
+    d, hq, hkv = 64, 8, 2
+    n = rng.integers(0, 40, size=140)
+    n[0] = 39
+    c = rng.integers(0, 200, size=140)
+    pool, tables, q, kn, vn = _case(rng, n, c, hq, hkv, d)
+    dp = DevicePool(kv, pool, d)
+    out, cu = _run(kv, dp, q, kn, vn, n, c, tables, 0.125)
+    ref = oracle_lib.prefill(pool, 16, d, 0, q, kn, vn, cu, c, tables, 0.125)
+    assert_attn_close(out, ref, "prefill, 140 sessions")
+    assert kv.ls_device_errors() == 0
+
+
 def test_prefill_chunked_equals_whole_turn(kv):
     """Two chunks (c advanced by the first) give the same rows as one call."""
     rng = np.random.default_rng(12)
@@ -94,7 +110,7 @@ def test_next_turn_prefill_full_sampled(kv, oracle_lib):
     rows = set()
     for s in range(case.num_sessions):
         rows.update([int(cu[s]), int(cu[s + 1] - 1)])
-    rows.update(int(cu[0]) + j for j in (15, 16, 17, 127, 128))
+    rows.update(int(cu[0]) + j for j in (15, 16, 17, 31, 32, 33, 63, 64, 127, 128))
     rows.update(rng.integers(0, int(cu[-1]), size=40).tolist())
     rows = np.array(sorted(rows))
     ref = oracle_lib.prefill(case.pool.data, 16, 128, 0, case.q, case.k_new, case.v_new, cu,
