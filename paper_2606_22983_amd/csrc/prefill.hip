@@ -16,7 +16,8 @@
 //   O^T[16 dims x 16 rows] += V^T[16 x 32 keys] . P^T  (MFMA 16x16x32 bf16)
 // The S^T accumulator layout (lane: row = lane%16, keys 4*(lane/16)+i) is the
 // B-operand layout of the PV product, so P stays in registers (rounded to
-// bf16); softmax statistics stay in fp32.  A row's running max is raised (and its O and l
+// bf16; the row sums add up the same rounded values); softmax statistics stay
+// in fp32.  A row's running max is raised (and its O and l
 // rescaled) only when a tile's max exceeds it by more than 2^8, which keeps
 // every probability at most 256 and makes rescales rare.
 //
@@ -31,6 +32,7 @@ namespace ls {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -62,9 +64,29 @@ struct PrefillArgs {
     unsigned int *err;
 };
 
+// NaN-propagating maxima (v_maximum3_f32 on gfx950: no operand canonicalisation).
+__device__ __forceinline__ float fmax3(float a, float b, float c) {
+    return __builtin_elementwise_maximum(__builtin_elementwise_maximum(a, b), c);
+}
+
+// Max over the four lanes l, l^16, l^32, l^48 (the lanes holding one row's
+// scores) with the gfx950 row-swap permutes: VALU only, no LDS round trip.
 __device__ __forceinline__ float xmax16_32(float x) {
-    x = fmaxf(x, __shfl_xor(x, 16));
-    return fmaxf(x, __shfl_xor(x, 32));
+    const unsigned int u = __float_as_uint(x);
+    const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    const float y = __builtin_elementwise_maximum(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const unsigned int w = __float_as_uint(y);
+    const auto b = __builtin_amdgcn_permlane16_swap(w, w, false, false);
+    return __builtin_elementwise_maximum(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+__device__ __forceinline__ float xsum16_32(float x) {
+    const unsigned int u = __float_as_uint(x);
+    const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const unsigned int w = __float_as_uint(y);
+    const auto b = __builtin_amdgcn_permlane16_swap(w, w, false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
 // Thread -> 16-byte chunk assignment of one 64-key tile (4 blocks of K, then
@@ -87,6 +109,13 @@ struct TileCfg {
 template <int D>
 struct TileRegs {
     u32x4 c[TileCfg<D>::kPerThread];
+};
+
+// Block-table entries behind one thread's chunks of a key tile (uniform per
+// wave: every wave's chunks of one load lie in one block).
+template <int D>
+struct TileIds {
+    int32_t b[TileCfg<D>::kPerThread];
 };
 
 template <int D>
@@ -115,31 +144,49 @@ __device__ __forceinline__ int32_t table_entry(const int32_t *table, int jb, int
     return jb < nv ? b : -1;
 }
 
+template <int D>
+__device__ __forceinline__ int chunk_block(int tid, int u) {
+    using C = TileCfg<D>;
+    int bi;
+    if (u < C::kKPer) {
+        bi = (tid + u * kPreThreads) / C::kCpt;
+    } else {
+        int dim, h;
+        v_chunk_coords<D>(tid, u - C::kKPer, bi, dim, h);
+    }
+    return __builtin_amdgcn_readfirstlane(bi);   // uniform per wave by construction
+}
+
+// Read the block ids of key tile kt (scalar loads, issued a step before use).
+template <int D>
+__device__ __forceinline__ void fetch_ids(TileIds<D> &ids, const int32_t *table, int nblk_valid,
+                                          int kt, int tid) {
+#pragma unroll
+    for (int u = 0; u < TileCfg<D>::kPerThread; ++u)
+        ids.b[u] = table_entry(table, kt * 4 + chunk_block<D>(tid, u), nblk_valid);
+}
+
 // Issue the loads of one key tile into registers.  Blocks past the session's
 // keys (or with an id outside the pool) are read through a zero-size buffer
 // descriptor: no memory traffic, zeros returned.  Every call issues the same
 // loads, so outstanding loads can be counted across iterations.
 template <int D>
-__device__ __forceinline__ void load_tile(TileRegs<D> &r, const PrefillArgs &a, const int32_t *table,
-                                          int nblk_valid, int g, int kt, int tid) {
+__device__ __forceinline__ void load_tile(TileRegs<D> &r, const TileIds<D> &ids, const PrefillArgs &a,
+                                          int g, int tid) {
     using C = TileCfg<D>;
 #pragma unroll
     for (int u = 0; u < C::kPerThread; ++u) {
-        int bi, off, is_v;
+        int off, is_v;
         if (u < C::kKPer) {
-            const int c = tid + u * kPreThreads;
-            bi = c / C::kCpt;
-            off = (c % C::kCpt) * 16;
+            off = ((tid + u * kPreThreads) % C::kCpt) * 16;
             is_v = 0;
         } else {
-            int dim, h;
+            int bi, dim, h;
             v_chunk_coords<D>(tid, u - C::kKPer, bi, dim, h);
             off = (dim * 2 + h) * 16;
             is_v = 1;
         }
-        bi = __builtin_amdgcn_readfirstlane(bi);   // uniform per wave by construction
-        const int jb = kt * 4 + bi;
-        const int32_t b = table_entry(table, jb, nblk_valid);
+        const int32_t b = ids.b[u];
         const bool valid = b >= 0 && b < a.num_blocks;
         const uint16_t *base =
             a.pool + (((int64_t)(valid ? b : 0) * 2 + is_v) * a.num_kv_heads + g) * (kBlock * D);
@@ -302,8 +349,9 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     // smallest causal limit among this wave's rows: key tiles past it need masking
     const int wave_lim_min = c + min(j0 + (wave * 32) / G, n - 1);
 
-    float m[2] = {-INFINITY, -INFINITY};
-    float lsum[2] = {0.f, 0.f};          // this lane's partial row sums
+    float m[2] = {-INFINITY, -INFINITY};  // running row maxima (raw scores)
+    float nm[2] = {0.f, 0.f};             // -m * scale * log2(e)
+    float lsum[2] = {0.f, 0.f};           // this lane's partial row sums
     f32x4 o[2][NDT];
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt)
@@ -312,9 +360,12 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
 
     const int32_t *table = a.block_tables + (int64_t)s * a.max_blocks;
     const float sl2 = a.scale_log2;
+    const float slack_raw = kRescaleSlack / sl2;
+    const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
 
     // One 64-key tile, in two halves of 32 keys (one PV k-step each), so that
-    // only 32 keys' scores per row tile are live at once.
+    // only 32 keys' scores per row tile are live at once.  Row maxima m are
+    // kept in raw score units; nm = -m * scale * log2(e) is the exponent offset.
     auto compute_tile = [&](int kt, const uint8_t *lk, const uint8_t *lv) {
 #pragma unroll
         for (int k2 = 0; k2 < 2; ++k2) {
@@ -335,44 +386,45 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
                     sacc[1][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[1][ks], sacc[1][sb], 0, 0, 0);
                 }
             }
-            // ---- online softmax per row, in log2 units (score * scale * log2 e);
-            // scale > 0 is checked on the host, so masking before scaling is exact.
+            // ---- online softmax per row (scale > 0 is checked on the host, so
+            // masking and maxima commute with scaling)
             const int key0 = kt * kKeyTile + k2 * 32;
             const bool diag = key0 + 31 > wave_lim_min;
             bf16x8 pop[2];
 #pragma unroll
             for (int rt = 0; rt < 2; ++rt) {
                 if (diag) {
+                    // key key0 + sb*16 + 4*g4 + i is visible iff sb*16 + i <= lim
+                    const int lim = row_lim[rt] - key0 - 4 * g4;
 #pragma unroll
                     for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
                         for (int i = 0; i < 4; ++i)
-                            if (key0 + sb * 16 + g4 * 4 + i > row_lim[rt]) sacc[rt][sb][i] = -INFINITY;
+                            if (sb * 16 + i > lim) sacc[rt][sb][i] = -INFINITY;
                 }
-                float bm = fmaxf(fmaxf(fmaxf(sacc[rt][0][0], sacc[rt][0][1]), fmaxf(sacc[rt][0][2], sacc[rt][0][3])),
-                                 fmaxf(fmaxf(sacc[rt][1][0], sacc[rt][1][1]), fmaxf(sacc[rt][1][2], sacc[rt][1][3])));
-                bm = xmax16_32(bm) * sl2;
-                if (__any(bm > m[rt] + kRescaleSlack)) {
-                    const float m_new = fmaxf(m[rt], bm);
-                    const float alpha = __builtin_amdgcn_exp2f(m[rt] - m_new);
+                const f32x4 x0 = sacc[rt][0], x1 = sacc[rt][1];
+                float bm = fmax3(fmax3(x0[0], x0[1], x0[2]), fmax3(x0[3], x1[0], x1[1]), fmax3(x1[2], x1[3], x1[3]));
+                bm = xmax16_32(bm);
+                if (__any(bm > m[rt] + slack_raw)) {
+                    const float m_new = __builtin_elementwise_maximum(m[rt], bm);
+                    const float alpha = __builtin_amdgcn_exp2f((m[rt] - m_new) * sl2);
                     lsum[rt] *= alpha;
 #pragma unroll
                     for (int dt = 0; dt < NDT; ++dt) o[rt][dt] *= alpha;
                     m[rt] = m_new;
+                    nm[rt] = -m_new * sl2;
                 }
-                const float nm = -m[rt];
-                float p[2][4];
-                float ps = 0.f;
+                uint32_t w[4];
 #pragma unroll
-                for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        p[sb][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[rt][sb][i], sl2, nm));
-                        ps += p[sb][i];
-                    }
-                lsum[rt] += ps;
-                pop[rt] = __builtin_bit_cast(bf16x8, u32x4{pack_bf16x2(p[0][0], p[0][1]), pack_bf16x2(p[0][2], p[0][3]),
-                                                           pack_bf16x2(p[1][0], p[1][1]), pack_bf16x2(p[1][2], p[1][3])});
+                for (int j = 0; j < 4; ++j) {
+                    const f32x4 &x = j < 2 ? x0 : x1;
+                    const int i0 = 2 * (j & 1);
+                    const bf16x2 pk = {(__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(x[i0], sl2, nm[rt])),
+                                       (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(x[i0 + 1], sl2, nm[rt]))};
+                    lsum[rt] = __builtin_amdgcn_fdot2_f32_bf16(pk, ones2, lsum[rt], false);
+                    w[j] = __builtin_bit_cast(uint32_t, pk);
+                }
+                pop[rt] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
             }
             // ---- O^T += V^T P^T
 #pragma unroll
@@ -389,31 +441,34 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     // register set and tile kt+2 is in flight into the other.
     auto nvalid = [&](int kt) { return kt < ntiles ? nblk_valid : 0; };
     TileRegs<D> ra, rb;
-    load_tile<D>(ra, a, table, nvalid(0), g, 0, tid);
-    load_tile<D>(rb, a, table, nvalid(1), g, 1, tid);
+    TileIds<D> ids;
+    fetch_ids<D>(ids, table, nvalid(0), 0, tid);
+    load_tile<D>(ra, ids, a, g, tid);
+    fetch_ids<D>(ids, table, nvalid(1), 1, tid);
+    load_tile<D>(rb, ids, a, g, tid);
+    fetch_ids<D>(ids, table, nvalid(2), 2, tid);
     store_tile<D>(ra, lds_k[0], lds_v[0], tid, 0, kv_len);
-    load_tile<D>(ra, a, table, nvalid(2), g, 2, tid);
+    load_tile<D>(ra, ids, a, g, tid);
     __syncthreads();
     // Both halves of the body issue the same loads on every path (only the
     // second compute is conditional), so outstanding loads are counted exactly.
     for (int kt = 0; kt < ntiles; kt += 2) {
+        fetch_ids<D>(ids, table, nvalid(kt + 3), kt + 3, tid);
         compute_tile(kt, lds_k[0], lds_v[0]);
         store_tile<D>(rb, lds_k[1], lds_v[1], tid, kt + 1, kv_len);
-        load_tile<D>(rb, a, table, nvalid(kt + 3), g, kt + 3, tid);
+        load_tile<D>(rb, ids, a, g, tid);
         __syncthreads();
+        fetch_ids<D>(ids, table, nvalid(kt + 4), kt + 4, tid);
         if (kt + 1 < ntiles) compute_tile(kt + 1, lds_k[1], lds_v[1]);
         store_tile<D>(ra, lds_k[0], lds_v[0], tid, kt + 2, kv_len);
-        load_tile<D>(ra, a, table, nvalid(kt + 4), g, kt + 4, tid);
+        load_tile<D>(ra, ids, a, g, tid);
         __syncthreads();
     }
 
     // ---- normalise and write
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
-        float l = lsum[rt];
-        l += __shfl_xor(l, 16);
-        l += __shfl_xor(l, 32);
-        const float inv = 1.f / l;
+        const float inv = 1.f / xsum16_32(lsum[rt]);
         if (!row_ok[rt]) continue;
         uint16_t *orow = a.out + row_out[rt];
 #pragma unroll
