@@ -133,7 +133,7 @@ __device__ __forceinline__ void v_chunk_coords(int tid, int e, int &bi, int &dim
     h = (within >> 5) & 1;
 }
 
-// Entry jb of a session's block table, or -1 at or past nv entries.  The table
+// Entry jb of a session's block table, or -1 outside [0, nv).  The table
 // does not change during a launch, so it is read through the constant address
 // space: a scalar load, whose wait does not also wait for the tile loads in
 // flight.  The clamped index keeps the read inside the table row.
@@ -141,7 +141,9 @@ __device__ __forceinline__ int32_t table_entry(const int32_t *table, int jb, int
     typedef const __attribute__((address_space(4))) int32_t const_i32;
     const int jc = max(min(jb, nv - 1), 0);
     const int32_t b = ((const_i32 *)table)[jc];
-    return jb < nv ? b : -1;
+    // select by mask rather than by branch: the load stays unconditional
+    const int32_t keep = -(int32_t)((unsigned)jb < (unsigned)nv);
+    return b | ~keep;
 }
 
 template <int D>
@@ -157,16 +159,20 @@ __device__ __forceinline__ int chunk_block(int tid, int u) {
     return __builtin_amdgcn_readfirstlane(bi);   // uniform per wave by construction
 }
 
-// Read the block ids of key tile kt (scalar loads, issued a step before use).
+// Load set t = {K of blocks 4t+2 .. 4t+5, V of blocks 4t .. 4t+3}: the keys
+// are staged 32 ahead of the values (see the pipeline in prefill_kernel).
+// Read the block ids behind this thread's chunks of set t (scalar loads,
+// issued a step before use); blocks outside [0, nb) read as absent.
 template <int D>
-__device__ __forceinline__ void fetch_ids(TileIds<D> &ids, const int32_t *table, int nblk_valid,
-                                          int kt, int tid) {
+__device__ __forceinline__ void fetch_ids(TileIds<D> &ids, const int32_t *table, int t, int nb, int tid) {
 #pragma unroll
-    for (int u = 0; u < TileCfg<D>::kPerThread; ++u)
-        ids.b[u] = table_entry(table, kt * 4 + chunk_block<D>(tid, u), nblk_valid);
+    for (int u = 0; u < TileCfg<D>::kPerThread; ++u) {
+        const bool is_k = u < TileCfg<D>::kKPer;
+        ids.b[u] = table_entry(table, 4 * t + (is_k ? 2 : 0) + chunk_block<D>(tid, u), nb);
+    }
 }
 
-// Issue the loads of one key tile into registers.  Blocks past the session's
+// Issue the loads of one load set into registers.  Blocks past the session's
 // keys (or with an id outside the pool) are read through a zero-size buffer
 // descriptor: no memory traffic, zeros returned.  Every call issues the same
 // loads, so outstanding loads can be counted across iterations.
@@ -196,18 +202,23 @@ __device__ __forceinline__ void load_tile(TileRegs<D> &r, const TileIds<D> &ids,
     }
 }
 
-// LDS layouts of a staged key tile:
-//   K: [block 4][token 16][D/8 chunks of 16 B], chunk index XOR (token % (D/8)).
-//   V: [k2 2][g4 4][dim D] groups of 16 B = {block 2*k2, tokens 4*g4..4*g4+3;
-//      block 2*k2+1, the same tokens}: the 8 keys one lane feeds the PV MFMA.
-// Slots at or past the session's last key (kv_len) are zeroed here, so masked
-// keys contribute exact zeros (never NaN) to PV.
+// LDS layouts of staged keys and values (32-key units: unit u = blocks 2u, 2u+1):
+//   K: four unit slots, unit u in slot u % 4: [block 2][token 16][D/8 chunks
+//      of 16 B], chunk index XOR (token % (D/8)).
+//   V: one 64-key tile per buffer: [k2 2][g4 4][dim D] groups of 16 B =
+//      {block 2*k2, tokens 4*g4..4*g4+3; block 2*k2+1, the same tokens}: the
+//      8 keys one lane feeds the PV MFMA.
+// Token slots at or past the session's last key (kv_len) are zeroed here, so
+// masked keys contribute exact zeros (never NaN) to PV.
 template <int D>
 __device__ __forceinline__ void store_tile(const TileRegs<D> &r, uint8_t *lds_k, uint8_t *lds_v,
-                                           int tid, int kt, int kv_len) {
+                                           int tid, int t, int kv_len) {
     using C = TileCfg<D>;
     constexpr int kRowChunks = D / 8;
-    const bool tail = (kt + 1) * kKeyTile > kv_len;
+    const int key_k = (4 * t + 2) * kBlock;          // first key of the set's K blocks
+    const int key_v = 4 * t * kBlock;                // first key of its V blocks
+    const bool tail_k = key_k + kKeyTile > kv_len;
+    const bool tail_v = key_v + kKeyTile > kv_len;
     u32x4 v[C::kVPer];
     int bi_v[C::kVPer], dim = 0, h = 0;
 #pragma unroll
@@ -219,15 +230,17 @@ __device__ __forceinline__ void store_tile(const TileRegs<D> &r, uint8_t *lds_k,
             const int token = within / kRowChunks;
             const int ch = within % kRowChunks;
             u32x4 x = r.c[u];
-            if (tail && kt * kKeyTile + bi * kBlock + token >= kv_len) x = u32x4{0u, 0u, 0u, 0u};
+            if (tail_k && key_k + bi * kBlock + token >= kv_len) x = u32x4{0u, 0u, 0u, 0u};
             const int slot = ch ^ (token & (kRowChunks - 1));
-            *reinterpret_cast<u32x4 *>(lds_k + bi * C::kTileBytes + token * (D * 2) + slot * 16) = x;
+            const int unit_slot = (2 * t + 1 + (bi >> 1)) & 3;
+            *reinterpret_cast<u32x4 *>(lds_k + unit_slot * (2 * C::kTileBytes) + (bi & 1) * C::kTileBytes +
+                                       token * (D * 2) + slot * 16) = x;
         } else {
             const int e = u - C::kKPer;
             v_chunk_coords<D>(tid, e, bi_v[e], dim, h);
             v[e] = r.c[u];
-            if (tail) {
-                const int t0 = kt * kKeyTile + bi_v[e] * kBlock + h * 8;
+            if (tail_v) {
+                const int t0 = key_v + bi_v[e] * kBlock + h * 8;
 #pragma unroll
                 for (int w = 0; w < 4; ++w) {
                     const int t = t0 + 2 * w;
@@ -259,7 +272,7 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     constexpr int KS = D / 32;           // 32-dim k-steps of QK
     constexpr int NDT = D / 16;          // 16-dim output tiles
     constexpr int kRowChunks = D / 8;
-    __shared__ __attribute__((aligned(16))) uint8_t lds_k[2][4 * C::kTileBytes];
+    __shared__ __attribute__((aligned(16))) uint8_t lds_k[4 * 2 * C::kTileBytes];   // 4 unit slots
     __shared__ __attribute__((aligned(16))) uint8_t lds_v[2][4 * C::kTileBytes];
     __shared__ int64_t sm_work[kMaxSortSessions];
     __shared__ int sm_order[kMaxSortSessions];
@@ -363,105 +376,139 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     const float slack_raw = kRescaleSlack / sl2;
     const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
 
-    // One 64-key tile, in two halves of 32 keys (one PV k-step each), so that
-    // only 32 keys' scores per row tile are live at once.  Row maxima m are
-    // kept in raw score units; nm = -m * scale * log2(e) is the exponent offset.
-    auto compute_tile = [&](int kt, const uint8_t *lk, const uint8_t *lv) {
+    // ---- one 32-key unit of the key stream: S^T = K Q^T for 2 key sub-tiles x
+    // 2 row tiles into acc (K unit slot s of lds_k)
+    auto qk_unit = [&](f32x4 (&acc)[2][2], int slot_u) {
+        const uint8_t *lk = lds_k + slot_u * (2 * C::kTileBytes);
 #pragma unroll
-        for (int k2 = 0; k2 < 2; ++k2) {
-            // ---- S^T = K Q^T for 2 key sub-tiles x 2 row tiles
-            f32x4 sacc[2][2];
+        for (int sb = 0; sb < 2; ++sb) {
+            const int sub = sb;
+            acc[0][sb] = f32x4{0.f, 0.f, 0.f, 0.f};
+            acc[1][sb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int sb = 0; sb < 2; ++sb) {
-                const int sub = 2 * k2 + sb;
-                sacc[0][sb] = f32x4{0.f, 0.f, 0.f, 0.f};
-                sacc[1][sb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) {
-                    const int ch = ks * 4 + g4;
-                    const int sl = ch ^ (c16 & (kRowChunks - 1));
-                    const bf16x8 kop = __builtin_bit_cast(
-                        bf16x8, *reinterpret_cast<const u32x4 *>(lk + sub * C::kTileBytes + c16 * (D * 2) + sl * 16));
-                    sacc[0][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[0][ks], sacc[0][sb], 0, 0, 0);
-                    sacc[1][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[1][ks], sacc[1][sb], 0, 0, 0);
-                }
-            }
-            // ---- online softmax per row (scale > 0 is checked on the host, so
-            // masking and maxima commute with scaling)
-            const int key0 = kt * kKeyTile + k2 * 32;
-            const bool diag = key0 + 31 > wave_lim_min;
-            bf16x8 pop[2];
-#pragma unroll
-            for (int rt = 0; rt < 2; ++rt) {
-                if (diag) {
-                    // key key0 + sb*16 + 4*g4 + i is visible iff sb*16 + i <= lim
-                    const int lim = row_lim[rt] - key0 - 4 * g4;
-#pragma unroll
-                    for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-                        for (int i = 0; i < 4; ++i)
-                            if (sb * 16 + i > lim) sacc[rt][sb][i] = -INFINITY;
-                }
-                const f32x4 x0 = sacc[rt][0], x1 = sacc[rt][1];
-                float bm = fmax3(fmax3(x0[0], x0[1], x0[2]), fmax3(x0[3], x1[0], x1[1]), fmax3(x1[2], x1[3], x1[3]));
-                bm = xmax16_32(bm);
-                if (__any(bm > m[rt] + slack_raw)) {
-                    const float m_new = __builtin_elementwise_maximum(m[rt], bm);
-                    const float alpha = __builtin_amdgcn_exp2f((m[rt] - m_new) * sl2);
-                    lsum[rt] *= alpha;
-#pragma unroll
-                    for (int dt = 0; dt < NDT; ++dt) o[rt][dt] *= alpha;
-                    m[rt] = m_new;
-                    nm[rt] = -m_new * sl2;
-                }
-                uint32_t w[4];
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const f32x4 &x = j < 2 ? x0 : x1;
-                    const int i0 = 2 * (j & 1);
-                    const bf16x2 pk = {(__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(x[i0], sl2, nm[rt])),
-                                       (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(x[i0 + 1], sl2, nm[rt]))};
-                    lsum[rt] = __builtin_amdgcn_fdot2_f32_bf16(pk, ones2, lsum[rt], false);
-                    w[j] = __builtin_bit_cast(uint32_t, pk);
-                }
-                pop[rt] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
-            }
-            // ---- O^T += V^T P^T
-#pragma unroll
-            for (int dt = 0; dt < NDT; ++dt) {
-                const bf16x8 vop = __builtin_bit_cast(
-                    bf16x8, *reinterpret_cast<const u32x4 *>(lv + ((k2 * 4 + g4) * D + dt * 16 + c16) * 16));
-                o[0][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[0], o[0][dt], 0, 0, 0);
-                o[1][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[1], o[1][dt], 0, 0, 0);
+            for (int ks = 0; ks < KS; ++ks) {
+                const int ch = ks * 4 + g4;
+                const int sl = ch ^ (c16 & (kRowChunks - 1));
+                const bf16x8 kop = __builtin_bit_cast(
+                    bf16x8, *reinterpret_cast<const u32x4 *>(lk + sub * C::kTileBytes + c16 * (D * 2) + sl * 16));
+                acc[0][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[0][ks], acc[0][sb], 0, 0, 0);
+                acc[1][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[1][ks], acc[1][sb], 0, 0, 0);
             }
         }
     };
+    // Causal mask of a unit whose first key is key0, then its row maxima; a
+    // row max that exceeds the running max by more than the slack raises it
+    // and rescales O and l (rare after the first unit).  scale > 0 is checked
+    // on the host, so masking and maxima commute with scaling.
+    auto max_unit = [&](f32x4 (&acc)[2][2], int key0) {
+        const bool diag = key0 + 31 > wave_lim_min;
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt) {
+            if (diag) {
+                // key key0 + sb*16 + 4*g4 + i is visible iff sb*16 + i <= lim
+                const int lim = row_lim[rt] - key0 - 4 * g4;
+#pragma unroll
+                for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        if (sb * 16 + i > lim) acc[rt][sb][i] = -INFINITY;
+            }
+            const f32x4 x0 = acc[rt][0], x1 = acc[rt][1];
+            float bm = fmax3(fmax3(x0[0], x0[1], x0[2]), fmax3(x0[3], x1[0], x1[1]), fmax3(x1[2], x1[3], x1[3]));
+            bm = xmax16_32(bm);
+            if (__any(bm > m[rt] + slack_raw)) {
+                const float m_new = __builtin_elementwise_maximum(m[rt], bm);
+                const float alpha = __builtin_amdgcn_exp2f((m[rt] - m_new) * sl2);
+                lsum[rt] *= alpha;
+#pragma unroll
+                for (int dt = 0; dt < NDT; ++dt) o[rt][dt] *= alpha;
+                m[rt] = m_new;
+                nm[rt] = -m_new * sl2;
+            }
+        }
+    };
+    // P = exp2(S * scale * log2 e - m') in bf16 (B operand of PV) and row sums.
+    auto exp_unit = [&](const f32x4 (&acc)[2][2], bf16x8 (&pop)[2]) {
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt) {
+            uint32_t w[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const f32x4 &x = acc[rt][j >> 1];
+                const int i0 = 2 * (j & 1);
+                const bf16x2 pk = {(__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(x[i0], sl2, nm[rt])),
+                                   (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(x[i0 + 1], sl2, nm[rt]))};
+                lsum[rt] = __builtin_amdgcn_fdot2_f32_bf16(pk, ones2, lsum[rt], false);
+                w[j] = __builtin_bit_cast(uint32_t, pk);
+            }
+            pop[rt] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
+        }
+    };
+    // O^T += V^T P^T for unit half h of a V tile staged at lv.
+    auto pv_unit = [&](const bf16x8 (&pop)[2], const uint8_t *lv, int h) {
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+            const bf16x8 vop = __builtin_bit_cast(
+                bf16x8, *reinterpret_cast<const u32x4 *>(lv + ((h * 4 + g4) * D + dt * 16 + c16) * 16));
+            o[0][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[0], o[0][dt], 0, 0, 0);
+            o[1][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[1], o[1][dt], 0, 0, 0);
+        }
+    };
+    // One pipeline step: the scores of unit u (in cur, masked, max applied)
+    // become P and are accumulated while the scores of unit u+1 are computed
+    // into nxt.  exp/PV of u and QK of u+1 are independent, so the MFMAs of one
+    // interleave with the VALU work of the other.
+    auto unit_step = [&](f32x4 (&cur)[2][2], f32x4 (&nxt)[2][2], int slot_next, int key0_next,
+                         const uint8_t *lv, int h) {
+        bf16x8 pop[2];
+        qk_unit(nxt, slot_next);
+        exp_unit(cur, pop);
+        pv_unit(pop, lv, h);
+        max_unit(nxt, key0_next);
+    };
 
-    // ---- pipeline: while tile kt is computed from LDS, tile kt+1 waits in one
-    // register set and tile kt+2 is in flight into the other.
-    auto nvalid = [&](int kt) { return kt < ntiles ? nblk_valid : 0; };
+    // ---- pipeline over 32-key units.  Step u turns the scores of unit u into
+    // P, accumulates P V of unit u and computes the scores of unit u+1, so K
+    // is needed one unit ahead of V: while key tile j (units 2j, 2j+1) is
+    // processed, LDS holds V(j) in lds_v[j&1] and K units 2j+1, 2j+2 in their
+    // slots.  At the end of tile j, load set j+1 (K units 2j+3, 2j+4 and V tile
+    // j+1) goes from registers to LDS, into slots and a buffer that tile j
+    // does not read; it was loaded two tiles ahead (register sets ra, rb).
+    // One barrier per tile.
+    const int nb = min(nblk_valid, ntiles * 4);     // blocks any row here can see
     TileRegs<D> ra, rb;
     TileIds<D> ids;
-    fetch_ids<D>(ids, table, nvalid(0), 0, tid);
+    f32x4 sa[2][2], sb2[2][2];
+    fetch_ids<D>(ids, table, -1, nb, tid);          // set -1: K unit 0 only
     load_tile<D>(ra, ids, a, g, tid);
-    fetch_ids<D>(ids, table, nvalid(1), 1, tid);
+    fetch_ids<D>(ids, table, 0, nb, tid);
     load_tile<D>(rb, ids, a, g, tid);
-    fetch_ids<D>(ids, table, nvalid(2), 2, tid);
-    store_tile<D>(ra, lds_k[0], lds_v[0], tid, 0, kv_len);
-    load_tile<D>(ra, ids, a, g, tid);
+    fetch_ids<D>(ids, table, 1, nb, tid);
+    store_tile<D>(ra, lds_k, lds_v[1], tid, -1, kv_len);
+    load_tile<D>(ra, ids, a, g, tid);               // set 1
+    fetch_ids<D>(ids, table, 2, nb, tid);
+    store_tile<D>(rb, lds_k, lds_v[0], tid, 0, kv_len);
+    load_tile<D>(rb, ids, a, g, tid);               // set 2
     __syncthreads();
+    qk_unit(sa, 0);
+    max_unit(sa, 0);
     // Both halves of the body issue the same loads on every path (only the
-    // second compute is conditional), so outstanding loads are counted exactly.
-    for (int kt = 0; kt < ntiles; kt += 2) {
-        fetch_ids<D>(ids, table, nvalid(kt + 3), kt + 3, tid);
-        compute_tile(kt, lds_k[0], lds_v[0]);
-        store_tile<D>(rb, lds_k[1], lds_v[1], tid, kt + 1, kv_len);
-        load_tile<D>(rb, ids, a, g, tid);
+    // second tile's compute is conditional), so outstanding loads are counted
+    // exactly.  Unit slots: tile j reads slots (2j+1)%4 and (2j+2)%4.
+    for (int j = 0; j < ntiles; j += 2) {
+        fetch_ids<D>(ids, table, j + 3, nb, tid);
+        unit_step(sa, sb2, 1, j * kKeyTile + 32, lds_v[0], 0);
+        unit_step(sb2, sa, 2, (j + 1) * kKeyTile, lds_v[0], 1);
+        store_tile<D>(ra, lds_k, lds_v[1], tid, j + 1, kv_len);
+        load_tile<D>(ra, ids, a, g, tid);           // set j+3
         __syncthreads();
-        fetch_ids<D>(ids, table, nvalid(kt + 4), kt + 4, tid);
-        if (kt + 1 < ntiles) compute_tile(kt + 1, lds_k[1], lds_v[1]);
-        store_tile<D>(ra, lds_k[0], lds_v[0], tid, kt + 2, kv_len);
-        load_tile<D>(ra, ids, a, g, tid);
+        fetch_ids<D>(ids, table, j + 4, nb, tid);
+        if (j + 1 < ntiles) {
+            unit_step(sa, sb2, 3, (j + 1) * kKeyTile + 32, lds_v[1], 0);
+            unit_step(sb2, sa, 0, (j + 2) * kKeyTile, lds_v[1], 1);
+        }
+        store_tile<D>(rb, lds_k, lds_v[0], tid, j + 2, kv_len);
+        load_tile<D>(rb, ids, a, g, tid);           // set j+4
         __syncthreads();
     }
 
