@@ -8,18 +8,28 @@
 // Workgroup = (session, KV head g, query tile).  The tile packs the GQA group
 // into the row dimension: 256 rows = (256 / G) new tokens x G query heads
 // sharing KV head g, so each K/V tile staged in LDS feeds 256 query rows.
-// Eight wavefronts own 32 rows each (two 16-row MFMA tiles).  Keys stream in
-// tiles of 64 (four 16-token blocks): buffer loads into registers two tiles
-// ahead, then LDS (double buffered, one barrier per tile).
+// Eight wavefronts own 32 rows each (two 16-row MFMA tiles).
 //
+// Keys stream in 32-key units (two 16-token blocks):
 //   S^T[16 keys x 16 rows] = K[16 x D] . Q^T          (MFMA 16x16x32 bf16)
 //   O^T[16 dims x 16 rows] += V^T[16 x 32 keys] . P^T  (MFMA 16x16x32 bf16)
-// The S^T accumulator layout (lane: row = lane%16, keys 4*(lane/16)+i) is the
-// B-operand layout of the PV product, so P stays in registers (rounded to
-// bf16; the row sums add up the same rounded values); softmax statistics stay
-// in fp32.  A row's running max is raised (and its O and l
-// rescaled) only when a tile's max exceeds it by more than 2^8, which keeps
-// every probability at most 256 and makes rescales rare.
+// The 16 A-rows of each S^T MFMA are chosen so that lane group g4 (lanes
+// 16*g4 .. 16*g4+15) ends up holding the scores of keys 8*g4 .. 8*g4+7 of the
+// unit: those 8 keys are the 8 k-slots the same lane supplies as the B operand
+// of PV, and they are 8 consecutive tokens of one block, i.e. one 16-byte
+// chunk of the block's dim-major V tile.  So P stays in registers (rounded to
+// bf16; the row sums add up the same rounded values) and every MFMA operand is
+// one 16-byte LDS read.  Softmax statistics stay in fp32; a row's running max
+// is raised (and O, l rescaled) only when a unit's max exceeds it by more than
+// 2^8 (log2 units), which keeps every probability at most 256 and makes
+// rescales rare.
+//
+// Pipeline: step u turns unit u's scores into P and accumulates P V while the
+// scores of unit u+1 are computed, so the MFMAs of one half overlap the VALU
+// work of the other.  K therefore runs one unit ahead of V.  Data moves from
+// HBM straight into LDS (buffer loads with the LDS-destination form: no
+// register staging, no LDS write instructions), three 64-key stages deep, one
+// barrier per 64 keys.
 //
 // Workgroups run longest session first and, within a session, latest query
 // tile first (longest-processing-time order against the tail).  Consecutive
@@ -36,10 +46,12 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int kPreThreads = 512;
+constexpr int kPreWaves = kPreThreads / kWave;
 constexpr int kPreRows = 256;            // query rows per workgroup
-constexpr int kKeyTile = 64;             // keys per staged tile (4 blocks)
+constexpr int kKeyTile = 64;             // keys per pipeline stage (4 blocks)
 constexpr int kBufferDword3P = 0x00020000;   // raw buffer, 32-bit data format
 constexpr float kLog2eP = 1.4426950408889634f;
 constexpr float kRescaleSlack = 8.0f;    // log2 units a row max may lag behind
@@ -69,8 +81,8 @@ __device__ __forceinline__ float fmax3(float a, float b, float c) {
     return __builtin_elementwise_maximum(__builtin_elementwise_maximum(a, b), c);
 }
 
-// Max over the four lanes l, l^16, l^32, l^48 (the lanes holding one row's
-// scores) with the gfx950 row-swap permutes: VALU only, no LDS round trip.
+// Max / sum over the four lanes l, l^16, l^32, l^48 (the lanes holding one
+// row's scores) with the gfx950 row-swap permutes: VALU only.
 __device__ __forceinline__ float xmax16_32(float x) {
     const unsigned int u = __float_as_uint(x);
     const auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);
@@ -89,53 +101,9 @@ __device__ __forceinline__ float xsum16_32(float x) {
     return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
-// Thread -> 16-byte chunk assignment of one 64-key tile (4 blocks of K, then
-// 4 blocks of V).  K: chunk c = tid + u * threads, block c / kCpt, the chunk's
-// bytes are token-major (token = within / (D/8)).  V tiles are dim-major
-// ([D][16 tokens], two chunks per dim): each wave covers 32 dims, lanes 0..31
-// the first 8 tokens, lanes 32..63 the last 8.  With two V chunks per thread
-// (D = 128) a thread holds the same (dim, half) of blocks 2*k2 and 2*k2+1.
-template <int D>
-struct TileCfg {
-    static constexpr int kTileBytes = kBlock * D * 2;                  // one block's K (or V)
-    static constexpr int kCpt = kTileBytes / 16;                       // chunks per block tile
-    static constexpr int kPerThread = 2 * 4 * kCpt / kPreThreads;      // 4 (D=128) or 2 (D=64)
-    static constexpr int kKPer = kPerThread / 2;
-    static constexpr int kVPer = kPerThread / 2;
-    static_assert(kCpt % 64 == 0, "a wave's chunks must stay inside one block tile");
-    static_assert(kVPer == 1 || 4 * kCpt == 2 * kPreThreads, "V pairing needs 2 chunks per thread");
-};
-
-template <int D>
-struct TileRegs {
-    u32x4 c[TileCfg<D>::kPerThread];
-};
-
-// Block-table entries behind one thread's chunks of a key tile (uniform per
-// wave: every wave's chunks of one load lie in one block).
-template <int D>
-struct TileIds {
-    int32_t b[TileCfg<D>::kPerThread];
-};
-
-template <int D>
-__device__ __forceinline__ void v_chunk_coords(int tid, int e, int &bi, int &dim, int &h) {
-    using C = TileCfg<D>;
-    int within;
-    if constexpr (C::kVPer == 2) {
-        bi = 2 * (tid / C::kCpt) + e;
-        within = tid % C::kCpt;
-    } else {
-        bi = tid / C::kCpt;
-        within = tid % C::kCpt;
-    }
-    dim = (within >> 6) * 32 + (within & 31);
-    h = (within >> 5) & 1;
-}
-
-// Entry jb of a session's block table, or -1 outside [0, nv).  The table
-// does not change during a launch, so it is read through the constant address
-// space: a scalar load, whose wait does not also wait for the tile loads in
+// Entry jb of a session's block table, or -1 outside [0, nv).  The table does
+// not change during a launch, so it is read through the constant address
+// space: a scalar load, whose wait does not also wait for vector loads in
 // flight.  The clamped index keeps the read inside the table row.
 __device__ __forceinline__ int32_t table_entry(const int32_t *table, int jb, int nv) {
     typedef const __attribute__((address_space(4))) int32_t const_i32;
@@ -146,134 +114,74 @@ __device__ __forceinline__ int32_t table_entry(const int32_t *table, int jb, int
     return b | ~keep;
 }
 
+// Geometry of one pipeline stage ("load set" t = K of blocks 4t+2 .. 4t+5,
+// i.e. units 2t+1 and 2t+2, and V of blocks 4t .. 4t+3, i.e. key tile t).
+// Each wave moves whole kilobytes: 64 lanes x 16 bytes per load.
 template <int D>
-__device__ __forceinline__ int chunk_block(int tid, int u) {
-    using C = TileCfg<D>;
-    int bi;
-    if (u < C::kKPer) {
-        bi = (tid + u * kPreThreads) / C::kCpt;
-    } else {
-        int dim, h;
-        v_chunk_coords<D>(tid, u - C::kKPer, bi, dim, h);
-    }
-    return __builtin_amdgcn_readfirstlane(bi);   // uniform per wave by construction
+struct Geo {
+    static constexpr int kBlockBytes = kBlock * D * 2;           // one block's K (or V) of one head
+    static constexpr int kRowChunks = D / 8;                      // 16-byte chunks per K token row
+    static constexpr int kUnitBytes = 2 * kBlockBytes;            // K of one 32-key unit
+    static constexpr int kStageBytes = 4 * kBlockBytes;           // K (or V) of one stage
+    static constexpr int kKbPerBlock = kBlockBytes / 1024;        // 4 (D=128) or 2 (D=64)
+    static constexpr int kLoadsK = 4 * kKbPerBlock / kPreWaves;   // per wave per stage: 2 or 1
+    static constexpr int kLoads = 2 * kLoadsK;                    // K and V loads per wave per stage
+    static_assert(kLoadsK >= 1 && (4 * kKbPerBlock) % kPreWaves == 0, "stage must split evenly");
+};
+
+// K LDS layout of one block: [token 16][D/8 chunks], chunk ch of token t in
+// slot ch ^ kswz(block-in-unit, t).  The swizzle makes the 16 rows one S^T
+// MFMA reads (tokens {0..3, 8..11} + 4*sb of both blocks) hit distinct banks.
+template <int D>
+__device__ __forceinline__ int kswz(int b, int t) {
+    return ((t & 3) | (((t >> 3) & 1) << 2) | (b << 3)) & (Geo<D>::kRowChunks - 1);
 }
 
-// Load set t = {K of blocks 4t+2 .. 4t+5, V of blocks 4t .. 4t+3}: the keys
-// are staged 32 ahead of the values (see the pipeline in prefill_kernel).
-// Read the block ids behind this thread's chunks of set t (scalar loads,
-// issued a step before use); blocks outside [0, nb) read as absent.
+// V LDS layout of one block: 16-byte chunks (dim, half) = tokens 8*half ..
+// 8*half+7 of one dim, chunk at position 2*dim + (half ^ vswz(dim)), so that
+// 8 or 16 consecutive dims of one half hit distinct banks.
+__device__ __forceinline__ int vswz(int dim) { return ((dim >> 2) ^ (dim >> 3)) & 1; }
+
+// One wave's load of one kilobyte of a block into LDS (lane l writes bytes
+// 16*l .. 16*l+15 of dst).  Absent blocks (id -1 or outside the pool) are read
+// through a zero-size buffer descriptor: no memory traffic.
 template <int D>
-__device__ __forceinline__ void fetch_ids(TileIds<D> &ids, const int32_t *table, int t, int nb, int tid) {
-#pragma unroll
-    for (int u = 0; u < TileCfg<D>::kPerThread; ++u) {
-        const bool is_k = u < TileCfg<D>::kKPer;
-        ids.b[u] = table_entry(table, 4 * t + (is_k ? 2 : 0) + chunk_block<D>(tid, u), nb);
-    }
+__device__ __forceinline__ void load_kb(const PrefillArgs &a, int g, int32_t b, int is_v, uint8_t *dst,
+                                        int voff) {
+    const bool valid = b >= 0 && b < a.num_blocks;
+    const uint16_t *base =
+        a.pool + (((int64_t)(valid ? b : 0) * 2 + is_v) * a.num_kv_heads + g) * (kBlock * D);
+    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t *>(base), 0, valid ? Geo<D>::kBlockBytes : 0, kBufferDword3P);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void *)dst, 16, voff, 0, 0, 0);
 }
 
-// Issue the loads of one load set into registers.  Blocks past the session's
-// keys (or with an id outside the pool) are read through a zero-size buffer
-// descriptor: no memory traffic, zeros returned.  Every call issues the same
-// loads, so outstanding loads can be counted across iterations.
+// Barrier between pipeline stages.  Each wave first waits until its loads of
+// the next stage have landed (only the kLoads loads of the stage after it may
+// still be in flight) and its LDS reads have returned; the barrier then
+// publishes the next stage to all waves and frees the stage just read.  No
+// memory fence: a fence would also wait for the loads two stages ahead.
 template <int D>
-__device__ __forceinline__ void load_tile(TileRegs<D> &r, const TileIds<D> &ids, const PrefillArgs &a,
-                                          int g, int tid) {
-    using C = TileCfg<D>;
-#pragma unroll
-    for (int u = 0; u < C::kPerThread; ++u) {
-        int off, is_v;
-        if (u < C::kKPer) {
-            off = ((tid + u * kPreThreads) % C::kCpt) * 16;
-            is_v = 0;
-        } else {
-            int bi, dim, h;
-            v_chunk_coords<D>(tid, u - C::kKPer, bi, dim, h);
-            off = (dim * 2 + h) * 16;
-            is_v = 1;
-        }
-        const int32_t b = ids.b[u];
-        const bool valid = b >= 0 && b < a.num_blocks;
-        const uint16_t *base =
-            a.pool + (((int64_t)(valid ? b : 0) * 2 + is_v) * a.num_kv_heads + g) * (kBlock * D);
-        const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<uint16_t *>(base), 0, valid ? C::kTileBytes : 0, kBufferDword3P);
-        r.c[u] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, 0);
-    }
-}
-
-// LDS layouts of staged keys and values (32-key units: unit u = blocks 2u, 2u+1):
-//   K: four unit slots, unit u in slot u % 4: [block 2][token 16][D/8 chunks
-//      of 16 B], chunk index XOR (token % (D/8)).
-//   V: one 64-key tile per buffer: [k2 2][g4 4][dim D] groups of 16 B =
-//      {block 2*k2, tokens 4*g4..4*g4+3; block 2*k2+1, the same tokens}: the
-//      8 keys one lane feeds the PV MFMA.
-// Token slots at or past the session's last key (kv_len) are zeroed here, so
-// masked keys contribute exact zeros (never NaN) to PV.
-template <int D>
-__device__ __forceinline__ void store_tile(const TileRegs<D> &r, uint8_t *lds_k, uint8_t *lds_v,
-                                           int tid, int t, int kv_len) {
-    using C = TileCfg<D>;
-    constexpr int kRowChunks = D / 8;
-    const int key_k = (4 * t + 2) * kBlock;          // first key of the set's K blocks
-    const int key_v = 4 * t * kBlock;                // first key of its V blocks
-    const bool tail_k = key_k + kKeyTile > kv_len;
-    const bool tail_v = key_v + kKeyTile > kv_len;
-    u32x4 v[C::kVPer];
-    int bi_v[C::kVPer], dim = 0, h = 0;
-#pragma unroll
-    for (int u = 0; u < C::kPerThread; ++u) {
-        if (u < C::kKPer) {
-            const int c = tid + u * kPreThreads;
-            const int bi = c / C::kCpt;
-            const int within = c % C::kCpt;
-            const int token = within / kRowChunks;
-            const int ch = within % kRowChunks;
-            u32x4 x = r.c[u];
-            if (tail_k && key_k + bi * kBlock + token >= kv_len) x = u32x4{0u, 0u, 0u, 0u};
-            const int slot = ch ^ (token & (kRowChunks - 1));
-            const int unit_slot = (2 * t + 1 + (bi >> 1)) & 3;
-            *reinterpret_cast<u32x4 *>(lds_k + unit_slot * (2 * C::kTileBytes) + (bi & 1) * C::kTileBytes +
-                                       token * (D * 2) + slot * 16) = x;
-        } else {
-            const int e = u - C::kKPer;
-            v_chunk_coords<D>(tid, e, bi_v[e], dim, h);
-            v[e] = r.c[u];
-            if (tail_v) {
-                const int t0 = key_v + bi_v[e] * kBlock + h * 8;
-#pragma unroll
-                for (int w = 0; w < 4; ++w) {
-                    const int t = t0 + 2 * w;
-                    const uint32_t mask = t + 1 < kv_len ? 0xFFFFFFFFu : (t < kv_len ? 0x0000FFFFu : 0u);
-                    v[e][w] &= mask;
-                }
-            }
-        }
-    }
-    // chunk words 0,1 hold tokens 8h..8h+3 (group g4 = 2h), words 2,3 the next four
-    if constexpr (C::kVPer == 2) {
-        const int k2 = bi_v[0] >> 1;
-        uint8_t *g0 = lds_v + ((k2 * 4 + 2 * h) * D + dim) * 16;
-        uint8_t *g1 = lds_v + ((k2 * 4 + 2 * h + 1) * D + dim) * 16;
-        *reinterpret_cast<u32x4 *>(g0) = u32x4{v[0][0], v[0][1], v[1][0], v[1][1]};
-        *reinterpret_cast<u32x4 *>(g1) = u32x4{v[0][2], v[0][3], v[1][2], v[1][3]};
-    } else {
-        const int k2 = bi_v[0] >> 1, half = bi_v[0] & 1;
-        uint8_t *g0 = lds_v + ((k2 * 4 + 2 * h) * D + dim) * 16 + half * 8;
-        uint8_t *g1 = lds_v + ((k2 * 4 + 2 * h + 1) * D + dim) * 16 + half * 8;
-        *reinterpret_cast<u32x2 *>(g0) = u32x2{v[0][0], v[0][1]};
-        *reinterpret_cast<u32x2 *>(g1) = u32x2{v[0][2], v[0][3]};
-    }
+__device__ __forceinline__ void stage_barrier() {
+    // s_waitcnt vmcnt(kLoads) expcnt(7) lgkmcnt(0)
+    __builtin_amdgcn_s_waitcnt(0x0070 | Geo<D>::kLoads);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
 }
 
 template <int D>
 __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
-    using C = TileCfg<D>;
+    using C = Geo<D>;
     constexpr int KS = D / 32;           // 32-dim k-steps of QK
     constexpr int NDT = D / 16;          // 16-dim output tiles
-    constexpr int kRowChunks = D / 8;
-    __shared__ __attribute__((aligned(16))) uint8_t lds_k[4 * 2 * C::kTileBytes];   // 4 unit slots
-    __shared__ __attribute__((aligned(16))) uint8_t lds_v[2][4 * C::kTileBytes];
+    // Three stages; separate arrays let the compiler track each one's loads.
+    __shared__ __attribute__((aligned(1024))) uint8_t k0[C::kStageBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t k1[C::kStageBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t k2[C::kStageBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t v0[C::kStageBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t v1[C::kStageBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t v2[C::kStageBytes];
     __shared__ int64_t sm_work[kMaxSortSessions];
     __shared__ int sm_order[kMaxSortSessions];
 
@@ -329,6 +237,7 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     }
     const int kv_end = c + j_last + 1;                    // keys this tile can see
     const int ntiles = (kv_end + kKeyTile - 1) / kKeyTile;
+    const int nb = min(nblk_valid, ntiles * 4);           // blocks any row here can see
 
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
     const int lane = tid % kWave;
@@ -356,11 +265,40 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
         for (int ks = 0; ks < KS; ++ks)
             qop[rt][ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(qrow + ks * 32 + g4 * 8));
     }
-    // Wait for q here, before the first tile loads are issued, so that no wait
-    // for q remains inside the key loop (vmcnt(0), other counters untouched).
+    // Wait for q here, before the first stage loads are issued, so that no
+    // wait for q remains inside the key loop (vmcnt(0), other counters untouched).
     __builtin_amdgcn_s_waitcnt(0x0F70);
-    // smallest causal limit among this wave's rows: key tiles past it need masking
+    // smallest causal limit among this wave's rows: units past it need masking
     const int wave_lim_min = c + min(j0 + (wave * 32) / G, n - 1);
+
+    // ---- this wave's share of every stage: kLoadsK kilobytes of one K block
+    // and of one V block (block 'blk' of the stage), at fixed lane offsets.
+    const int blk = (wave * C::kLoadsK) / C::kKbPerBlock;
+    int k_voff[C::kLoadsK], v_voff[C::kLoadsK], kb_off[C::kLoadsK];
+#pragma unroll
+    for (int e = 0; e < C::kLoadsK; ++e) {
+        const int q = (wave * C::kLoadsK + e) % C::kKbPerBlock;       // kilobyte within the block
+        kb_off[e] = blk * C::kBlockBytes + q * 1024;
+        // K: lane -> (token, slot); fetch the chunk that belongs in that slot
+        const int t = q * (1024 / (D * 2)) + lane / C::kRowChunks;
+        const int sl = lane % C::kRowChunks;
+        k_voff[e] = t * (D * 2) + (sl ^ kswz<D>(blk & 1, t)) * 16;
+        // V: lane -> chunk position p = 2*dim + (half ^ vswz(dim))
+        const int p = q * 64 + lane;
+        const int dim = p >> 1;
+        v_voff[e] = dim * 32 + (((p & 1) ^ vswz(dim)) * 16);
+    }
+    const int32_t *table = a.block_tables + (int64_t)s * a.max_blocks;
+    auto load_k = [&](uint8_t *stage, int32_t b) {
+#pragma unroll
+        for (int e = 0; e < C::kLoadsK; ++e) load_kb<D>(a, g, b, 0, stage + kb_off[e], k_voff[e]);
+    };
+    auto load_v = [&](uint8_t *stage, int32_t b) {
+#pragma unroll
+        for (int e = 0; e < C::kLoadsK; ++e) load_kb<D>(a, g, b, 1, stage + kb_off[e], v_voff[e]);
+    };
+    auto id_k = [&](int t) { return table_entry(table, 4 * t + 2 + blk, nb); };
+    auto id_v = [&](int t) { return table_entry(table, 4 * t + blk, nb); };
 
     float m[2] = {-INFINITY, -INFINITY};  // running row maxima (raw scores)
     float nm[2] = {0.f, 0.f};             // -m * scale * log2(e)
@@ -370,48 +308,57 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) o[rt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    const int32_t *table = a.block_tables + (int64_t)s * a.max_blocks;
     const float sl2 = a.scale_log2;
     const float slack_raw = kRescaleSlack / sl2;
     const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
 
-    // ---- one 32-key unit of the key stream: S^T = K Q^T for 2 key sub-tiles x
-    // 2 row tiles into acc (K unit slot s of lds_k)
-    auto qk_unit = [&](f32x4 (&acc)[2][2], int slot_u) {
-        const uint8_t *lk = lds_k + slot_u * (2 * C::kTileBytes);
+    // ---- S^T = K Q^T of one 32-key unit (K of the unit at lk) for 2 key
+    // sub-tiles x 2 row tiles.  A-row r of sub-tile sb is token
+    // 8*((r>>2)&1) + 4*sb + (r&3) of block r>>3, i.e. unit key 8*(r>>2) + 4*sb + (r&3).
+    // Per-lane byte offsets of the K rows read for sub-tile sb and k-step ks,
+    // relative to the unit.  They are made opaque to the compiler so that no
+    // constant part is split off the address: the split loses the LDS alias
+    // information that lets these reads overlap the loads still in flight.
+    int kroff[2][KS];
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb) {
+        const int b = c16 >> 3;
+        const int t = 8 * ((c16 >> 2) & 1) + 4 * sb + (c16 & 3);
+        const int sw = kswz<D>(b, t);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            kroff[sb][ks] = b * C::kBlockBytes + t * (D * 2) + ((ks * 4 + g4) ^ sw) * 16;
+            asm volatile("" : "+v"(kroff[sb][ks]));
+        }
+    }
+    auto qk_unit = [&](f32x4 (&acc)[2][2], const uint8_t *lk) {
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb) {
-            const int sub = sb;
             acc[0][sb] = f32x4{0.f, 0.f, 0.f, 0.f};
             acc[1][sb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
-                const int ch = ks * 4 + g4;
-                const int sl = ch ^ (c16 & (kRowChunks - 1));
-                const bf16x8 kop = __builtin_bit_cast(
-                    bf16x8, *reinterpret_cast<const u32x4 *>(lk + sub * C::kTileBytes + c16 * (D * 2) + sl * 16));
+                const bf16x8 kop = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(lk + kroff[sb][ks]));
                 acc[0][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[0][ks], acc[0][sb], 0, 0, 0);
                 acc[1][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[1][ks], acc[1][sb], 0, 0, 0);
             }
         }
     };
-    // Causal mask of a unit whose first key is key0, then its row maxima; a
-    // row max that exceeds the running max by more than the slack raises it
-    // and rescales O and l (rare after the first unit).  scale > 0 is checked
-    // on the host, so masking and maxima commute with scaling.
+    // Causal mask of a unit whose first key is key0 (lane group g4 holds unit
+    // keys 8*g4 + 4*sb + i), then its row maxima; a row max that exceeds the
+    // running max by more than the slack raises it and rescales O and l.
+    // scale > 0 is checked on the host, so masking and maxima commute with scaling.
     auto max_unit = [&](f32x4 (&acc)[2][2], int key0) {
         const bool diag = key0 + 31 > wave_lim_min;
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt) {
             if (diag) {
-                // key key0 + sb*16 + 4*g4 + i is visible iff sb*16 + i <= lim
-                const int lim = row_lim[rt] - key0 - 4 * g4;
+                const int lim = row_lim[rt] - key0 - 8 * g4;
 #pragma unroll
                 for (int sb = 0; sb < 2; ++sb)
 #pragma unroll
                     for (int i = 0; i < 4; ++i)
-                        if (sb * 16 + i > lim) acc[rt][sb][i] = -INFINITY;
+                        if (4 * sb + i > lim) acc[rt][sb][i] = -INFINITY;
             }
             const f32x4 x0 = acc[rt][0], x1 = acc[rt][1];
             float bm = fmax3(fmax3(x0[0], x0[1], x0[2]), fmax3(x0[3], x1[0], x1[1]), fmax3(x1[2], x1[3], x1[3]));
@@ -444,72 +391,83 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
             pop[rt] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
         }
     };
-    // O^T += V^T P^T for unit half h of a V tile staged at lv.
-    auto pv_unit = [&](const bf16x8 (&pop)[2], const uint8_t *lv, int h) {
+    // O^T += V^T P^T for unit half h of the V tile at lv; the unit's first key
+    // is key0.  Keys at or past kv_len (unwritten or foreign pool contents)
+    // are zeroed in the operand, so 0 * NaN cannot reach O.
+    auto pv_unit = [&](const bf16x8 (&pop)[2], const uint8_t *lv, int h, int key0) {
+        const uint8_t *blkv = lv + (2 * h + (g4 >> 1)) * C::kBlockBytes;
+        const int half = g4 & 1;
+        const bool tail = key0 + 31 >= kv_len;
+        u32x4 vmask = u32x4{~0u, ~0u, ~0u, ~0u};
+        if (tail) {
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                const int kk = key0 + 8 * g4 + 2 * w;
+                vmask[w] = kk + 1 < kv_len ? 0xFFFFFFFFu : (kk < kv_len ? 0x0000FFFFu : 0u);
+            }
+        }
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) {
-            const bf16x8 vop = __builtin_bit_cast(
-                bf16x8, *reinterpret_cast<const u32x4 *>(lv + ((h * 4 + g4) * D + dt * 16 + c16) * 16));
+            const int dim = dt * 16 + c16;
+            u32x4 raw = *reinterpret_cast<const u32x4 *>(blkv + (2 * dim + (half ^ vswz(dim))) * 16);
+            if (tail) raw &= vmask;
+            const bf16x8 vop = __builtin_bit_cast(bf16x8, raw);
             o[0][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[0], o[0][dt], 0, 0, 0);
             o[1][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[1], o[1][dt], 0, 0, 0);
         }
     };
-    // One pipeline step: the scores of unit u (in cur, masked, max applied)
-    // become P and are accumulated while the scores of unit u+1 are computed
-    // into nxt.  exp/PV of u and QK of u+1 are independent, so the MFMAs of one
-    // interleave with the VALU work of the other.
-    auto unit_step = [&](f32x4 (&cur)[2][2], f32x4 (&nxt)[2][2], int slot_next, int key0_next,
-                         const uint8_t *lv, int h) {
-        bf16x8 pop[2];
-        qk_unit(nxt, slot_next);
-        exp_unit(cur, pop);
-        pv_unit(pop, lv, h);
-        max_unit(nxt, key0_next);
-    };
 
     // ---- pipeline over 32-key units.  Step u turns the scores of unit u into
-    // P, accumulates P V of unit u and computes the scores of unit u+1, so K
-    // is needed one unit ahead of V: while key tile j (units 2j, 2j+1) is
-    // processed, LDS holds V(j) in lds_v[j&1] and K units 2j+1, 2j+2 in their
-    // slots.  At the end of tile j, load set j+1 (K units 2j+3, 2j+4 and V tile
-    // j+1) goes from registers to LDS, into slots and a buffer that tile j
-    // does not read; it was loaded two tiles ahead (register sets ra, rb).
-    // One barrier per tile.
-    const int nb = min(nblk_valid, ntiles * 4);     // blocks any row here can see
-    TileRegs<D> ra, rb;
-    TileIds<D> ids;
+    // P, accumulates P V of unit u and computes the scores of unit u+1.  Key
+    // tile j (units 2j, 2j+1) reads stage j % 3: K units 2j+1, 2j+2 and V(j).
+    // While it is processed, the loads of stage j+2 are issued into the third
+    // buffer pair (read last in tile j-1); stage j+1 has landed by the barrier
+    // that ends tile j.
     f32x4 sa[2][2], sb2[2][2];
-    fetch_ids<D>(ids, table, -1, nb, tid);          // set -1: K unit 0 only
-    load_tile<D>(ra, ids, a, g, tid);
-    fetch_ids<D>(ids, table, 0, nb, tid);
-    load_tile<D>(rb, ids, a, g, tid);
-    fetch_ids<D>(ids, table, 1, nb, tid);
-    store_tile<D>(ra, lds_k, lds_v[1], tid, -1, kv_len);
-    load_tile<D>(ra, ids, a, g, tid);               // set 1
-    fetch_ids<D>(ids, table, 2, nb, tid);
-    store_tile<D>(rb, lds_k, lds_v[0], tid, 0, kv_len);
-    load_tile<D>(rb, ids, a, g, tid);               // set 2
-    __syncthreads();
-    qk_unit(sa, 0);
+    int32_t idk = id_k(-1), idv = id_v(-1);
+    load_k(k2, idk);                      // stage -1: K unit 0 (its V part is empty)
+    load_v(v2, idv);
+    idk = id_k(0); idv = id_v(0);
+    load_k(k0, idk);
+    load_v(v0, idv);
+    idk = id_k(1); idv = id_v(1);
+    load_k(k1, idk);
+    load_v(v1, idv);
+    idk = id_k(2); idv = id_v(2);
+    stage_barrier<D>();                   // stages -1 and 0 have landed
+    qk_unit(sa, k2 + C::kUnitBytes);      // unit 0 = second unit of stage -1
     max_unit(sa, 0);
-    // Both halves of the body issue the same loads on every path (only the
-    // second tile's compute is conditional), so outstanding loads are counted
-    // exactly.  Unit slots: tile j reads slots (2j+1)%4 and (2j+2)%4.
-    for (int j = 0; j < ntiles; j += 2) {
-        fetch_ids<D>(ids, table, j + 3, nb, tid);
-        unit_step(sa, sb2, 1, j * kKeyTile + 32, lds_v[0], 0);
-        unit_step(sb2, sa, 2, (j + 1) * kKeyTile, lds_v[0], 1);
-        store_tile<D>(ra, lds_k, lds_v[1], tid, j + 1, kv_len);
-        load_tile<D>(ra, ids, a, g, tid);           // set j+3
-        __syncthreads();
-        fetch_ids<D>(ids, table, j + 4, nb, tid);
-        if (j + 1 < ntiles) {
-            unit_step(sa, sb2, 3, (j + 1) * kKeyTile + 32, lds_v[1], 0);
-            unit_step(sb2, sa, 0, (j + 2) * kKeyTile, lds_v[1], 1);
+    stage_barrier<D>();                   // stage -1 fully read: k2/v2 are free
+
+    // Tile j: issue stage j+2 (ids fetched one tile earlier), compute, barrier.
+    // The loads are issued on every path, so outstanding loads are counted
+    // exactly; only the compute of tiles past the last one is skipped.
+    auto tile = [&](int j, const uint8_t *ks, const uint8_t *vs, uint8_t *kn, uint8_t *vn) {
+        const int32_t ik = idk, iv = idv;
+        idk = id_k(j + 3);
+        idv = id_v(j + 3);
+        if (j < ntiles) {
+            bf16x8 pop[2];
+            load_k(kn, ik);
+            qk_unit(sb2, ks);                       // scores of unit 2j+1
+            exp_unit(sa, pop);                      // P of unit 2j
+            pv_unit(pop, vs, 0, j * kKeyTile);
+            max_unit(sb2, j * kKeyTile + 32);
+            load_v(vn, iv);
+            qk_unit(sa, ks + C::kUnitBytes);        // scores of unit 2j+2
+            exp_unit(sb2, pop);                     // P of unit 2j+1
+            pv_unit(pop, vs, 1, j * kKeyTile + 32);
+            max_unit(sa, (j + 1) * kKeyTile);
+        } else {
+            load_k(kn, ik);
+            load_v(vn, iv);
         }
-        store_tile<D>(rb, lds_k, lds_v[0], tid, j + 2, kv_len);
-        load_tile<D>(rb, ids, a, g, tid);           // set j+4
-        __syncthreads();
+        stage_barrier<D>();
+    };
+    for (int j = 0; j < ntiles; j += 3) {
+        tile(j, k0, v0, k2, v2);
+        tile(j + 1, k1, v1, k0, v0);
+        tile(j + 2, k2, v2, k1, v1);
     }
 
     // ---- normalise and write
