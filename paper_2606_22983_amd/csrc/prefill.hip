@@ -8,7 +8,7 @@
 // Workgroup = (session, KV head g, query tile).  The tile packs the GQA group
 // into the row dimension: 256 rows = (256 / G) new tokens x G query heads
 // sharing KV head g, so each K/V tile staged in LDS feeds 256 query rows.
-// Eight wavefronts own 32 rows each (two 16-row MFMA tiles).
+// Each wavefront owns kRT 16-row MFMA tiles.
 //
 // Keys stream in 32-key units (two 16-token blocks):
 //   S^T[16 keys x 16 rows] = K[16 x D] . Q^T          (MFMA 16x16x32 bf16)
@@ -48,9 +48,11 @@ typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 
-constexpr int kPreThreads = 512;
-constexpr int kPreWaves = kPreThreads / kWave;
 constexpr int kPreRows = 256;            // query rows per workgroup
+constexpr int kRT = 2;                   // 16-row MFMA tiles per wavefront
+constexpr int kWaveRows = 16 * kRT;
+constexpr int kPreWaves = kPreRows / kWaveRows;
+constexpr int kPreThreads = kPreWaves * kWave;
 constexpr int kKeyTile = 64;             // keys per pipeline stage (4 blocks)
 constexpr int kBufferDword3P = 0x00020000;   // raw buffer, 32-bit data format
 constexpr float kLog2eP = 1.4426950408889634f;
@@ -246,13 +248,13 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     const int hq_total = Hkv * G;
 
     // Rows of this lane (one per 16-row tile): r = wave*32 + rt*16 + c16.
-    int row_lim[2];
-    int64_t row_out[2];
-    bool row_ok[2];
-    bf16x8 qop[2][KS];
+    int row_lim[kRT];
+    int64_t row_out[kRT];
+    bool row_ok[kRT];
+    bf16x8 qop[kRT][KS];
 #pragma unroll
-    for (int rt = 0; rt < 2; ++rt) {
-        const int r = wave * 32 + rt * 16 + c16;
+    for (int rt = 0; rt < kRT; ++rt) {
+        const int r = wave * kWaveRows + rt * 16 + c16;
         const int jl = j0 + r / G;
         const int h = r % G;
         row_ok[rt] = jl < n;
@@ -269,7 +271,7 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     // wait for q remains inside the key loop (vmcnt(0), other counters untouched).
     __builtin_amdgcn_s_waitcnt(0x0F70);
     // smallest causal limit among this wave's rows: units past it need masking
-    const int wave_lim_min = c + min(j0 + (wave * 32) / G, n - 1);
+    const int wave_lim_min = c + min(j0 + (wave * kWaveRows) / G, n - 1);
 
     // ---- this wave's share of every stage: kLoadsK kilobytes of one K block
     // and of one V block (block 'blk' of the stage), at fixed lane offsets.
@@ -300,12 +302,16 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     auto id_k = [&](int t) { return table_entry(table, 4 * t + 2 + blk, nb); };
     auto id_v = [&](int t) { return table_entry(table, 4 * t + blk, nb); };
 
-    float m[2] = {-INFINITY, -INFINITY};  // running row maxima (raw scores)
-    float nm[2] = {0.f, 0.f};             // -m * scale * log2(e)
-    float lsum[2] = {0.f, 0.f};           // this lane's partial row sums
-    f32x4 o[2][NDT];
+    float m[kRT], nm[kRT], lsum[kRT];     // running row maxima (raw scores),
+    f32x4 o[kRT][NDT];                    // -m * scale * log2(e), partial row sums
 #pragma unroll
-    for (int rt = 0; rt < 2; ++rt)
+    for (int rt = 0; rt < kRT; ++rt) {
+        m[rt] = -INFINITY;
+        nm[rt] = 0.f;
+        lsum[rt] = 0.f;
+    }
+#pragma unroll
+    for (int rt = 0; rt < kRT; ++rt)
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) o[rt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
     const float sl2 = a.scale_log2;
@@ -331,16 +337,17 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
             asm volatile("" : "+v"(kroff[sb][ks]));
         }
     }
-    auto qk_unit = [&](f32x4 (&acc)[2][2], const uint8_t *lk) {
+    auto qk_unit = [&](f32x4 (&acc)[kRT][2], const uint8_t *lk) {
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb) {
-            acc[0][sb] = f32x4{0.f, 0.f, 0.f, 0.f};
-            acc[1][sb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int rt = 0; rt < kRT; ++rt) acc[rt][sb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
                 const bf16x8 kop = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(lk + kroff[sb][ks]));
-                acc[0][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[0][ks], acc[0][sb], 0, 0, 0);
-                acc[1][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[1][ks], acc[1][sb], 0, 0, 0);
+#pragma unroll
+                for (int rt = 0; rt < kRT; ++rt)
+                    acc[rt][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[rt][ks], acc[rt][sb], 0, 0, 0);
             }
         }
     };
@@ -348,10 +355,10 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     // keys 8*g4 + 4*sb + i), then its row maxima; a row max that exceeds the
     // running max by more than the slack raises it and rescales O and l.
     // scale > 0 is checked on the host, so masking and maxima commute with scaling.
-    auto max_unit = [&](f32x4 (&acc)[2][2], int key0) {
+    auto max_unit = [&](f32x4 (&acc)[kRT][2], int key0) {
         const bool diag = key0 + 31 > wave_lim_min;
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt) {
+        for (int rt = 0; rt < kRT; ++rt) {
             if (diag) {
                 const int lim = row_lim[rt] - key0 - 8 * g4;
 #pragma unroll
@@ -375,9 +382,9 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
         }
     };
     // P = exp2(S * scale * log2 e - m') in bf16 (B operand of PV) and row sums.
-    auto exp_unit = [&](const f32x4 (&acc)[2][2], bf16x8 (&pop)[2]) {
+    auto exp_unit = [&](const f32x4 (&acc)[kRT][2], bf16x8 (&pop)[kRT]) {
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt) {
+        for (int rt = 0; rt < kRT; ++rt) {
             uint32_t w[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
@@ -394,26 +401,36 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     // O^T += V^T P^T for unit half h of the V tile at lv; the unit's first key
     // is key0.  Keys at or past kv_len (unwritten or foreign pool contents)
     // are zeroed in the operand, so 0 * NaN cannot reach O.
-    auto pv_unit = [&](const bf16x8 (&pop)[2], const uint8_t *lv, int h, int key0) {
-        const uint8_t *blkv = lv + (2 * h + (g4 >> 1)) * C::kBlockBytes;
-        const int half = g4 & 1;
-        const bool tail = key0 + 31 >= kv_len;
-        u32x4 vmask = u32x4{~0u, ~0u, ~0u, ~0u};
-        if (tail) {
+    // Per-lane byte offset of the V chunk this lane reads (dims dt*16 + c16
+    // differ from it by the constant dt*512), opaque for the same reason as kroff.
+    int vroff = (g4 >> 1) * C::kBlockBytes + (2 * c16 + ((g4 & 1) ^ vswz(c16))) * 16;
+    asm volatile("" : "+v"(vroff));
+    auto pv_unit = [&](const bf16x8 (&pop)[kRT], const uint8_t *lv, int h, int key0) {
+        const uint8_t *blkv = lv + 2 * h * C::kBlockBytes + vroff;
+        // dim = dt*16 + c16 has the same swizzle bit as c16: chunks dt*512 apart
+        if (key0 + 31 < kv_len) {
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) {
+                const bf16x8 vop = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(blkv + dt * 512));
+#pragma unroll
+                for (int rt = 0; rt < kRT; ++rt)
+                    o[rt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[rt], o[rt][dt], 0, 0, 0);
+            }
+        } else {
+            u32x4 vmask;
 #pragma unroll
             for (int w = 0; w < 4; ++w) {
                 const int kk = key0 + 8 * g4 + 2 * w;
                 vmask[w] = kk + 1 < kv_len ? 0xFFFFFFFFu : (kk < kv_len ? 0x0000FFFFu : 0u);
             }
-        }
 #pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) {
-            const int dim = dt * 16 + c16;
-            u32x4 raw = *reinterpret_cast<const u32x4 *>(blkv + (2 * dim + (half ^ vswz(dim))) * 16);
-            if (tail) raw &= vmask;
-            const bf16x8 vop = __builtin_bit_cast(bf16x8, raw);
-            o[0][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[0], o[0][dt], 0, 0, 0);
-            o[1][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[1], o[1][dt], 0, 0, 0);
+            for (int dt = 0; dt < NDT; ++dt) {
+                const u32x4 raw = *reinterpret_cast<const u32x4 *>(blkv + dt * 512) & vmask;
+                const bf16x8 vop = __builtin_bit_cast(bf16x8, raw);
+#pragma unroll
+                for (int rt = 0; rt < kRT; ++rt)
+                    o[rt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[rt], o[rt][dt], 0, 0, 0);
+            }
         }
     };
 
@@ -423,7 +440,7 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     // While it is processed, the loads of stage j+2 are issued into the third
     // buffer pair (read last in tile j-1); stage j+1 has landed by the barrier
     // that ends tile j.
-    f32x4 sa[2][2], sb2[2][2];
+    f32x4 sa[kRT][2], sb2[kRT][2];
     int32_t idk = id_k(-1), idv = id_v(-1);
     load_k(k2, idk);                      // stage -1: K unit 0 (its V part is empty)
     load_v(v2, idv);
@@ -446,21 +463,21 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
         const int32_t ik = idk, iv = idv;
         idk = id_k(j + 3);
         idv = id_v(j + 3);
-        if (j < ntiles) {
-            bf16x8 pop[2];
-            load_k(kn, ik);
+        const bool live = j < ntiles;
+        bf16x8 pop[kRT];
+        load_k(kn, ik);
+        if (live) {
             qk_unit(sb2, ks);                       // scores of unit 2j+1
             exp_unit(sa, pop);                      // P of unit 2j
             pv_unit(pop, vs, 0, j * kKeyTile);
             max_unit(sb2, j * kKeyTile + 32);
-            load_v(vn, iv);
+        }
+        load_v(vn, iv);
+        if (live) {
             qk_unit(sa, ks + C::kUnitBytes);        // scores of unit 2j+2
             exp_unit(sb2, pop);                     // P of unit 2j+1
             pv_unit(pop, vs, 1, j * kKeyTile + 32);
             max_unit(sa, (j + 1) * kKeyTile);
-        } else {
-            load_k(kn, ik);
-            load_v(vn, iv);
         }
         stage_barrier<D>();
     };
@@ -472,7 +489,7 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
 
     // ---- normalise and write
 #pragma unroll
-    for (int rt = 0; rt < 2; ++rt) {
+    for (int rt = 0; rt < kRT; ++rt) {
         const float inv = 1.f / xsum16_32(lsum[rt]);
         if (!row_ok[rt]) continue;
         uint16_t *orow = a.out + row_out[rt];
