@@ -31,10 +31,9 @@
 // register staging, no LDS write instructions), three 64-key stages deep, one
 // barrier per 64 keys.
 //
-// Workgroups run longest session first and, within a session, latest query
-// tile first (longest-processing-time order against the tail).  Consecutive
-// query tiles of one (session, KV head) are placed on the same XCD so that
-// they share its L2.
+// Scheduling: all query tiles of one (session, KV head) pair run on one XCD,
+// so they stream the same keys through its L2; pairs are dealt to XCDs
+// longest first (see the schedule in prefill_kernel).
 #include "common.h"
 
 namespace ls {
@@ -58,8 +57,7 @@ constexpr int kBufferDword3P = 0x00020000;   // raw buffer, 32-bit data format
 constexpr float kLog2eP = 1.4426950408889634f;
 constexpr float kRescaleSlack = 8.0f;    // log2 units a row max may lag behind
 constexpr int kXcds = 8;                 // workgroups are dispatched round-robin over XCDs
-constexpr int kXcdChunk = 8;             // consecutive items kept on one XCD
-constexpr int kMaxSortSessions = 128;    // larger batches run in index order
+constexpr int kMaxPairs = 512;           // (session, KV head) pairs scheduled; more run in index order
 
 struct PrefillArgs {
     const uint16_t *pool;          // layer base
@@ -184,8 +182,9 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     __shared__ __attribute__((aligned(1024))) uint8_t v0[C::kStageBytes];
     __shared__ __attribute__((aligned(1024))) uint8_t v1[C::kStageBytes];
     __shared__ __attribute__((aligned(1024))) uint8_t v2[C::kStageBytes];
-    __shared__ int64_t sm_work[kMaxSortSessions];
-    __shared__ int sm_order[kMaxSortSessions];
+    __shared__ int64_t sm_work[kMaxPairs];
+    __shared__ int sm_items[kMaxPairs];
+    __shared__ int sm_order[kMaxPairs];
 
     const int tid = threadIdx.x;
     const int S = a.num_sessions;
@@ -194,36 +193,57 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     const int QT = a.qtiles;
     const int Hkv = a.num_kv_heads;
 
-    // ---- XCD-aware placement: each XCD takes kXcdChunk consecutive items
-    const int64_t total = (int64_t)S * Hkv * QT;
-    const int64_t hw = blockIdx.x;
-    const int64_t slot = hw / kXcds;
-    const int64_t logical =
-        (slot / kXcdChunk) * (kXcds * kXcdChunk) + (hw % kXcds) * kXcdChunk + slot % kXcdChunk;
-    if (logical >= total) return;
-    const int qt = QT - 1 - (int)(logical % QT);
-    const int g = (int)((logical / QT) % Hkv);
-    const int rank = (int)(logical / ((int64_t)QT * Hkv));
-
-    // ---- session of this rank: longest (query tiles x keys) first, ties by index
-    int s = rank;
-    if (S <= kMaxSortSessions) {
-        if (tid < S) {
-            const int nt = a.cu[tid + 1] - a.cu[tid];
-            sm_work[tid] = (int64_t)((nt + qtok - 1) / qtok) * (a.ctx[tid] + nt);
+    // ---- schedule.  Items are (session s, KV head g, query tile qt).  All query
+    // tiles of one (s, g) pair run on one XCD, so they stream the same keys
+    // through its L2 at about the same time.  Pairs are dealt to the 8 XCDs in
+    // snake order of decreasing work (longest-processing-time first); an XCD
+    // runs its pairs in that order, each pair's latest (longest) query tile
+    // first.  Workgroup i is dispatched to XCD i % 8 and is the (i / 8)-th
+    // item there; every workgroup derives the same schedule from the lengths.
+    const int P = S * Hkv;
+    int s, g, qt;
+    if (P <= kMaxPairs) {
+        for (int p = tid; p < P; p += kPreThreads) {
+            const int sp = p / Hkv;
+            const int nt = max(a.cu[sp + 1] - a.cu[sp], 0);
+            const int items = (nt + qtok - 1) / qtok;
+            sm_items[p] = items;
+            sm_work[p] = (int64_t)items * (2 * (int64_t)max(a.ctx[sp], 0) + nt);
         }
         __syncthreads();
-        if (tid < S) {
-            const int64_t w = sm_work[tid];
+        for (int p = tid; p < P; p += kPreThreads) {
+            const int64_t w = sm_work[p];
             int r = 0;
-            for (int t = 0; t < S; ++t) {
-                const int64_t wt = sm_work[t];
-                r += (wt > w) || (wt == w && t < tid);
+            for (int q = 0; q < P; ++q) {
+                const int64_t wq = sm_work[q];
+                r += (wq > w) || (wq == w && q < p);
             }
-            sm_order[r] = tid;
+            sm_order[r] = p;
         }
         __syncthreads();
-        s = sm_order[rank];
+        const int xcd = (int)(blockIdx.x % kXcds);
+        int slot = (int)(blockIdx.x / kXcds);
+        int pick = -1;
+        for (int k = 0; kXcds * k < P; ++k) {
+            const int r = kXcds * k + ((k & 1) ? kXcds - 1 - xcd : xcd);
+            if (r >= P) break;
+            const int cnt = sm_items[sm_order[r]];
+            if (slot < cnt) {
+                pick = sm_order[r];
+                break;
+            }
+            slot -= cnt;
+        }
+        if (pick < 0) return;
+        s = pick / Hkv;
+        g = pick % Hkv;
+        qt = sm_items[pick] - 1 - slot;
+    } else {
+        const int64_t lg = blockIdx.x;
+        if (lg >= (int64_t)S * Hkv * QT) return;
+        qt = QT - 1 - (int)(lg % QT);
+        g = (int)((lg / QT) % Hkv);
+        s = (int)(lg / ((int64_t)QT * Hkv));
     }
 
     const int n = a.cu[s + 1] - a.cu[s];
@@ -526,11 +546,10 @@ hipError_t launch_prefill(const PoolGeom &p, int layer, int32_t num_sessions, in
     a.err = err;
     const int qtok = kPreRows / a.group;
     a.qtiles = (max_new_len + qtok - 1) / qtok;
-    const int64_t items = (int64_t)num_sessions * p.num_kv_heads * a.qtiles;
-    // Whole groups of kXcds * kXcdChunk workgroups keep the placement map a
-    // bijection onto [0, grid); workgroups past the item count exit at once.
-    const int64_t per_group = (int64_t)kXcds * kXcdChunk;
-    const int64_t grid = (items + per_group - 1) / per_group * per_group;
+    // An XCD holds at most ceil(pairs / 8) pairs of at most qtiles items each;
+    // workgroups past an XCD's item count exit at once.
+    const int64_t pairs = (int64_t)num_sessions * p.num_kv_heads;
+    const int64_t grid = (pairs + kXcds - 1) / kXcds * kXcds * a.qtiles;
     if (grid > 0x7FFFFFFFLL) return hipErrorInvalidConfiguration;
     if (p.head_dim == 128)
         hipLaunchKernelGGL(prefill_kernel<128>, dim3((unsigned)grid), dim3(kPreThreads), 0, stream, a);
