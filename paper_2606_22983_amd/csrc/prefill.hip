@@ -138,9 +138,8 @@ __device__ __forceinline__ int kswz(int b, int t) {
 }
 
 // V LDS layout of one block: 16-byte chunks (dim, half) = tokens 8*half ..
-// 8*half+7 of one dim, chunk at position 2*dim + (half ^ vswz(dim)), so that
-// 8 or 16 consecutive dims of one half hit distinct banks.
-__device__ __forceinline__ int vswz(int dim) { return ((dim >> 2) ^ (dim >> 3)) & 1; }
+// 8*half+7 of one dim, chunk at position half*D + dim: the 16 lanes that read
+// one (half, 16 dims) read 256 contiguous bytes.
 
 // One wave's load of one kilobyte of a block into LDS (lane l writes bytes
 // 16*l .. 16*l+15 of dst).  Absent blocks (id -1 or outside the pool) are read
@@ -305,10 +304,9 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
         const int t = q * (1024 / (D * 2)) + lane / C::kRowChunks;
         const int sl = lane % C::kRowChunks;
         k_voff[e] = t * (D * 2) + (sl ^ kswz<D>(blk & 1, t)) * 16;
-        // V: lane -> chunk position p = 2*dim + (half ^ vswz(dim))
+        // V: lane -> chunk position p = half*D + dim
         const int p = q * 64 + lane;
-        const int dim = p >> 1;
-        v_voff[e] = dim * 32 + (((p & 1) ^ vswz(dim)) * 16);
+        v_voff[e] = (p % D) * 32 + (p / D) * 16;
     }
     const int32_t *table = a.block_tables + (int64_t)s * a.max_blocks;
     auto load_k = [&](uint8_t *stage, int32_t b) {
@@ -418,40 +416,45 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
             pop[rt] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
         }
     };
-    // O^T += V^T P^T for unit half h of the V tile at lv; the unit's first key
-    // is key0.  Keys at or past kv_len (unwritten or foreign pool contents)
-    // are zeroed in the operand, so 0 * NaN cannot reach O.
-    // Per-lane byte offset of the V chunk this lane reads (dims dt*16 + c16
-    // differ from it by the constant dt*512), opaque for the same reason as kroff.
-    int vroff = (g4 >> 1) * C::kBlockBytes + (2 * c16 + ((g4 & 1) ^ vswz(c16))) * 16;
+    // Per-lane byte offset of the V chunk this lane reads, opaque for the same
+    // reason as kroff.
+    int vroff = (g4 >> 1) * C::kBlockBytes + ((g4 & 1) * D + c16) * 16;
     asm volatile("" : "+v"(vroff));
-    auto pv_unit = [&](const bf16x8 (&pop)[kRT], const uint8_t *lv, int h, int key0) {
+    // O^T += V^T P^T for unit half h of the V tile at lv (dims dt*16 + c16 of
+    // one lane are 256 bytes apart).
+    auto pv_unit = [&](const bf16x8 (&pop)[kRT], const uint8_t *lv, int h) {
         const uint8_t *blkv = lv + 2 * h * C::kBlockBytes + vroff;
-        // dim = dt*16 + c16 has the same swizzle bit as c16: chunks dt*512 apart
-        if (key0 + 31 < kv_len) {
 #pragma unroll
-            for (int dt = 0; dt < NDT; ++dt) {
-                const bf16x8 vop = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(blkv + dt * 512));
+        for (int dt = 0; dt < NDT; ++dt) {
+            const bf16x8 vop = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(blkv + dt * 256));
 #pragma unroll
-                for (int rt = 0; rt < kRT; ++rt)
-                    o[rt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[rt], o[rt][dt], 0, 0, 0);
-            }
-        } else {
-            u32x4 vmask;
+            for (int rt = 0; rt < kRT; ++rt)
+                o[rt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[rt], o[rt][dt], 0, 0, 0);
+        }
+    };
+    // Values of keys at or past kv_len (the rest of the session's last block,
+    // or blocks never loaded) are zeroed in the staged V tile of key tile j
+    // before it is used, so that 0 * NaN cannot reach O.  Only the last key
+    // tile can hold such keys; one extra LDS barrier, once per workgroup.
+    auto zero_v_tail = [&](uint8_t *lv, int j) {
+        constexpr int kChunks = 4 * 2 * D;                    // (block, half, dim) chunks of 8 tokens
+        for (int ci = tid; ci < kChunks; ci += kPreThreads) {
+            const int bi = ci / (2 * D), hf = (ci / D) & 1;
+            const int t0 = j * kKeyTile + bi * kBlock + hf * 8;
+            if (t0 + 8 <= kv_len) continue;
+            u32x4 *chunk = reinterpret_cast<u32x4 *>(lv + ci * 16);
+            u32x4 x = *chunk;
 #pragma unroll
             for (int w = 0; w < 4; ++w) {
-                const int kk = key0 + 8 * g4 + 2 * w;
-                vmask[w] = kk + 1 < kv_len ? 0xFFFFFFFFu : (kk < kv_len ? 0x0000FFFFu : 0u);
+                const int t = t0 + 2 * w;
+                x[w] &= t + 1 < kv_len ? 0xFFFFFFFFu : (t < kv_len ? 0x0000FFFFu : 0u);
             }
-#pragma unroll
-            for (int dt = 0; dt < NDT; ++dt) {
-                const u32x4 raw = *reinterpret_cast<const u32x4 *>(blkv + dt * 512) & vmask;
-                const bf16x8 vop = __builtin_bit_cast(bf16x8, raw);
-#pragma unroll
-                for (int rt = 0; rt < kRT; ++rt)
-                    o[rt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[rt], o[rt][dt], 0, 0, 0);
-            }
+            *chunk = x;
         }
+        __builtin_amdgcn_s_waitcnt(0xC07F);                   // lgkmcnt(0) only
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
     };
 
     // ---- pipeline over 32-key units.  Step u turns the scores of unit u into
@@ -479,24 +482,25 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     // Tile j: issue stage j+2 (ids fetched one tile earlier), compute, barrier.
     // The loads are issued on every path, so outstanding loads are counted
     // exactly; only the compute of tiles past the last one is skipped.
-    auto tile = [&](int j, const uint8_t *ks, const uint8_t *vs, uint8_t *kn, uint8_t *vn) {
+    auto tile = [&](int j, const uint8_t *ks, uint8_t *vs, uint8_t *kn, uint8_t *vn) {
         const int32_t ik = idk, iv = idv;
         idk = id_k(j + 3);
         idv = id_v(j + 3);
         const bool live = j < ntiles;
         bf16x8 pop[kRT];
+        if (live && (j + 1) * kKeyTile > kv_len) zero_v_tail(vs, j);
         load_k(kn, ik);
         if (live) {
             qk_unit(sb2, ks);                       // scores of unit 2j+1
             exp_unit(sa, pop);                      // P of unit 2j
-            pv_unit(pop, vs, 0, j * kKeyTile);
+            pv_unit(pop, vs, 0);
             max_unit(sb2, j * kKeyTile + 32);
         }
         load_v(vn, iv);
         if (live) {
             qk_unit(sa, ks + C::kUnitBytes);        // scores of unit 2j+2
             exp_unit(sb2, pop);                     // P of unit 2j+1
-            pv_unit(pop, vs, 1, j * kKeyTile + 32);
+            pv_unit(pop, vs, 1);
             max_unit(sa, (j + 1) * kKeyTile);
         }
         stage_barrier<D>();
