@@ -370,11 +370,16 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
         }
     };
     // Causal mask of a unit whose first key is key0 (lane group g4 holds unit
-    // keys 8*g4 + 4*sb + i), then its row maxima; a row max that exceeds the
-    // running max by more than the slack raises it and rescales O and l.
-    // scale > 0 is checked on the host, so masking and maxima commute with scaling.
+    // keys 8*g4 + 4*sb + i), then the rescale test: a row's running max is
+    // raised (and its O and l rescaled) when the unit's max exceeds it by more
+    // than the slack.  The row max exceeds it iff one of the four lanes holding
+    // the row sees a local max that does, so the common path tests local maxima
+    // and only the rare raise computes row maxima across lanes.  scale > 0 is
+    // checked on the host, so masking and maxima commute with scaling.
     auto max_unit = [&](f32x4 (&acc)[kRT][2], int key0) {
         const bool diag = key0 + 31 > wave_lim_min;
+        float lm[kRT];
+        bool raise = false;
 #pragma unroll
         for (int rt = 0; rt < kRT; ++rt) {
             if (diag) {
@@ -386,10 +391,13 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
                         if (4 * sb + i > lim) acc[rt][sb][i] = -INFINITY;
             }
             const f32x4 x0 = acc[rt][0], x1 = acc[rt][1];
-            float bm = fmax3(fmax3(x0[0], x0[1], x0[2]), fmax3(x0[3], x1[0], x1[1]), fmax3(x1[2], x1[3], x1[3]));
-            bm = xmax16_32(bm);
-            if (__any(bm > m[rt] + slack_raw)) {
-                const float m_new = __builtin_elementwise_maximum(m[rt], bm);
+            lm[rt] = fmax3(fmax3(x0[0], x0[1], x0[2]), fmax3(x0[3], x1[0], x1[1]), fmax3(x1[2], x1[3], x1[3]));
+            raise = raise || lm[rt] > m[rt] + slack_raw;
+        }
+        if (__any(raise)) {
+#pragma unroll
+            for (int rt = 0; rt < kRT; ++rt) {
+                const float m_new = __builtin_elementwise_maximum(m[rt], xmax16_32(lm[rt]));
                 const float alpha = __builtin_amdgcn_exp2f((m[rt] - m_new) * sl2);
                 lsum[rt] *= alpha;
 #pragma unroll
