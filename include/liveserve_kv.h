@@ -38,7 +38,10 @@
  *
  * Pool layout (device memory, bf16, num_layers x num_blocks x 2 x Hkv tiles):
  *   pool[layer][block][kv][head][tile]         kv = 0: K, kv = 1: V
- *   K tile = [block_size tokens][head_dim]     (token-major)
+ *   K tile = [head_dim / 8][block_size tokens][8 dims]
+ *            (chunk-major: element (token t, dim d) at ((d / 8) * block_size
+ *            + t) * 8 + d % 8, i.e. 16-byte chunks of 8 dims, all tokens of
+ *            dims 0..7 first; every supported head_dim is a multiple of 8)
  *   V tile = [head_dim][block_size tokens]     (dim-major)
  * Logical token t of session s lives in slot t % block_size of block
  * block_tables[s * max_blocks_per_session + t / block_size].

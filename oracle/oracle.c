@@ -28,7 +28,8 @@
  *
  * Pool layout (definition; bf16 stored as uint16):
  *   pool[layer][block][kv][head][tile]   kv = 0 for K, 1 for V
- *   K tile: [token o in 0..B-1][dim d in 0..D-1]   (token-major)
+ *   K tile: [chunk d/W in 0..D/W-1][token o in 0..B-1][d%W], W = min(8, D)
+ *           (chunk-major)
  *   V tile: [dim d in 0..D-1][token o in 0..B-1]   (dim-major)
  * Staging layout for stash/restore: staging[i][layer][kv][head][tile], i.e.
  * the per-layer (kv, head, tile) slab of block ids[i] for every layer, block
@@ -54,7 +55,8 @@ static int64_t k_index(int64_t num_blocks, int num_kv_heads, int head_dim, int b
                        int layer, int64_t block, int head, int token, int dim)
 {
     int64_t tile = (((int64_t)layer * num_blocks + block) * 2 + 0) * num_kv_heads + head;
-    return (tile * block_size + token) * head_dim + dim;
+    int w = head_dim < 8 ? head_dim : 8;          /* chunk width in dims */
+    return ((tile * (head_dim / w) + dim / w) * block_size + token) * w + dim % w;
 }
 
 static int64_t v_index(int64_t num_blocks, int num_kv_heads, int head_dim, int block_size,

@@ -2,7 +2,8 @@
 // attention reads them — the decode step's own token (autoregressive decode,
 // LiveServe §2.1 / §6) and a next turn's tokens (prefill over reused context,
 // §5).  Slot of logical token t of session s: block block_tables[s][t / 16],
-// offset t % 16; K tiles are token-major, V tiles dim-major.
+// offset t % 16; K tiles are chunk-major ([D/8][16 tokens][8 dims]), V tiles
+// dim-major.
 #include "common.h"
 
 namespace ls {
@@ -51,7 +52,7 @@ __global__ void append_kernel(uint16_t *__restrict__ layer_pool, int64_t num_blo
     uint16_t *vtile = layer_pool + (((int64_t)blk * 2 + 1) * num_kv_heads + g) * tile;
     const int64_t src = ((int64_t)tok * num_kv_heads + g) * head_dim;
     for (int d = threadIdx.x; d < head_dim; d += blockDim.x) {
-        ktile[o * head_dim + d] = k_new[src + d];
+        ktile[((d >> 3) * kBlock + o) * 8 + (d & 7)] = k_new[src + d];
         vtile[d * kBlock + o] = v_new[src + d];
     }
 }

@@ -17,9 +17,11 @@
 //   O^T[16 dims   x 16 heads] += V^T[16 x 16 tokens] . P^T     (16x16x16 bf16)
 // The MFMA accumulator layout of S^T (lane: head = lane%16, tokens 4*(lane/16)+i)
 // is exactly the B-operand layout PV needs, so the probabilities never leave
-// registers.  K tiles are token-major and V tiles dim-major in the pool, so both
-// operands load straight from HBM into their MFMA lanes (16- and 8-byte
-// coalesced buffer loads), prefetched two blocks ahead.  The split's block ids
+// registers.  K tiles are chunk-major ([D/8][16 tokens][8 dims]) and V tiles
+// dim-major in the pool, so both operands load straight from HBM into their
+// MFMA lanes: each K load instruction reads 1 KiB contiguous (lane l: bytes
+// 16l .. 16l+15 of the k-step's chunks), each V load 512 contiguous bytes;
+// prefetched two blocks ahead.  The split's block ids
 // are read once into a register and broadcast with readlane, so the load
 // stream never waits on an index fetch; a block that does not exist is loaded
 // through a zero-size buffer descriptor (no memory traffic, no branch).  Heads
@@ -240,7 +242,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
     const int g4 = lane >> 4;
     int koff[D / 32], voff[D / 16];
 #pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks) koff[ks] = (c16 * D + ks * 32 + g4 * 8) * 2;
+    for (int ks = 0; ks < D / 32; ++ks) koff[ks] = ((ks * 4 + g4) * kBlock + c16) * 16;   // = ks*1024 + lane*16
 #pragma unroll
     for (int dt = 0; dt < D / 16; ++dt) voff[dt] = ((dt * 16 + c16) * kBlock + g4 * 4) * 2;
 

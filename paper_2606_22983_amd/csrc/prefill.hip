@@ -303,7 +303,7 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
         // K: lane -> (token, slot); fetch the chunk that belongs in that slot
         const int t = q * (1024 / (D * 2)) + lane / C::kRowChunks;
         const int sl = lane % C::kRowChunks;
-        k_voff[e] = t * (D * 2) + (sl ^ kswz<D>(blk & 1, t)) * 16;
+        k_voff[e] = ((sl ^ kswz<D>(blk & 1, t)) * kBlock + t) * 16;   // chunk-major K tile
         // V: lane -> chunk position p = half*D + dim
         const int p = q * 64 + lane;
         v_voff[e] = (p % D) * 32 + (p / D) * 16;

@@ -12,7 +12,8 @@ sessions (thinker/talker decode, next-turn prefill over reused history,
 block restore during user speech).
 
 Pool layout: ``pool[layer][block][kv][head][tile]`` (bf16 bit patterns, uint16),
-K tile token-major ``[B][D]``, V tile dim-major ``[D][B]``.  Every slot that no
+K tile chunk-major ``[D/W][B][W]`` with ``W = min(8, D)`` (element (t, d) at
+``((d//W)*B + t)*W + d%W``), V tile dim-major ``[D][B]``.  Every slot that no
 session references (unused blocks, the tail of a session's last block, slots
 reserved for tokens not yet appended) holds the bf16 quiet NaN 0x7FC0, so a
 kernel that lets a masked slot leak into a result produces NaN.
@@ -160,7 +161,8 @@ def _poison(pool: np.ndarray, head_dim: int, tables: np.ndarray, valid_tokens: n
         used[tables[s, :nblk]] = True
     unused = np.nonzero(~used)[0]
     pool[:, unused] = NAN_BF16
-    k_view = pool[:, :, 0].reshape(nl, nb, hkv, BLOCK, head_dim)
+    w = min(8, head_dim)
+    k_view = pool[:, :, 0].reshape(nl, nb, hkv, head_dim // w, BLOCK, w)
     v_view = pool[:, :, 1].reshape(nl, nb, hkv, head_dim, BLOCK)
     for s in range(tables.shape[0]):
         nblk = int((tables[s] >= 0).sum())
@@ -168,7 +170,7 @@ def _poison(pool: np.ndarray, head_dim: int, tables: np.ndarray, valid_tokens: n
         for j in range(v // BLOCK, nblk):
             b = tables[s, j]
             first = max(0, v - j * BLOCK)
-            k_view[:, b, :, first:, :] = NAN_BF16
+            k_view[:, b, :, :, first:, :] = NAN_BF16
             v_view[:, b, :, :, first:] = NAN_BF16
     assert referenced_blocks == int(used.sum())
 

@@ -47,7 +47,8 @@ def make_paged(rng, lens, hkv, d, spare=3, nl=1, layer=0, k=None, v=None):
         for t in range(n):
             b = tables[s, t // B]
             for g in range(hkv):
-                pool[layer, b, 0, g].reshape(B, d)[t % B, :] = ks_[t, g]
+                w = min(8, d)   # K tile chunk-major [d/w][B][w]
+                pool[layer, b, 0, g].reshape(d // w, B, w)[:, t % B, :] = ks_[t, g].reshape(d // w, w)
                 pool[layer, b, 1, g].reshape(d, B)[:, t % B] = vs_[t, g]
     return pool, tables, ks, vs
 
