@@ -142,14 +142,15 @@ __device__ __forceinline__ int kswz(int b, int t) {
 // one (half, 16 dims) read 256 contiguous bytes.
 
 // One wave's load of one kilobyte of a block into LDS (lane l writes bytes
-// 16*l .. 16*l+15 of dst).  Absent blocks (id -1 or outside the pool) are read
-// through a zero-size buffer descriptor: no memory traffic.
+// 16*l .. 16*l+15 of dst).  head_base is this KV head's K (or V) tile in
+// block 0 of the layer; a block's tile is slab_elems further per block id,
+// one 32 x 32 -> 64-bit multiply.  Absent blocks (id -1 or outside the pool)
+// are read through a zero-size buffer descriptor: no memory traffic.
 template <int D>
-__device__ __forceinline__ void load_kb(const PrefillArgs &a, int g, int32_t b, int is_v, uint8_t *dst,
-                                        int voff) {
-    const bool valid = b >= 0 && b < a.num_blocks;
-    const uint16_t *base =
-        a.pool + (((int64_t)(valid ? b : 0) * 2 + is_v) * a.num_kv_heads + g) * (kBlock * D);
+__device__ __forceinline__ void load_kb(const uint16_t *head_base, uint32_t slab_elems, uint32_t nblocks,
+                                             int32_t b, uint8_t *dst, int voff) {
+    const bool valid = (uint32_t)b < nblocks;
+    const uint16_t *base = head_base + (uint64_t)(valid ? (uint32_t)b : 0u) * slab_elems;
     const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint16_t *>(base), 0, valid ? Geo<D>::kBlockBytes : 0, kBufferDword3P);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void *)dst, 16, voff, 0, 0, 0);
@@ -309,13 +310,17 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
         v_voff[e] = (p % D) * 32 + (p / D) * 16;
     }
     const int32_t *table = a.block_tables + (int64_t)s * a.max_blocks;
+    const uint32_t slab_elems = (uint32_t)(2 * Hkv * kBlock * D);
+    const uint32_t nblocks32 = (uint32_t)min(a.num_blocks, (int64_t)0x7fffffff);
+    const uint16_t *kbase = a.pool + (int64_t)g * (kBlock * D);
+    const uint16_t *vbase = kbase + (int64_t)Hkv * (kBlock * D);
     auto load_k = [&](uint8_t *stage, int32_t b) {
 #pragma unroll
-        for (int e = 0; e < C::kLoadsK; ++e) load_kb<D>(a, g, b, 0, stage + kb_off[e], k_voff[e]);
+        for (int e = 0; e < C::kLoadsK; ++e) load_kb<D>(kbase, slab_elems, nblocks32, b, stage + kb_off[e], k_voff[e]);
     };
     auto load_v = [&](uint8_t *stage, int32_t b) {
 #pragma unroll
-        for (int e = 0; e < C::kLoadsK; ++e) load_kb<D>(a, g, b, 1, stage + kb_off[e], v_voff[e]);
+        for (int e = 0; e < C::kLoadsK; ++e) load_kb<D>(vbase, slab_elems, nblocks32, b, stage + kb_off[e], v_voff[e]);
     };
     auto id_k = [&](int t) { return table_entry(table, 4 * t + 2 + blk, nb); };
     auto id_v = [&](int t) { return table_entry(table, 4 * t + blk, nb); };
