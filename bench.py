@@ -49,6 +49,7 @@ def parse():
     ap.add_argument("--restore-reps", type=int, default=5)
     ap.add_argument("--restore-sessions", type=int, default=128)
     ap.add_argument("--host-leg-gib", type=float, default=4.0)
+    ap.add_argument("--restore-cus", type=int, default=32)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     return ap.parse_args()
 
@@ -257,6 +258,43 @@ def talker_leg(torch, kv, W, args):
             "value": round(gbs, 1), "unit": "GB/s", "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)}
 
 
+def _hip_runtime():
+    """The HIP runtime this process already loaded (the one torch uses)."""
+    import ctypes
+    for line in open("/proc/self/maps"):
+        path = line.split()[-1] if len(line.split()) >= 6 else ""
+        if "libamdhip64" in os.path.basename(path):
+            return ctypes.CDLL(path)
+    return None
+
+
+def cu_masked_streams(torch, restore_cus):
+    """(decode stream on CUs restore_cus.., restore stream on CUs 0..restore_cus-1, CU count),
+    or None when the runtime does not offer CU-masked streams."""
+    import ctypes
+    lib = _hip_runtime()
+    n_cus = torch.cuda.get_device_properties(0).multi_processor_count
+    if lib is None or not hasattr(lib, "hipExtStreamCreateWithCUMask") or not 0 < restore_cus < n_cus:
+        return None
+    streams = []
+    for lo, hi in ((restore_cus, n_cus), (0, restore_cus)):
+        mask = (ctypes.c_uint32 * 32)()
+        for cu in range(lo, hi):
+            mask[cu // 32] |= 1 << (cu % 32)
+        h = ctypes.c_void_p()
+        if lib.hipExtStreamCreateWithCUMask(ctypes.byref(h), 32, mask) != 0:
+            return None
+        streams.append((torch.cuda.ExternalStream(h.value), h))
+    return streams[0][0], streams[1][0], n_cus, streams
+
+
+def destroy_streams(masked):
+    torch_streams = masked[3]
+    lib = _hip_runtime()
+    for _, h in torch_streams:
+        lib.hipStreamDestroy(h)
+
+
 def restore_leg(torch, kv, W, args, dec):
     rc = W.restore_case(num_sessions=args.restore_sessions)
     nl, hkv, d, nb = rc.num_layers, rc.num_kv_heads, rc.head_dim, rc.num_blocks
@@ -309,25 +347,26 @@ def restore_leg(torch, kv, W, args, dec):
     side = torch.cuda.Stream()
     dec_alone_ms = dec["kernel_ms"]
 
-    def overlap_decode(start_side):
+    def overlap_decode(start_side, dec_stream=stream, side_stream=side, alone=False):
         n_dec = 0
-        dtimer = Timer(torch, stream)
+        dtimer = Timer(torch, dec_stream)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         ev_side_start = torch.cuda.Event(enable_timing=True)
         ev_side_end = torch.cuda.Event(enable_timing=True)
-        ev_side_start.record(side)
-        with torch.cuda.stream(side):
-            start_side(side)
-        ev_side_end.record(side)
-        while not ev_side_end.query() and n_dec < 4000:
+        ev_side_start.record(side_stream)
+        if not alone:
+            with torch.cuda.stream(side_stream):
+                start_side(side_stream)
+        ev_side_end.record(side_stream)
+        while (n_dec < 64 if alone else not ev_side_end.query()) and n_dec < 4000:
             e = dtimer.start()
             kv.paged_attn_decode(dec["pools"][n_dec % 3], 0, dec["q"], dec["tables"], dec["lens"],
-                                 dec["case"].scale, dec["out"], dec["ws"])
+                                 dec["case"].scale, dec["out"], dec["ws"], stream=dec_stream)
             dtimer.stop(e)
             n_dec += 1
             if n_dec % 16 == 0:
-                stream.synchronize()
+                dec_stream.synchronize()
         torch.cuda.synchronize()
         return {"steps": n_dec, "makespan": time.perf_counter() - t0,
                 "side_ms": round(ev_side_start.elapsed_time(ev_side_end), 3),
@@ -338,6 +377,28 @@ def restore_leg(torch, kv, W, args, dec):
     agg = (2.0 * payload + n_dec * dec["alg_bytes"]) / ov["makespan"] / 1e9
     log("overlap: restore %.2f ms on the side stream, %d decode steps at %.1f us (alone %.1f us)" % (
         side_ms, n_dec, dec_conc_ms * 1e3, dec_alone_ms * 1e3))
+
+    # The same restore confined to a few CUs (a CU-masked side stream, the
+    # knob the paper's preloader would use to bound interference), decode on a
+    # stream masked to the other CUs; the library sizes both persistent grids
+    # to their stream's CUs.
+    part = {}
+    masked = cu_masked_streams(torch, args.restore_cus)
+    if masked:
+        dec_st, res_st, n_cus, _ = masked
+        solo = overlap_decode(None, dec_stream=dec_st, side_stream=res_st, alone=True)
+        conc = overlap_decode(lambda st: kv.kv_blocks_restore(pool, b, staging, stream=st),
+                              dec_stream=dec_st, side_stream=res_st)
+        part = {"restore_cus": args.restore_cus, "decode_cus": n_cus - args.restore_cus,
+                "restore_side_stream_ms": conc["side_ms"],
+                "restore_gbs": round(2.0 * payload / (conc["side_ms"] * 1e-3) / 1e9, 1),
+                "decode_steps": conc["steps"], "decode_us_alone_all_cus": round(dec_alone_ms * 1e3, 2),
+                "decode_us_alone_own_cus": solo["us"], "decode_us_concurrent": conc["us"],
+                "decode_slowdown_pct": round(100 * (conc["us"] * 1e-3 / dec_alone_ms - 1), 1)}
+        log("partitioned overlap: restore on %d CUs %.2f ms (%.0f GB/s), decode on %d CUs %.1f us alone, %.1f us "
+            "concurrent" % (args.restore_cus, conc["side_ms"], part["restore_gbs"], n_cus - args.restore_cus,
+                            solo["us"], conc["us"]))
+        destroy_streams(masked)
 
     # host leg: pinned host staging -> device ring -> scatter, through the same call
     host = {}
@@ -380,6 +441,7 @@ def restore_leg(torch, kv, W, args, dec):
                          "unit": "GB/s", "frac": round(scatter_gbs / HBM_PEAK_GBS, 4),
                          "traffic": measured_traffic("block_copy", source_digest("blockcopy.hip"))},
             "overlap_host_preload": host_overlap,
+            "overlap_device_staging_partitioned": part,
             "overlap_device_staging": {"restore_side_stream_ms": round(side_ms, 3), "decode_steps": n_dec,
                                        "decode_us_alone": round(dec_alone_ms * 1e3, 2),
                                        "decode_us_concurrent": round(dec_conc_ms * 1e3, 2),

@@ -35,6 +35,19 @@ unsigned int *device_error_word() {
     return addr[dev];
 }
 
+int stream_cus(const PoolGeom &p, hipStream_t stream) {
+    const int dev_cus = p.num_cus > 0 ? p.num_cus : 256;
+    if (!stream) return dev_cus;
+    uint32_t mask[32] = {};                    // up to 1024 CUs
+    if (hipExtStreamGetCUMask(stream, 32, mask) != hipSuccess) {
+        (void)hipGetLastError();               // leave no sticky error behind
+        return dev_cus;
+    }
+    int n = 0;
+    for (uint32_t w : mask) n += __builtin_popcount(w);
+    return n > 0 && n < dev_cus ? n : dev_cus;
+}
+
 namespace {
 
 thread_local char t_last_error[512] = "";

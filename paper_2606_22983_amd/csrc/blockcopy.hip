@@ -63,7 +63,7 @@ hipError_t launch_block_copy(const PoolGeom &p, int32_t n, const int32_t *ids, u
                              bool to_pool, unsigned int *err, hipStream_t stream) {
     if (n <= 0) return hipSuccess;
     const int64_t units = (int64_t)n * p.num_layers;
-    const int64_t grid = std::min<int64_t>(units, (int64_t)kCopyWorkgroupsPerCu * (p.num_cus > 0 ? p.num_cus : 256));
+    const int64_t grid = std::min<int64_t>(units, (int64_t)kCopyWorkgroupsPerCu * stream_cus(p, stream));
     hipLaunchKernelGGL(block_copy_kernel, dim3((unsigned)grid), dim3(kCopyThreads), 0, stream,
                        reinterpret_cast<uint8_t *>(p.base), ids, staging, p.num_blocks,
                        p.num_layers, (int64_t)p.slab_bytes(), units, to_pool ? 1 : 0, err);

@@ -34,6 +34,13 @@ struct PoolGeom {
     }
 };
 
+// Compute units a kernel launched on `stream` may use: the popcount of the
+// stream's CU mask when it is narrower than the device (a stream created with
+// hipExtStreamCreateWithCUMask), else the device's CU count.  Persistent grids
+// are sized from it, so a kernel confined to part of the GPU does not queue
+// workgroups that cannot become resident.
+int stream_cus(const PoolGeom &p, hipStream_t stream);
+
 // Device address of this device's error word (LS_DEVERR_* bits), or null if
 // the runtime could not resolve it.  Kernels receive it as an argument.
 unsigned int *device_error_word();
@@ -43,7 +50,6 @@ struct DecodePlan {
     int split_tokens;               // tokens per split (multiple of 64)
     int max_splits;                 // splits of the longest possible session
     bool supported;                 // false when a session could need too many splits
-    int resident_workgroups;        // persistent grid size
     size_t ml_bytes;                // fp32 [S][Hkv][max_splits][G][2]
     size_t acc_bytes;               // fp32 [S][Hkv][max_splits][G][D]
     size_t total() const { return ml_bytes + acc_bytes; }

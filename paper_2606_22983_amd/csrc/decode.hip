@@ -537,9 +537,6 @@ DecodePlan plan_decode(const PoolGeom &p, int32_t num_sessions, int32_t num_q_he
     plan.max_splits = (int)((max_tokens + T - 1) / T);
     if (plan.max_splits < 1) plan.max_splits = 1;
     plan.supported = plan.max_splits <= kMaxSplits && num_sessions <= kMaxBatch;
-    // Persistent grid: as many workgroups as the CUs hold at this kernel's
-    // occupancy (two 256-thread workgroups per CU).
-    plan.resident_workgroups = 2 * (p.num_cus > 0 ? p.num_cus : 256);
     const int G = p.num_kv_heads > 0 ? num_q_heads / p.num_kv_heads : 0;
     const int64_t sg = (int64_t)num_sessions * p.num_kv_heads;
     auto pad = [](size_t b) { return (b + 255) & ~(size_t)255; };
@@ -573,7 +570,10 @@ hipError_t launch_decode(const PoolGeom &p, int layer, int32_t num_sessions, int
     a.part_acc = reinterpret_cast<float *>(ws + plan.ml_bytes);
     a.num_sessions = num_sessions;
     const int64_t upper = (int64_t)num_sessions * p.num_kv_heads * plan.max_splits;
-    dim3 grid((unsigned)std::min<int64_t>(upper, (int64_t)plan.resident_workgroups));
+    // Persistent grid: two 256-thread workgroups (this kernel's occupancy) on
+    // every CU the stream may use.
+    const int64_t resident = 2 * (int64_t)stream_cus(p, stream);
+    dim3 grid((unsigned)std::min<int64_t>(upper, resident));
 #define LS_DECODE(DD, PW) \
     hipLaunchKernelGGL((decode_kernel<DD, 2, PW>), grid, dim3(kDecThreads), 0, stream, a)
     const int per_wave = plan.split_tokens / (kDecWaves * kBlock);
