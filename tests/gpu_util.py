@@ -73,3 +73,31 @@ def run_decode(kv_mod, dp: DevicePool, q, tables, lens, scale, k_new=None, v_new
         workspace = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
     kv_mod.paged_attn_decode(dp.pool, layer, q, tables, lens, scale, out, workspace, k_new, v_new)
     return out, workspace
+
+
+def cu_masked_stream(lo: int, hi: int):
+    """A torch stream whose kernels may run only on CUs lo .. hi-1 (through
+    hipExtStreamCreateWithCUMask of the runtime this process loaded), or None
+    when that runtime entry is unavailable.  Returns (stream, handle)."""
+    import ctypes
+    import os
+    lib = None
+    for line in open("/proc/self/maps"):
+        parts = line.split()
+        if len(parts) >= 6 and "libamdhip64" in os.path.basename(parts[-1]):
+            lib = ctypes.CDLL(parts[-1])
+            break
+    if lib is None or not hasattr(lib, "hipExtStreamCreateWithCUMask"):
+        return None
+    mask = (ctypes.c_uint32 * 32)()
+    for cu in range(lo, hi):
+        mask[cu // 32] |= 1 << (cu % 32)
+    h = ctypes.c_void_p()
+    if lib.hipExtStreamCreateWithCUMask(ctypes.byref(h), 32, mask) != 0:
+        return None
+    return torch.cuda.ExternalStream(h.value), (lib, h)
+
+
+def destroy_stream(handle):
+    lib, h = handle
+    lib.hipStreamDestroy(h)
