@@ -19,17 +19,25 @@
 // of PV, and they are 8 consecutive tokens of one block, i.e. one 16-byte
 // chunk of the block's dim-major V tile.  So P stays in registers (rounded to
 // bf16; the row sums add up the same rounded values) and every MFMA operand is
-// one 16-byte LDS read.  Softmax statistics stay in fp32; a row's running max
-// is raised (and O, l rescaled) only when a unit's max exceeds it by more than
-// 2^8 (log2 units), which keeps every probability at most 256 and makes
-// rescales rare.
+// one 16-byte LDS read.
 //
-// Pipeline: step u turns unit u's scores into P and accumulates P V while the
-// scores of unit u+1 are computed, so the MFMAs of one half overlap the VALU
-// work of the other.  K therefore runs one unit ahead of V.  Data moves from
-// HBM straight into LDS (buffer loads with the LDS-destination form: no
-// register staging, no LDS write instructions), three 64-key stages deep, one
-// barrier per 64 keys.
+// Scores are formed in log2 units: q is multiplied by scale * log2(e) and
+// rounded to bf16 once per workgroup, and every score tile's MFMA accumulator
+// starts at -m (the row's running max), so a finished tile holds S - m and P
+// is exp2 of it with no further arithmetic.  Softmax statistics stay in fp32;
+// m is raised (and O, l and the tile at hand shifted) only when a unit's max
+// exceeds it by more than 8 (log2 units), which keeps every probability at
+// most 256 and makes rescales rare.
+//
+// Pipeline: K runs one unit ahead of V.  Each 32-key unit takes two phases:
+// A computes the scores of unit u+1 while turning those of unit u into P; B
+// accumulates P V of unit u while testing the maxima of unit u+1.  Each MFMA
+// is followed by its share of the phase's VALU work, and the operands of the
+// next phase are read from LDS during the current one, so the softmax
+// arithmetic issues while the matrix core is busy and LDS latency stays
+// hidden.  Data moves from HBM straight into LDS (buffer loads with the
+// LDS-destination form: no register staging, no LDS write instructions),
+// three 64-key stages deep, one barrier per 64 keys.
 //
 // Scheduling: all query tiles of one (session, KV head) pair run on one XCD,
 // so they stream the same keys through its L2; pairs are dealt to XCDs
@@ -170,6 +178,22 @@ __device__ __forceinline__ void stage_barrier() {
     asm volatile("" ::: "memory");
 }
 
+// Scheduling constraint for one phase of N MFMAs: MFMA i is followed by one
+// LDS read (even i, while reads remain) and its share of the phase's VALU
+// instructions.
+template <int I, int N, int Reads, int Trans, int Valu>
+__device__ __forceinline__ void order_phase() {
+    if constexpr (I < N) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if constexpr (I % 2 == 0 && I / 2 < Reads) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        constexpr int t = (I + 1) * Trans / N - I * Trans / N;
+        if constexpr (t > 0) __builtin_amdgcn_sched_group_barrier(0x400, t, 0);
+        constexpr int v = (I + 1) * Valu / N - I * Valu / N;
+        if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x002, v, 0);
+        order_phase<I + 1, N, Reads, Trans, Valu>();
+    }
+}
+
 template <int D>
 __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     using C = Geo<D>;
@@ -287,9 +311,15 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
         for (int ks = 0; ks < KS; ++ks)
             qop[rt][ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(qrow + ks * 32 + g4 * 8));
     }
-    // Wait for q here, before the first stage loads are issued, so that no
-    // wait for q remains inside the key loop (vmcnt(0), other counters untouched).
-    __builtin_amdgcn_s_waitcnt(0x0F70);
+    // Scores are formed in log2 units: q is scaled by scale * log2(e) once and
+    // rounded back to bf16, so that exp2 needs no per-score multiply.
+    const float sl2 = a.scale_log2;
+#pragma unroll
+    for (int rt = 0; rt < kRT; ++rt)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) qop[rt][ks][i] = (__bf16)((float)qop[rt][ks][i] * sl2);
     // smallest causal limit among this wave's rows: units past it need masking
     const int wave_lim_min = c + min(j0 + (wave * kWaveRows) / G, n - 1);
 
@@ -325,29 +355,30 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     auto id_k = [&](int t) { return table_entry(table, 4 * t + 2 + blk, nb); };
     auto id_v = [&](int t) { return table_entry(table, 4 * t + blk, nb); };
 
-    float m[kRT], nm[kRT], lsum[kRT];     // running row maxima (raw scores),
-    f32x4 o[kRT][NDT];                    // -m * scale * log2(e), partial row sums
+    // Running row maxima m (log2 units), the MFMA accumulator start -m of
+    // every score tile (so that a finished tile holds S - m), partial row sums.
+    float m[kRT], lsum[kRT];
+    f32x4 cneg[kRT];
+    f32x4 o[kRT][NDT];
 #pragma unroll
     for (int rt = 0; rt < kRT; ++rt) {
-        m[rt] = -INFINITY;
-        nm[rt] = 0.f;
+        m[rt] = 0.f;
+        cneg[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
         lsum[rt] = 0.f;
     }
 #pragma unroll
     for (int rt = 0; rt < kRT; ++rt)
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) o[rt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const float sl2 = a.scale_log2;
-    const float slack_raw = kRescaleSlack / sl2;
     const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
 
-    // ---- S^T = K Q^T of one 32-key unit (K of the unit at lk) for 2 key
-    // sub-tiles x 2 row tiles.  A-row r of sub-tile sb is token
-    // 8*((r>>2)&1) + 4*sb + (r&3) of block r>>3, i.e. unit key 8*(r>>2) + 4*sb + (r&3).
-    // Per-lane byte offsets of the K rows read for sub-tile sb and k-step ks,
-    // relative to the unit.  They are made opaque to the compiler so that no
-    // constant part is split off the address: the split loses the LDS alias
-    // information that lets these reads overlap the loads still in flight.
+    // ---- S^T = K Q^T of one 32-key unit for 2 key sub-tiles x 2 row tiles.
+    // A-row r of sub-tile sb is token 8*((r>>2)&1) + 4*sb + (r&3) of block
+    // r>>3, i.e. unit key 8*(r>>2) + 4*sb + (r&3).  Per-lane byte offsets of
+    // the K rows read for sub-tile sb and k-step ks, relative to the unit.
+    // They are made opaque to the compiler so that no constant part is split
+    // off the address: the split loses the LDS alias information that lets
+    // these reads overlap the loads still in flight.
     int kroff[2][KS];
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb) {
@@ -360,56 +391,86 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
             asm volatile("" : "+v"(kroff[sb][ks]));
         }
     }
-    auto qk_unit = [&](f32x4 (&acc)[kRT][2], const uint8_t *lk) {
+    // Operands are read from LDS one phase before the MFMAs that use them:
+    // kop (K of the next unit) while the current P V runs, vop (V of the
+    // current unit) while the next scores are computed.
+    bf16x8 kop[2][KS];
+    bf16x8 vop[NDT];
+    auto read_k = [&](const uint8_t *lk) {
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                kop[sb][ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(lk + kroff[sb][ks]));
+    };
+    auto qk_mfma = [&](f32x4 (&acc)[kRT][2]) {
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb) {
 #pragma unroll
-            for (int rt = 0; rt < kRT; ++rt) acc[rt][sb] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int rt = 0; rt < kRT; ++rt) acc[rt][sb] = cneg[rt];
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const bf16x8 kop = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(lk + kroff[sb][ks]));
+            for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
                 for (int rt = 0; rt < kRT; ++rt)
-                    acc[rt][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[rt][ks], acc[rt][sb], 0, 0, 0);
-            }
+                    acc[rt][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop[sb][ks], qop[rt][ks], acc[rt][sb], 0, 0, 0);
         }
     };
     // Causal mask of a unit whose first key is key0 (lane group g4 holds unit
-    // keys 8*g4 + 4*sb + i), then the rescale test: a row's running max is
-    // raised (and its O and l rescaled) when the unit's max exceeds it by more
-    // than the slack.  The row max exceeds it iff one of the four lanes holding
-    // the row sees a local max that does, so the common path tests local maxima
-    // and only the rare raise computes row maxima across lanes.  scale > 0 is
+    // keys 8*g4 + 4*sb + i); only units that reach past the smallest causal
+    // limit of the wave's rows need it.
+    auto mask_unit = [&](f32x4 (&acc)[kRT][2], int key0) {
+        if (key0 + 31 <= wave_lim_min) return;
+#pragma unroll
+        for (int rt = 0; rt < kRT; ++rt) {
+            const int lim = row_lim[rt] - key0 - 8 * g4;
+#pragma unroll
+            for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (4 * sb + i > lim) acc[rt][sb][i] = -INFINITY;
+        }
+    };
+    // Rescale test: a row's running max is raised (and its O and l rescaled)
+    // when the unit's max exceeds it by more than the slack.  The row max
+    // exceeds it iff one of the four lanes holding the row sees a local max
+    // that does, so the common path tests local maxima only.  scale > 0 is
     // checked on the host, so masking and maxima commute with scaling.
-    auto max_unit = [&](f32x4 (&acc)[kRT][2], int key0) {
-        const bool diag = key0 + 31 > wave_lim_min;
-        float lm[kRT];
+    float lm[kRT];
+    auto max_test = [&](const f32x4 (&acc)[kRT][2]) {
         bool raise = false;
 #pragma unroll
         for (int rt = 0; rt < kRT; ++rt) {
-            if (diag) {
-                const int lim = row_lim[rt] - key0 - 8 * g4;
-#pragma unroll
-                for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        if (4 * sb + i > lim) acc[rt][sb][i] = -INFINITY;
-            }
             const f32x4 x0 = acc[rt][0], x1 = acc[rt][1];
             lm[rt] = fmax3(fmax3(x0[0], x0[1], x0[2]), fmax3(x0[3], x1[0], x1[1]), fmax3(x1[2], x1[3], x1[3]));
-            raise = raise || lm[rt] > m[rt] + slack_raw;
+            raise = raise || lm[rt] > kRescaleSlack;
         }
-        if (__any(raise)) {
+        return raise;
+    };
+    // The rare raise: row maxima across the four lanes, then rescale.
+    // The tile just tested (acc, relative to the old maxima) is shifted too.
+    auto rescale = [&](f32x4 (&acc)[kRT][2]) {
 #pragma unroll
-            for (int rt = 0; rt < kRT; ++rt) {
-                const float m_new = __builtin_elementwise_maximum(m[rt], xmax16_32(lm[rt]));
-                const float alpha = __builtin_amdgcn_exp2f((m[rt] - m_new) * sl2);
-                lsum[rt] *= alpha;
+        for (int rt = 0; rt < kRT; ++rt) {
+            const float delta = __builtin_elementwise_maximum(xmax16_32(lm[rt]), 0.f);
+            const float alpha = __builtin_amdgcn_exp2f(-delta);
+            lsum[rt] *= alpha;
 #pragma unroll
-                for (int dt = 0; dt < NDT; ++dt) o[rt][dt] *= alpha;
-                m[rt] = m_new;
-                nm[rt] = -m_new * sl2;
-            }
+            for (int dt = 0; dt < NDT; ++dt) o[rt][dt] *= alpha;
+            acc[rt][0] -= delta;
+            acc[rt][1] -= delta;
+            m[rt] += delta;
+            cneg[rt] = f32x4{-m[rt], -m[rt], -m[rt], -m[rt]};
+        }
+    };
+    // The first unit of a row sets its maximum outright (key 0 is visible to
+    // every row, so it is finite).
+    auto set_max = [&](f32x4 (&acc)[kRT][2]) {
+#pragma unroll
+        for (int rt = 0; rt < kRT; ++rt) {
+            m[rt] = xmax16_32(lm[rt]);
+            acc[rt][0] -= m[rt];
+            acc[rt][1] -= m[rt];
+            cneg[rt] = f32x4{-m[rt], -m[rt], -m[rt], -m[rt]};
         }
     };
     // P = exp2(S * scale * log2 e - m') in bf16 (B operand of PV) and row sums.
@@ -421,8 +482,7 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
             for (int j = 0; j < 4; ++j) {
                 const f32x4 &x = acc[rt][j >> 1];
                 const int i0 = 2 * (j & 1);
-                const bf16x2 pk = {(__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(x[i0], sl2, nm[rt])),
-                                   (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(x[i0 + 1], sl2, nm[rt]))};
+                const bf16x2 pk = {(__bf16)__builtin_amdgcn_exp2f(x[i0]), (__bf16)__builtin_amdgcn_exp2f(x[i0 + 1])};
                 lsum[rt] = __builtin_amdgcn_fdot2_f32_bf16(pk, ones2, lsum[rt], false);
                 w[j] = __builtin_bit_cast(uint32_t, pk);
             }
@@ -430,20 +490,36 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
         }
     };
     // Per-lane byte offset of the V chunk this lane reads, opaque for the same
-    // reason as kroff.
+    // reason as kroff.  Dims dt*16 + c16 of one lane are 256 bytes apart.
     int vroff = (g4 >> 1) * C::kBlockBytes + ((g4 & 1) * D + c16) * 16;
     asm volatile("" : "+v"(vroff));
-    // O^T += V^T P^T for unit half h of the V tile at lv (dims dt*16 + c16 of
-    // one lane are 256 bytes apart).
-    auto pv_unit = [&](const bf16x8 (&pop)[kRT], const uint8_t *lv, int h) {
+    auto read_v = [&](const uint8_t *lv, int h) {
         const uint8_t *blkv = lv + 2 * h * C::kBlockBytes + vroff;
 #pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) {
-            const bf16x8 vop = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(blkv + dt * 256));
+        for (int dt = 0; dt < NDT; ++dt)
+            vop[dt] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(blkv + dt * 256));
+    };
+    // O^T += V^T P^T for one unit.
+    auto pv_mfma = [&](const bf16x8 (&pop)[kRT]) {
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
             for (int rt = 0; rt < kRT; ++rt)
-                o[rt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop[rt], o[rt][dt], 0, 0, 0);
-        }
+                o[rt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop[dt], pop[rt], o[rt][dt], 0, 0, 0);
+    };
+    // Instruction order inside a phase: each MFMA is followed by a share of
+    // the phase's VALU work and, every other MFMA, by one operand read for the
+    // next phase, so that the softmax arithmetic issues while the matrix core
+    // is busy and every LDS read has a whole phase to return.
+    constexpr int kPhaseMfma = 2 * KS * kRT;              // == NDT * kRT
+    constexpr int kExpTrans = kRT * 4 * 2;                // exp phase: 2 exp ...
+    constexpr int kExpValu = kRT * 4 * 2;                 // ... and cvt, dot2 per pair
+    constexpr int kMaxValu = kRT * 6;                     // max phase
+    // Keeps the probabilities of a phase from being computed later (after the
+    // masking branch that follows the phase).
+    auto pin = [&](const bf16x8 (&pop)[kRT]) {
+#pragma unroll
+        for (int rt = 0; rt < kRT; ++rt) asm volatile("" ::"v"(pop[rt]));
     };
     // Values of keys at or past kv_len (the rest of the session's last block,
     // or blocks never loaded) are zeroed in the staged V tile of key tile j
@@ -470,12 +546,15 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
         asm volatile("" ::: "memory");
     };
 
-    // ---- pipeline over 32-key units.  Step u turns the scores of unit u into
-    // P, accumulates P V of unit u and computes the scores of unit u+1.  Key
-    // tile j (units 2j, 2j+1) reads stage j % 3: K units 2j+1, 2j+2 and V(j).
-    // While it is processed, the loads of stage j+2 are issued into the third
-    // buffer pair (read last in tile j-1); stage j+1 has landed by the barrier
-    // that ends tile j.
+    // ---- pipeline over 32-key units.  Key tile j (units 2j, 2j+1) reads
+    // stage j % 3: K of units 2j+1, 2j+2 and V of units 2j, 2j+1.  While it
+    // is processed, the loads of stage j+2 go into the third buffer pair (last
+    // read in tile j-1).  A tile runs four phases:
+    //   A0: scores of unit 2j+1 | P of unit 2j      | read V of unit 2j
+    //   B0: P V of unit 2j      | max of unit 2j+1  | read K of unit 2j+2
+    //   A1: scores of unit 2j+2 | P of unit 2j+1    | read V of unit 2j+1
+    //   -- barrier: stage j+1 has landed and every read of stage j is done --
+    //   B1: P V of unit 2j+1    | max of unit 2j+2  | read K of unit 2j+3
     f32x4 sa[kRT][2], sb2[kRT][2];
     int32_t idk = id_k(-1), idv = id_v(-1);
     load_k(k2, idk);                      // stage -1: K unit 0 (its V part is empty)
@@ -488,14 +567,17 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     load_v(v1, idv);
     idk = id_k(2); idv = id_v(2);
     stage_barrier<D>();                   // stages -1 and 0 have landed
-    qk_unit(sa, k2 + C::kUnitBytes);      // unit 0 = second unit of stage -1
-    max_unit(sa, 0);
+    read_k(k2 + C::kUnitBytes);           // unit 0 = second unit of stage -1
+    qk_mfma(sa);
+    read_k(k0);                           // unit 1
+    mask_unit(sa, 0);
+    max_test(sa);
+    set_max(sa);
     stage_barrier<D>();                   // stage -1 fully read: k2/v2 are free
 
-    // Tile j: issue stage j+2 (ids fetched one tile earlier), compute, barrier.
     // The loads are issued on every path, so outstanding loads are counted
     // exactly; only the compute of tiles past the last one is skipped.
-    auto tile = [&](int j, const uint8_t *ks, uint8_t *vs, uint8_t *kn, uint8_t *vn) {
+    auto tile = [&](int j, const uint8_t *ks, uint8_t *vs, const uint8_t *knext, uint8_t *kn, uint8_t *vn) {
         const int32_t ik = idk, iv = idv;
         idk = id_k(j + 3);
         idv = id_v(j + 3);
@@ -503,25 +585,39 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
         bf16x8 pop[kRT];
         if (live && (j + 1) * kKeyTile > kv_len) zero_v_tail(vs, j);
         load_k(kn, ik);
-        if (live) {
-            qk_unit(sb2, ks);                       // scores of unit 2j+1
-            exp_unit(sa, pop);                      // P of unit 2j
-            pv_unit(pop, vs, 0);
-            max_unit(sb2, j * kKeyTile + 32);
-        }
         load_v(vn, iv);
         if (live) {
-            qk_unit(sa, ks + C::kUnitBytes);        // scores of unit 2j+2
-            exp_unit(sb2, pop);                     // P of unit 2j+1
-            pv_unit(pop, vs, 1);
-            max_unit(sa, (j + 1) * kKeyTile);
+            qk_mfma(sb2);                           // A0
+            exp_unit(sa, pop);
+            read_v(vs, 0);
+            order_phase<0, kPhaseMfma, NDT, kExpTrans, kExpValu>();
+            pin(pop);
+            mask_unit(sb2, j * kKeyTile + 32);
+            pv_mfma(pop);                           // B0
+            const bool r0 = max_test(sb2);
+            read_k(ks + C::kUnitBytes);
+            order_phase<0, kPhaseMfma, 2 * KS, 0, kMaxValu>();
+            if (__any(r0)) rescale(sb2);
+            qk_mfma(sa);                            // A1
+            exp_unit(sb2, pop);
+            read_v(vs, 1);
+            order_phase<0, kPhaseMfma, NDT, kExpTrans, kExpValu>();
+            pin(pop);
+            mask_unit(sa, (j + 1) * kKeyTile);
         }
         stage_barrier<D>();
+        if (live) {
+            pv_mfma(pop);                           // B1
+            const bool r1 = max_test(sa);
+            read_k(knext);                          // (unused when tile j+1 is past the end)
+            order_phase<0, kPhaseMfma, 2 * KS, 0, kMaxValu>();
+            if (__any(r1)) rescale(sa);
+        }
     };
     for (int j = 0; j < ntiles; j += 3) {
-        tile(j, k0, v0, k2, v2);
-        tile(j + 1, k1, v1, k0, v0);
-        tile(j + 2, k2, v2, k1, v1);
+        tile(j, k0, v0, k1, k2, v2);
+        tile(j + 1, k1, v1, k2, k0, v0);
+        tile(j + 2, k2, v2, k0, k1, v1);
     }
 
     // ---- normalise and write
