@@ -19,15 +19,12 @@
 // of PV, and they are 8 consecutive tokens of one block, i.e. one 16-byte
 // chunk of the block's dim-major V tile.  So P stays in registers (rounded to
 // bf16; the row sums add up the same rounded values) and every MFMA operand is
-// one 16-byte LDS read.
-//
-// Scores are formed in log2 units: q is multiplied by scale * log2(e) and
-// rounded to bf16 once per workgroup, and every score tile's MFMA accumulator
-// starts at -m (the row's running max), so a finished tile holds S - m and P
-// is exp2 of it with no further arithmetic.  Softmax statistics stay in fp32;
-// m is raised (and O, l and the tile at hand shifted) only when a unit's max
-// exceeds it by more than 8 (log2 units), which keeps every probability at
-// most 256 and makes rescales rare.
+// one 16-byte LDS read.  Scores are exact fp32 sums of bf16 products; the
+// softmax scale is applied in fp32 (folding it into q before the MFMA would
+// round q * scale to bf16, an error that grows with the score magnitude).
+// Softmax statistics stay in fp32; a row's running max is raised (and O, l
+// rescaled) only when a unit's max exceeds it by more than 8 (log2 units),
+// which keeps every probability at most 256 and makes rescales rare.
 //
 // Pipeline: K runs one unit ahead of V.  Each 32-key unit takes two phases:
 // A computes the scores of unit u+1 while turning those of unit u into P; B
@@ -179,8 +176,8 @@ __device__ __forceinline__ void stage_barrier() {
 }
 
 // Scheduling constraint for one phase of N MFMAs: MFMA i is followed by one
-// LDS read (even i, while reads remain) and its share of the phase's VALU
-// instructions.
+// LDS read (even i, while reads remain) and its share of the phase's
+// transcendental and other VALU instructions.
 template <int I, int N, int Reads, int Trans, int Valu>
 __device__ __forceinline__ void order_phase() {
     if constexpr (I < N) {
@@ -311,15 +308,9 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
         for (int ks = 0; ks < KS; ++ks)
             qop[rt][ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(qrow + ks * 32 + g4 * 8));
     }
-    // Scores are formed in log2 units: q is scaled by scale * log2(e) once and
-    // rounded back to bf16, so that exp2 needs no per-score multiply.
-    const float sl2 = a.scale_log2;
-#pragma unroll
-    for (int rt = 0; rt < kRT; ++rt)
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-            for (int i = 0; i < 8; ++i) qop[rt][ks][i] = (__bf16)((float)qop[rt][ks][i] * sl2);
+    // Wait for q here, before the first stage loads are issued, so that no
+    // wait for q remains inside the key loop (vmcnt(0), other counters untouched).
+    __builtin_amdgcn_s_waitcnt(0x0F70);
     // smallest causal limit among this wave's rows: units past it need masking
     const int wave_lim_min = c + min(j0 + (wave * kWaveRows) / G, n - 1);
 
@@ -355,21 +346,20 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     auto id_k = [&](int t) { return table_entry(table, 4 * t + 2 + blk, nb); };
     auto id_v = [&](int t) { return table_entry(table, 4 * t + blk, nb); };
 
-    // Running row maxima m (log2 units), the MFMA accumulator start -m of
-    // every score tile (so that a finished tile holds S - m), partial row sums.
-    float m[kRT], lsum[kRT];
-    f32x4 cneg[kRT];
-    f32x4 o[kRT][NDT];
+    float m[kRT], nm[kRT], lsum[kRT];     // running row maxima (raw scores),
+    f32x4 o[kRT][NDT];                    // -m * scale * log2(e), partial row sums
 #pragma unroll
     for (int rt = 0; rt < kRT; ++rt) {
-        m[rt] = 0.f;
-        cneg[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        m[rt] = -INFINITY;
+        nm[rt] = 0.f;
         lsum[rt] = 0.f;
     }
 #pragma unroll
     for (int rt = 0; rt < kRT; ++rt)
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) o[rt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const float sl2 = a.scale_log2;
+    const float slack_raw = kRescaleSlack / sl2;
     const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
 
     // ---- S^T = K Q^T of one 32-key unit for 2 key sub-tiles x 2 row tiles.
@@ -407,7 +397,7 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb) {
 #pragma unroll
-            for (int rt = 0; rt < kRT; ++rt) acc[rt][sb] = cneg[rt];
+            for (int rt = 0; rt < kRT; ++rt) acc[rt][sb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
@@ -442,35 +432,21 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
         for (int rt = 0; rt < kRT; ++rt) {
             const f32x4 x0 = acc[rt][0], x1 = acc[rt][1];
             lm[rt] = fmax3(fmax3(x0[0], x0[1], x0[2]), fmax3(x0[3], x1[0], x1[1]), fmax3(x1[2], x1[3], x1[3]));
-            raise = raise || lm[rt] > kRescaleSlack;
+            raise = raise || lm[rt] > m[rt] + slack_raw;
         }
         return raise;
     };
     // The rare raise: row maxima across the four lanes, then rescale.
-    // The tile just tested (acc, relative to the old maxima) is shifted too.
-    auto rescale = [&](f32x4 (&acc)[kRT][2]) {
+    auto rescale = [&]() {
 #pragma unroll
         for (int rt = 0; rt < kRT; ++rt) {
-            const float delta = __builtin_elementwise_maximum(xmax16_32(lm[rt]), 0.f);
-            const float alpha = __builtin_amdgcn_exp2f(-delta);
+            const float m_new = __builtin_elementwise_maximum(m[rt], xmax16_32(lm[rt]));
+            const float alpha = __builtin_amdgcn_exp2f((m[rt] - m_new) * sl2);
             lsum[rt] *= alpha;
 #pragma unroll
             for (int dt = 0; dt < NDT; ++dt) o[rt][dt] *= alpha;
-            acc[rt][0] -= delta;
-            acc[rt][1] -= delta;
-            m[rt] += delta;
-            cneg[rt] = f32x4{-m[rt], -m[rt], -m[rt], -m[rt]};
-        }
-    };
-    // The first unit of a row sets its maximum outright (key 0 is visible to
-    // every row, so it is finite).
-    auto set_max = [&](f32x4 (&acc)[kRT][2]) {
-#pragma unroll
-        for (int rt = 0; rt < kRT; ++rt) {
-            m[rt] = xmax16_32(lm[rt]);
-            acc[rt][0] -= m[rt];
-            acc[rt][1] -= m[rt];
-            cneg[rt] = f32x4{-m[rt], -m[rt], -m[rt], -m[rt]};
+            m[rt] = m_new;
+            nm[rt] = -m_new * sl2;
         }
     };
     // P = exp2(S * scale * log2 e - m') in bf16 (B operand of PV) and row sums.
@@ -482,7 +458,8 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
             for (int j = 0; j < 4; ++j) {
                 const f32x4 &x = acc[rt][j >> 1];
                 const int i0 = 2 * (j & 1);
-                const bf16x2 pk = {(__bf16)__builtin_amdgcn_exp2f(x[i0]), (__bf16)__builtin_amdgcn_exp2f(x[i0 + 1])};
+                const bf16x2 pk = {(__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(x[i0], sl2, nm[rt])),
+                                   (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(x[i0 + 1], sl2, nm[rt]))};
                 lsum[rt] = __builtin_amdgcn_fdot2_f32_bf16(pk, ones2, lsum[rt], false);
                 w[j] = __builtin_bit_cast(uint32_t, pk);
             }
@@ -513,7 +490,7 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     // is busy and every LDS read has a whole phase to return.
     constexpr int kPhaseMfma = 2 * KS * kRT;              // == NDT * kRT
     constexpr int kExpTrans = kRT * 4 * 2;                // exp phase: 2 exp ...
-    constexpr int kExpValu = kRT * 4 * 2;                 // ... and cvt, dot2 per pair
+    constexpr int kExpValu = kRT * 4 * 4;                 // ... and 2 fma, cvt, dot2 per pair
     constexpr int kMaxValu = kRT * 6;                     // max phase
     // Keeps the probabilities of a phase from being computed later (after the
     // masking branch that follows the phase).
@@ -571,8 +548,7 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     qk_mfma(sa);
     read_k(k0);                           // unit 1
     mask_unit(sa, 0);
-    max_test(sa);
-    set_max(sa);
+    if (__any(max_test(sa))) rescale();
     stage_barrier<D>();                   // stage -1 fully read: k2/v2 are free
 
     // The loads are issued on every path, so outstanding loads are counted
@@ -597,7 +573,7 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
             const bool r0 = max_test(sb2);
             read_k(ks + C::kUnitBytes);
             order_phase<0, kPhaseMfma, 2 * KS, 0, kMaxValu>();
-            if (__any(r0)) rescale(sb2);
+            if (__any(r0)) rescale();
             qk_mfma(sa);                            // A1
             exp_unit(sb2, pop);
             read_v(vs, 1);
@@ -611,7 +587,7 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
             const bool r1 = max_test(sa);
             read_k(knext);                          // (unused when tile j+1 is past the end)
             order_phase<0, kPhaseMfma, 2 * KS, 0, kMaxValu>();
-            if (__any(r1)) rescale(sa);
+            if (__any(r1)) rescale();
         }
     };
     for (int j = 0; j < ntiles; j += 3) {

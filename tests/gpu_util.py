@@ -101,3 +101,36 @@ def cu_masked_stream(lo: int, hi: int):
 def destroy_stream(handle):
     lib, h = handle
     lib.hipStreamDestroy(h)
+
+
+def key_ramp(shape: str, nblk: int, j: np.ndarray) -> np.ndarray:
+    """Per-block K scale for block positions j of an nblk-block context.
+
+    rising: 1 -> 10 along the context, so the running max is raised many times;
+    spike: 16 on the second-to-last block only, one large late raise;
+    falling: 10 -> 1, the first blocks hold the max and nothing is raised.
+    """
+    t = j / max(nblk - 1, 1)
+    if shape == "rising":
+        return 1.0 + 9.0 * t
+    if shape == "falling":
+        return 10.0 - 9.0 * t
+    if shape == "spike":
+        return np.where(j == max(nblk - 2, 0), 16.0, 1.0)
+    raise ValueError(shape)
+
+
+def scale_keys(pool: np.ndarray, tables: np.ndarray, ctx_tokens, shape: str):
+    """Multiply the K tiles of each session's context blocks by key_ramp (in place,
+    rounded to bf16; NaN slots stay NaN).  ``ctx_tokens[s]`` tokens are in the pool."""
+    from paper_2606_22983_amd import workloads as W
+    for s in range(tables.shape[0]):
+        nblk = (int(ctx_tokens[s]) + 15) // 16
+        if nblk == 0:
+            continue
+        j = np.arange(nblk)
+        f = key_ramp(shape, nblk, j).astype(np.float32)
+        ids = tables[s, :nblk]
+        k = W.from_bf16(pool[0, ids, 0])
+        pool[0, ids, 0] = W.to_bf16(k * f[:, None, None])
+

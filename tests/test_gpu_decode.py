@@ -7,7 +7,7 @@ import torch
 
 from paper_2606_22983_amd import workloads as W
 from tests.gpu_util import (DevicePool, assert_attn_close, bf16_dev, host_bits, i32_dev, log,
-                            run_decode)
+                            run_decode, scale_keys)
 
 pytestmark = pytest.mark.gpu
 
@@ -83,6 +83,22 @@ def test_decode_lengths_and_groups(kv, oracle_lib, d, hq, hkv, append):
     assert_attn_close(out, ref, "decode D=%d G=%d append=%s" % (d, hq // hkv, append))
     if append:
         assert np.array_equal(dp.host(), ref_pool)
+    assert kv.ls_device_errors() == 0
+
+
+@pytest.mark.parametrize("shape", ["rising", "spike", "falling"])
+def test_decode_peaky_scores(kv, oracle_lib, shape):
+    """Large, uneven scores (key norms rising along the context, one late block of
+    much larger keys, or falling norms): the running-max raise and its rescale of
+    (l, O), within a split and across the split merge."""
+    rng = np.random.default_rng({"rising": 81, "spike": 82, "falling": 83}[shape])
+    lens = [3001, 1025, 513, 77, 16]
+    pool, tables, q, _, _ = _synthetic(rng, lens, 32, 4, 128, False)
+    scale_keys(pool, tables, lens, shape)
+    dp = DevicePool(kv, pool, 128)
+    out, _ = run_decode(kv, dp, bf16_dev(q), i32_dev(tables), i32_dev(lens), 1 / math.sqrt(128))
+    ref = oracle_lib.decode(pool, 16, 128, 0, q, tables, np.array(lens), 1 / math.sqrt(128))
+    assert_attn_close(out, ref, "decode %s keys" % shape)
     assert kv.ls_device_errors() == 0
 
 

@@ -6,7 +6,7 @@ import pytest
 import torch
 
 from paper_2606_22983_amd import workloads as W
-from tests.gpu_util import DevicePool, assert_attn_close, bf16_dev, i32_dev, log
+from tests.gpu_util import DevicePool, assert_attn_close, bf16_dev, i32_dev, log, scale_keys
 
 pytestmark = pytest.mark.gpu
 
@@ -76,6 +76,26 @@ def test_prefill_many_sessions(kv, oracle_lib):
     out, cu = _run(kv, dp, q, kn, vn, n, c, tables, 0.125)
     ref = oracle_lib.prefill(pool, 16, d, 0, q, kn, vn, cu, c, tables, 0.125)
     assert_attn_close(out, ref, "prefill, 140 sessions")
+    assert kv.ls_device_errors() == 0
+
+
+@pytest.mark.parametrize("shape", ["rising", "spike", "falling"])
+@pytest.mark.parametrize("d,hq,hkv", [(128, 32, 4), (64, 8, 8)])
+def test_prefill_peaky_scores(kv, oracle_lib, shape, d, hq, hkv):
+    """Large, uneven scores: key norms that rise along the context (the running
+    max is raised many times), one block of much larger keys late in the context,
+    or norms that fall (the first keys hold the max).  Scores reach tens of log2
+    units, so the rescale path and the exactness of the scaled scores are tested."""
+    rng = np.random.default_rng({"rising": 71, "spike": 72, "falling": 73}[shape] + d)
+    n, c = [200, 70, 33], [1500, 700, 0]
+    pool, tables, q, kn, vn = _case(rng, n, c, hq, hkv, d)
+    scale_keys(pool, tables, c, shape)
+    if shape == "rising":               # the turn's own keys continue the ramp
+        kn = W.to_bf16(W.from_bf16(kn) * np.float32(10.0))
+    dp = DevicePool(kv, pool, d)
+    out, cu = _run(kv, dp, q, kn, vn, np.array(n), np.array(c), tables, 1 / math.sqrt(d))
+    ref = oracle_lib.prefill(pool, 16, d, 0, q, kn, vn, cu, c, tables, 1 / math.sqrt(d))
+    assert_attn_close(out, ref, "prefill %s keys D=%d G=%d" % (shape, d, hq // hkv))
     assert kv.ls_device_errors() == 0
 
 
