@@ -27,8 +27,9 @@
 // which keeps every probability at most 256 and makes rescales rare.
 //
 // Pipeline: K runs one unit ahead of V.  Each 32-key unit takes two phases:
-// A computes the scores of unit u+1 while turning those of unit u into P; B
-// accumulates P V of unit u while testing the maxima of unit u+1.  Each MFMA
+// A computes the scores of unit u+1 while turning the exp2 arguments of unit
+// u into P; B accumulates P V of unit u while it tests the maxima of unit u+1
+// and scales its scores into exp2 arguments (S * scale * log2(e) - m').  Each MFMA
 // is followed by its share of the phase's VALU work, and the operands of the
 // next phase are read from LDS during the current one, so the softmax
 // arithmetic issues while the matrix core is busy and LDS latency stays
@@ -437,7 +438,17 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
         return raise;
     };
     // The rare raise: row maxima across the four lanes, then rescale.
-    auto rescale = [&]() {
+    // Scores -> exp2 arguments S * scale * log2(e) - m' (phase B, after the max test).
+    auto scale_unit = [&](f32x4 (&acc)[kRT][2]) {
+#pragma unroll
+        for (int rt = 0; rt < kRT; ++rt)
+#pragma unroll
+            for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[rt][sb][i] = __builtin_fmaf(acc[rt][sb][i], sl2, nm[rt]);
+    };
+    // The raise, after scale_unit: the unit's exp2 arguments move with the max.
+    auto rescale = [&](f32x4 (&acc)[kRT][2]) {
 #pragma unroll
         for (int rt = 0; rt < kRT; ++rt) {
             const float m_new = __builtin_elementwise_maximum(m[rt], xmax16_32(lm[rt]));
@@ -446,7 +457,11 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
 #pragma unroll
             for (int dt = 0; dt < NDT; ++dt) o[rt][dt] *= alpha;
             m[rt] = m_new;
-            nm[rt] = -m_new * sl2;
+            const float nm_new = -m_new * sl2;
+            const float shift = nm_new - nm[rt];
+            nm[rt] = nm_new;
+            acc[rt][0] += shift;
+            acc[rt][1] += shift;
         }
     };
     // P = exp2(S * scale * log2 e - m') in bf16 (B operand of PV) and row sums.
@@ -458,8 +473,7 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
             for (int j = 0; j < 4; ++j) {
                 const f32x4 &x = acc[rt][j >> 1];
                 const int i0 = 2 * (j & 1);
-                const bf16x2 pk = {(__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(x[i0], sl2, nm[rt])),
-                                   (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(x[i0 + 1], sl2, nm[rt]))};
+                const bf16x2 pk = {(__bf16)__builtin_amdgcn_exp2f(x[i0]), (__bf16)__builtin_amdgcn_exp2f(x[i0 + 1])};
                 lsum[rt] = __builtin_amdgcn_fdot2_f32_bf16(pk, ones2, lsum[rt], false);
                 w[j] = __builtin_bit_cast(uint32_t, pk);
             }
@@ -490,8 +504,8 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     // is busy and every LDS read has a whole phase to return.
     constexpr int kPhaseMfma = 2 * KS * kRT;              // == NDT * kRT
     constexpr int kExpTrans = kRT * 4 * 2;                // exp phase: 2 exp ...
-    constexpr int kExpValu = kRT * 4 * 4;                 // ... and 2 fma, cvt, dot2 per pair
-    constexpr int kMaxValu = kRT * 6;                     // max phase
+    constexpr int kExpValu = kRT * 4 * 2;                 // ... and cvt, dot2 per pair
+    constexpr int kMaxValu = kRT * 14;                    // max phase, scale FMAs
     // Keeps the probabilities of a phase from being computed later (after the
     // masking branch that follows the phase).
     auto pin = [&](const bf16x8 (&pop)[kRT]) {
@@ -548,7 +562,11 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     qk_mfma(sa);
     read_k(k0);                           // unit 1
     mask_unit(sa, 0);
-    if (__any(max_test(sa))) rescale();
+    {
+        const bool r = max_test(sa);
+        scale_unit(sa);
+        if (__any(r)) rescale(sa);
+    }
     stage_barrier<D>();                   // stage -1 fully read: k2/v2 are free
 
     // The loads are issued on every path, so outstanding loads are counted
@@ -571,9 +589,10 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
             mask_unit(sb2, j * kKeyTile + 32);
             pv_mfma(pop);                           // B0
             const bool r0 = max_test(sb2);
+            scale_unit(sb2);
             read_k(ks + C::kUnitBytes);
             order_phase<0, kPhaseMfma, 2 * KS, 0, kMaxValu>();
-            if (__any(r0)) rescale();
+            if (__any(r0)) rescale(sb2);
             qk_mfma(sa);                            // A1
             exp_unit(sb2, pop);
             read_v(vs, 1);
@@ -585,9 +604,10 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
         if (live) {
             pv_mfma(pop);                           // B1
             const bool r1 = max_test(sa);
+            scale_unit(sa);
             read_k(knext);                          // (unused when tile j+1 is past the end)
             order_phase<0, kPhaseMfma, 2 * KS, 0, kMaxValu>();
-            if (__any(r1)) rescale();
+            if (__any(r1)) rescale(sa);
         }
     };
     for (int j = 0; j < ntiles; j += 3) {
