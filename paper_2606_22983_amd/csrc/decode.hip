@@ -46,6 +46,8 @@ constexpr int kMaxSplitTokens = 512;         // 8 blocks per wave (the unrolled 
 constexpr int kMaxSplits = 256;              // combine kernel's LDS capacity
 constexpr int kMaxBatch = 2048;              // sessions per decode call (LDS prefix sums)
 constexpr int kMaxGroup = 8;                 // query heads per KV head
+static_assert(kMaxBatch * kMaxSplits <= 0xFFFFF && kMaxBatch < 4096,
+              "work-row counts must fit the packed scan (20 + 12 bits)");
 constexpr int kSpinLimit = 1 << 22;          // bound of the merge-slot wait (~0.1 s)
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kBufferDword3 = 0x00020000;   // raw buffer, 32-bit data format
@@ -175,23 +177,24 @@ __device__ __forceinline__ void process_block(BlockRegs<D> &r, const bf16x8 (&qo
                                                           o[dt], 0, 0, 0);
 }
 
-// Block-wide exclusive scan of one int per thread (kDecThreads threads).
-__device__ __forceinline__ int block_exclusive_scan(int v, int *sm_wave_tot, int &total) {
+// Block-wide exclusive scan of one value per thread (kDecThreads threads),
+// modulo 2^32.
+__device__ __forceinline__ unsigned block_exclusive_scan(unsigned v, unsigned *sm_wave_tot, unsigned &total) {
     const int lane = threadIdx.x % kWave;
     const int wave = threadIdx.x / kWave;
-    int x = v;
+    unsigned x = v;
 #pragma unroll
     for (int off = 1; off < kWave; off <<= 1) {
-        const int y = __shfl_up(x, off);
+        const unsigned y = __shfl_up(x, off);
         if (lane >= off) x += y;
     }
     if (lane == kWave - 1) sm_wave_tot[wave] = x;
     __syncthreads();
-    int before = 0;
+    unsigned before = 0;
     total = 0;
 #pragma unroll
     for (int w = 0; w < kDecWaves; ++w) {
-        const int t = sm_wave_tot[w];
+        const unsigned t = sm_wave_tot[w];
         if (w < wave) before += t;
         total += t;
     }
@@ -199,15 +202,23 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int *sm_wave_tot, int
 }
 
 // Persistent decode: a fixed grid (about two workgroups per CU) walks the work
-// items (session s, split k, KV head g) round-robin.  Each workgroup first
-// computes, in LDS, how many splits every session needs (a prefix sum over the
-// batch), so no workgroup is launched for a split that does not exist, and it
-// fetches the next item's block ids while it works on the current one.
+// items (session s, split k, KV head g).  Each workgroup first orders, in LDS,
+// the work rows (session, split) longest first: every full split (T tokens),
+// then each session's last, shorter split by block count, largest first (an
+// empty session's one row is among them).  Items are dealt in snake order:
+// round k gives item k*W + w to workgroup w for even k and k*W + W-1-w for odd
+// k (W workgroups), so every workgroup receives about the same number of
+// tokens; with plain round-robin the workgroups holding one item more than the
+// rest decide the call's duration.  Every workgroup derives the same order
+// from the lengths, no workgroup is launched for a split that does not exist,
+// and each fetches the next item's block ids while it works on the current one.
 template <int D, int kDepth, int kMaxPerWave>
 __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
-    __shared__ int sm_cum[kMaxBatch + 1];       // first work row of each session
+    __shared__ int sm_cum[kMaxBatch + 1];       // first full-split row of each session
     __shared__ int sm_len[kMaxBatch];           // attended length of each session
-    __shared__ int sm_wave_tot[kDecWaves];
+    __shared__ int sm_porder[kMaxBatch];        // sessions of the short-split rows, in row order
+    __shared__ int sm_key[kDecThreads];         // block count of a session's short split (-1: none)
+    __shared__ unsigned sm_wave_tot[kDecWaves];
     // Per-item merge slots (double-buffered): each wave leaves its (m, l, O) of
     // the group's heads, the last wave to arrive merges them.
     __shared__ float sm_m[2][kDecWaves][kMaxGroup];
@@ -226,25 +237,56 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
         sm_arrived[tid] = 0;
         sm_merged[tid] = 0;
     }
-    // ---- splits per session and their prefix sum
+    // ---- work rows: full splits per session (prefix sum) and short splits.
+    // Both counts share one unsigned scan: full rows in bits 0..19 (at most
+    // kMaxBatch * kMaxSplits = 2^19 in total), short rows (at most kMaxBatch)
+    // in bits 20..31.
     const int per_thread = (S + kDecThreads - 1) / kDecThreads;
     const int s_begin = min(S, tid * per_thread);
     const int s_end = min(S, s_begin + per_thread);
-    int mine = 0;
+    auto has_short = [&](int L) { return L == 0 || L % T != 0; };   // an empty session still owns one row
+    unsigned mine = 0;
     for (int s = s_begin; s < s_end; ++s) {
         const int L = attended_len(a, s, blockIdx.x == 0);
         sm_len[s] = L;
-        mine += L > 0 ? (L + T - 1) / T : 1;        // an empty session still owns one row
+        mine += (unsigned)(L / T) + (has_short(L) ? 1u << 20 : 0u);
     }
-    int total_rows = 0;
-    int run = block_exclusive_scan(mine, sm_wave_tot, total_rows);
-    for (int s = s_begin; s < s_end; ++s) {
-        sm_cum[s] = run;
-        run += sm_len[s] > 0 ? (sm_len[s] + T - 1) / T : 1;
+    unsigned packed_total = 0;
+    const unsigned packed_run = block_exclusive_scan(mine, sm_wave_tot, packed_total);
+    const int full_rows = (int)(packed_total & 0xFFFFFu);
+    const int total_rows = full_rows + (int)(packed_total >> 20);
+    {
+        int frun = (int)(packed_run & 0xFFFFFu), prun = (int)(packed_run >> 20);
+        for (int s = s_begin; s < s_end; ++s) {
+            const int L = sm_len[s];
+            sm_cum[s] = frun;
+            frun += L / T;
+            if (has_short(L)) {
+                if (S > kDecThreads) sm_porder[prun] = s;         // large batch: session order
+                ++prun;
+            }
+        }
+        if (S <= kDecThreads && tid < S) {
+            const int L = sm_len[tid];
+            sm_key[tid] = has_short(L) ? (L % T + kBlock - 1) / kBlock : -1;
+        }
     }
-    if (tid == 0) sm_cum[S] = total_rows;
+    if (tid == 0) sm_cum[S] = full_rows;
+    __syncthreads();
+    if (S <= kDecThreads && tid < S && sm_key[tid] >= 0) {
+        // rank among short rows: larger block count first, then session order
+        const int key = sm_key[tid];
+        int rank = 0;
+        for (int j = 0; j < S; ++j) {
+            const int kj = sm_key[j];
+            rank += (kj > key) || (kj == key && j < tid);
+        }
+        sm_porder[rank] = tid;
+    }
     __syncthreads();
     const int total_items = total_rows * a.num_kv_heads;
+    const int W = (int)gridDim.x;
+    auto item_of = [&](int round) { return round * W + ((round & 1) ? W - 1 - (int)blockIdx.x : (int)blockIdx.x); };
 
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
     const int lane = tid % kWave;
@@ -256,8 +298,16 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
 #pragma unroll
     for (int dt = 0; dt < D / 16; ++dt) voff[dt] = ((dt * 16 + c16) * kBlock + g4 * 4) * 2;
 
-    // (session, split) of work row r: largest s with sm_cum[s] <= r.
+    // (session, split) of work row r.  A full row: the largest s with
+    // sm_cum[s] <= r (a session without full splits shares its sm_cum with the
+    // next session, so it is never the largest).  A short row: its session's
+    // last split.
     auto locate = [&](int row, int &s_out, int &split_out) {
+        if (row >= full_rows) {
+            s_out = sm_porder[row - full_rows];
+            split_out = sm_len[s_out] / T;
+            return;
+        }
         int lo = 0, hi = S - 1;
         while (lo < hi) {
             const int mid = (lo + hi + 1) >> 1;
@@ -310,7 +360,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
     // its own LDS slots (double-buffered; read back with readlane), so no value
     // loaded from memory is carried around the item loop.
     __shared__ int sm_ids[kDecWaves][2][kMaxSplitTokens / kBlock];
-    int item = blockIdx.x;
+    int item = item_of(0);
     int s = 0, split = 0;
     if (item < total_items) {
         locate(item / a.num_kv_heads, s, split);
@@ -324,13 +374,13 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
             load_block<D>(r[j], a.pool, a.num_kv_heads, item % a.num_kv_heads, bb[j], koff, voff);
         }
     }
-    for (int k = 0; item < total_items; item += gridDim.x, ++k) {
+    for (int k = 0; item < total_items; ++k, item = item_of(k)) {
         const int g = item % a.num_kv_heads;
         const int L = sm_len[s];
         const int cur_s = s, cur_split = split;
         const int cur_ids = lane < kMaxSplitTokens / kBlock ? sm_ids[wave][k & 1][lane] : -1;
         // Next item: its (session, split) and block ids, fetched now.
-        const int next = item + gridDim.x;
+        const int next = item_of(k + 1);
         const bool has_next = next < total_items;
         int next_ids = -1;
         if (has_next) {
