@@ -212,6 +212,148 @@ ls_status kv_blocks_restore(ls_kv_pool *pool, int32_t n, const int32_t *block_id
                             const int32_t *block_ids_host, const void *staging,
                             int32_t staging_on_host, hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * KV manager (host only): the policy that decides which blocks the
+ * stash/restore calls above move — next-use-aware eviction (§5.1) with the
+ * indexed candidate heap (§6) and speech-triggered preload with admission,
+ * cancellation and synchronous fallback (§5.2).  It tracks, per session, the
+ * block table (by block position: device block, host slot, state) and the
+ * side-table metadata of §6 (running, speech/barge-in protection, warm
+ * protection after a preload, playback horizon, reply-interval average).
+ * It launches nothing: a call that frees or assigns blocks returns moves, and
+ * the caller issues the copies (kv_blocks_stash for evictions,
+ * kv_blocks_restore for restores) on a stream before any kernel writes the
+ * freed blocks or reads the restored ones.  Host slots index the caller's
+ * host store of whole blocks (staging layout above).  Device block ids and
+ * host slots are handed out lowest first.  One manager must not be used from
+ * two threads at once.  Status and ls_last_error() as for the rest of the ABI.
+ * ---------------------------------------------------------------------- */
+
+typedef struct ls_kv_manager ls_kv_manager;
+
+typedef struct {
+    int64_t num_device_blocks;  /* pool block ids the manager owns: [0, n) */
+    int64_t num_host_slots;     /* host store capacity in blocks: slots [0, n) */
+    int32_t max_sessions;       /* session ids are [0, max_sessions) */
+    double reply_prior_s;       /* T_reply before a session's first observed reply interval */
+    double reply_ema_alpha;     /* weight of the newest interval in the moving average, (0, 1] */
+    double seconds_per_token;   /* playback per unfinished response token, when the horizon is unknown */
+    double warm_ttl_s;          /* how long a completed preload stays protected */
+    int64_t warm_cap_blocks;    /* cap on blocks under that protection (oldest released first) */
+} ls_kv_manager_desc;
+
+/* Block states in kv_manager_table. */
+#define LS_KV_RESIDENT  0       /* in the pool at the listed device block */
+#define LS_KV_OFFLOADED 1       /* in the host store at the listed host slot */
+#define LS_KV_LOADING   2       /* restore issued: host slot -> device block, not yet done */
+
+/* Session flags in kv_manager_session_info. */
+#define LS_KV_RUNNING   0x1     /* pinned by a running request */
+#define LS_KV_IMMEDIATE 0x2     /* speech start / barge-in: protected from eviction */
+#define LS_KV_WARM      0x4     /* protected after a completed preload */
+#define LS_KV_EVICTABLE 0x8     /* an eviction candidate (idle, resident blocks, unprotected) */
+
+/* One block move: position `position` of `session` between device block
+ * `device_block` and host slot `host_slot` (direction given by the call). */
+typedef struct {
+    int32_t session;
+    int32_t position;
+    int32_t device_block;
+    int32_t host_slot;
+} ls_kv_move;
+
+/* Create / destroy (destroy frees host metadata only; NULL is OK). */
+ls_status kv_manager_create(const ls_kv_manager_desc *desc, ls_kv_manager **out);
+ls_status kv_manager_destroy(ls_kv_manager *m);
+
+/* Register / forget a session (forgetting returns its blocks and slots). */
+ls_status kv_manager_add_session(ls_kv_manager *m, int32_t session);
+ls_status kv_manager_remove_session(ls_kv_manager *m, int32_t session);
+
+/* Allocate n device blocks at the tail of the session's table (new tokens);
+ * block_ids[n] receives them.  LS_ENOMEM when fewer than n are free: evict
+ * first (kv_manager_evict). */
+ls_status kv_manager_append_blocks(ls_kv_manager *m, int32_t session, int32_t n, int32_t *block_ids);
+
+/* A request of the session starts (running != 0: its KV is pinned, and the
+ * speech and warm protections end) or finishes (running == 0: idle). */
+ls_status kv_manager_set_running(ls_kv_manager *m, int32_t session, int32_t running);
+
+/* Monitor inputs to T_next = T_play + T_reply (§5.1).  t_play_s: remaining
+ * playback horizon, or < 0 when unknown (then unfinished_tokens x
+ * seconds_per_token stands in).  observe_reply: one interval from playback
+ * completion to the next completed user input (moving average). */
+ls_status kv_manager_set_playback(ls_kv_manager *m, int32_t session, double t_play_s,
+                                  int64_t unfinished_tokens);
+ls_status kv_manager_observe_reply(ls_kv_manager *m, int32_t session, double interval_s);
+
+/* Speech start or barge-in: the session's resident KV becomes immediate
+ * reuse, excluded from eviction until its request runs. */
+ls_status kv_manager_speech_start(ls_kv_manager *m, int32_t session);
+
+/*
+ * Free at least blocks_needed device blocks (fewer only when every eligible
+ * block is gone or the host store is full): eligible sessions in decreasing
+ * T_next (ties: smaller id first), each from its last resident position
+ * downwards (suffix first, §5.1).  Writes the moves (device block -> host
+ * slot) to moves[0 .. *num_moves); the blocks are free once the call returns,
+ * so the caller stashes them before anything else writes them.
+ * LS_ENOMEM if max_moves < blocks_needed.
+ */
+ls_status kv_manager_evict(ls_kv_manager *m, int64_t blocks_needed, ls_kv_move *moves,
+                           int32_t max_moves, int32_t *num_moves);
+
+/*
+ * Speech-triggered preload (§5.2).  Marks the session immediate (as
+ * kv_manager_speech_start).  When it has offloaded blocks, the preload is
+ * admitted (*admitted = 1) only if offloaded blocks x bytes_per_block /
+ * bandwidth_bytes_per_s <= time_available_s (the time left before its LLM
+ * stage runs, under the current transfer pressure the caller measures) and
+ * enough device blocks are free or can be freed from eligible sessions.  Then
+ * restores[0 .. *num_restores) lists, prefix first, every offloaded position
+ * with its host slot and newly assigned device block (state LOADING), and
+ * evictions[0 .. *num_evictions) the blocks evicted to make room: stash those
+ * before restoring into them.  Not admitted: *admitted = 0, nothing moves;
+ * the caller may retry later or load on demand (kv_manager_load_sync).
+ * LS_ENOMEM if max_restores is below the offloaded count; LS_EINVAL if a
+ * preload of the session is still in flight.
+ */
+ls_status kv_manager_preload(ls_kv_manager *m, int32_t session, double time_available_s,
+                             double bytes_per_block, double bandwidth_bytes_per_s,
+                             ls_kv_move *restores, int32_t max_restores, int32_t *num_restores,
+                             ls_kv_move *evictions, int32_t max_evictions, int32_t *num_evictions,
+                             int32_t *admitted);
+
+/* The synchronous fallback: kv_manager_preload without the time test;
+ * LS_ENOMEM when not enough device blocks can be freed. */
+ls_status kv_manager_load_sync(ls_kv_manager *m, int32_t session, ls_kv_move *restores,
+                               int32_t max_restores, int32_t *num_restores, ls_kv_move *evictions,
+                               int32_t max_evictions, int32_t *num_evictions);
+
+/* The restores of the session's preload have completed (the caller has
+ * waited on their stream): LOADING blocks become resident, their host slots
+ * free, and unless the session is running its KV is protected for warm_ttl_s
+ * (releasing the oldest protections beyond warm_cap_blocks). */
+ls_status kv_manager_preload_done(ls_kv_manager *m, int32_t session, double now_s);
+
+/* Abandon the session's preload: LOADING blocks return to OFFLOADED and their
+ * device blocks are freed (the caller must not let the abandoned restores
+ * land after those blocks are reused: same stream, or wait first). */
+ls_status kv_manager_preload_cancel(ls_kv_manager *m, int32_t session);
+
+/* Release warm protections older than warm_ttl_s at time now_s. */
+ls_status kv_manager_tick(ls_kv_manager *m, double now_s);
+
+/* Queries: T_next, LS_KV_* flags and table length; the table itself
+ * (device block or -1, host slot or -1, LS_KV_* state per position; NULL
+ * arrays are skipped; LS_ENOMEM if max_blocks is below the length); counts. */
+ls_status kv_manager_session_info(ls_kv_manager *m, int32_t session, double *t_next, int32_t *flags,
+                                  int32_t *num_blocks);
+ls_status kv_manager_table(ls_kv_manager *m, int32_t session, int32_t max_blocks, int32_t *device_ids,
+                           int32_t *host_slots, int32_t *states);
+ls_status kv_manager_counts(ls_kv_manager *m, int64_t *free_device_blocks, int64_t *free_host_slots,
+                            int64_t *evictable_blocks, int64_t *warm_blocks);
+
 /*
  * Wait for `stream`, then return (and clear) the device error word of the
  * current device in *bits (LS_DEVERR_* bits; 0 when no kernel met a bad index).

@@ -140,6 +140,15 @@ ls_status copy_blocks(ls_kv_pool *pool, int32_t n, const int32_t *block_ids,
 }
 
 }  // namespace
+
+// Message for ls_last_error() from code outside this file (the KV manager).
+void set_last_error(const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(t_last_error, sizeof t_last_error, fmt, ap);
+    va_end(ap);
+}
+
 }  // namespace ls
 
 using namespace ls;
