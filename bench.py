@@ -13,7 +13,7 @@ and the KV-block restore/stash scatter legs (48 layers x 4 KV heads x 128 dims,
 side stream.  Inputs are seeded synthetic sessions, resident in HBM before the
 timed region starts.  ``cpu_baseline`` is the CPU oracle timed on this host.
 
-Usage: python bench.py [--steps K] [--warmup W] [--legs decode,prefill,talker,restore,calib]
+Usage: python bench.py [--steps K] [--warmup W] [--legs decode,prefill,talker,restore,kvm,calib]
 (decode always runs; "calib" adds a 1 GiB plain device copy used to scale the
 rocprofv3 HBM-traffic counters.)
 """
@@ -44,7 +44,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--legs", default="decode,prefill,talker,restore")
+    ap.add_argument("--legs", default="decode,prefill,talker,restore,kvm")
     ap.add_argument("--prefill-reps", type=int, default=5)
     ap.add_argument("--restore-reps", type=int, default=5)
     ap.add_argument("--restore-sessions", type=int, default=128)
@@ -450,6 +450,107 @@ def restore_leg(torch, kv, W, args, dec):
             "host_leg": host}
 
 
+def _replay_manager(m, tr, limit, times):
+    """Drive a KV manager (library or oracle: same calls) through a trace.
+
+    Set-up fills the pool session by session, evicting a fifth of the pool
+    whenever the next context does not fit; then each event is replayed:
+    monitor updates, eviction under pressure, and turns (speech-start preload,
+    synchronous load when not admitted, the turn's appended blocks, new
+    playback horizon and reply interval).  Wall time of each manager call is
+    recorded by kind; the moves are returned for comparison."""
+    import time
+    free = tr.num_device_blocks
+    log_moves = []
+    def call(kind, fn, *a):
+        t0 = time.perf_counter_ns()
+        r = fn(*a)
+        if times is not None:
+            times.setdefault(kind, []).append(time.perf_counter_ns() - t0)
+        return r
+    for s in range(len(tr.context_blocks)):
+        m.add_session(s)
+    for s, nb in enumerate(tr.context_blocks):
+        nb = int(nb)
+        if free < nb:
+            ev = m.evict(max(nb - free, tr.num_device_blocks // 5))
+            free += len(ev)
+        m.append_blocks(s, nb)
+        free -= nb
+    now = 0.0
+    for e in tr.events[:limit]:
+        now += 0.01
+        if e[0] == "play":
+            call("update", m.set_playback, e[1], e[2])
+        elif e[0] == "pressure":
+            ev = call("evict", m.evict, e[1])
+            free += len(ev)
+            log_moves.append(("evict", [tuple(int(x) for x in r) for r in ev]))
+        else:
+            _, s, t_avail, nb, reply, t_play = e
+            adm, r, ev = call("preload", m.preload, s, t_avail, tr.bytes_per_block, tr.bandwidth)
+            if not adm:
+                r, ev = call("load_sync", m.load_sync, s)
+            free += len(ev) - len(r)
+            log_moves.append(("load", [tuple(int(x) for x in x_) for x_ in r], [tuple(int(x) for x in x_) for x_ in ev]))
+            m.preload_done(s, now)
+            m.set_running(s, True)
+            if free < nb:
+                ev = call("evict", m.evict, nb - free)
+                free += len(ev)
+                log_moves.append(("evict", [tuple(int(x) for x in r) for r in ev]))
+            m.append_blocks(s, nb)
+            free -= nb
+            m.set_running(s, False)
+            m.observe_reply(s, reply)
+            call("update", m.set_playback, s, t_play)
+            m.tick(now)
+    return log_moves
+
+
+def kvm_leg(W):
+    """Host overhead of the KV manager's decisions (the eviction-index overhead
+    of §7): the library at full trace scale, and the library against the
+    brute-force oracle (a sort of all candidates per eviction, the scan the
+    indexed heap replaces) on a reduced trace, where their moves must agree."""
+    import time
+    from paper_2606_22983_amd.kv_manager import KVManager
+    from oracle.kv_manager import RefKVManager
+    def summary(t):
+        out = {}
+        for k, v in t.items():
+            a = np.array(v, dtype=np.float64) / 1e3
+            out[k] = {"calls": len(v), "avg_us": round(float(a.mean()), 2), "p90_us": round(float(np.percentile(a, 90)), 2)}
+        return out
+    def make(cls, tr):
+        return cls(tr.num_device_blocks, tr.num_host_slots, len(tr.context_blocks), reply_prior_s=3.0,
+                   reply_ema_alpha=0.5, seconds_per_token=0.04, warm_ttl_s=5.0)
+    full = W.manager_trace()
+    t_lib = {}
+    t0 = time.perf_counter()
+    _replay_manager(make(KVManager, full), full, None, t_lib)
+    full_s = time.perf_counter() - t0
+    small = W.manager_trace(num_sessions=256, num_events=400)
+    t_ref, t_small = {}, {}
+    ref_moves = _replay_manager(make(RefKVManager, small), small, None, t_ref)
+    lib_moves = _replay_manager(make(KVManager, small), small, None, t_small)
+    if ref_moves != lib_moves:
+        raise AssertionError("KV manager: library moves differ from the oracle's on the reduced trace")
+    log("kv manager: %d sessions, %d events in %.2f s; evict avg %.1f us (oracle scan at %d sessions: %.0f us)" % (
+        len(full.context_blocks), len(full.events), full_s, np.mean(t_lib["evict"]) / 1e3,
+        len(small.context_blocks), np.mean(t_ref["evict"]) / 1e3))
+    return {"workload": "KV manager trace: %d sessions (contexts lognormal, median 64 blocks), pool holding half "
+                        "their KV (%d blocks), %d events (monitor updates, eviction under pressure, speech-start "
+                        "preloads with synchronous fallback)" % (len(full.context_blocks), full.num_device_blocks,
+                                                                  len(full.events)),
+            "per_call_through_python_binding": summary(t_lib),
+            "reduced_trace": {"sessions": len(small.context_blocks), "events": len(small.events),
+                              "library": summary(t_small), "oracle_scan": summary(t_ref),
+                              "moves_identical": True},
+            "paper_context": "eviction overhead 0.093 ms avg / 0.222 ms P90 with the heap index vs "
+                             "5.311 / 8.270 ms with tail scanning (Python, their testbed)"}
+
+
 def calib_leg(torch, args):
     """A plain device copy of known size, the reference for HBM traffic counters
     (FETCH_SIZE / WRITE_SIZE of this kernel per launch should read 1 GiB each)."""
@@ -498,6 +599,8 @@ def main():
         torch.cuda.empty_cache()
     if "restore" in legs:
         extra["restore"] = restore_leg(torch, kv, W, args, dec)
+    if "kvm" in legs:
+        extra["kv_manager"] = kvm_leg(W)
     if calib:
         extra["calibration_copy"] = calib
     cpu = None if args.no_cpu_baseline else cpu_baseline(dec, W)

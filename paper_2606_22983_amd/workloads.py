@@ -281,3 +281,51 @@ def restore_case(seed: int = SEEDS["restore"], num_sessions: int = 128, tokens: 
     b = rng.permutation(num_blocks)[:n].astype(np.int32)
     return RestoreCase(name="kv_restore", seed=seed, num_layers=num_layers, num_kv_heads=hkv,
                        head_dim=d, num_blocks=num_blocks, stash_ids=a, restore_ids=b)
+
+
+@dataclass
+class ManagerTrace:
+    """Seeded event sequence for the KV manager (the policy of §5.1, §5.2).
+
+    ``context_blocks[s]``: blocks of session s's reused multi-turn context at the
+    start.  ``events``: tuples
+      ("play", s, t_play)       monitor update of the remaining playback horizon (s)
+      ("pressure", n)           running requests need n more device blocks
+      ("turn", s, t_avail, new_blocks, reply_s, t_play)
+                                speech start with t_avail seconds before the LLM
+                                stage runs, then the turn appends new_blocks; the
+                                observed reply interval and the new reply's horizon.
+    """
+    name: str
+    seed: int
+    num_device_blocks: int
+    num_host_slots: int
+    context_blocks: np.ndarray
+    events: list
+    bytes_per_block: float
+    bandwidth: float
+
+
+def manager_trace(seed: int = 26066, num_sessions: int = 4096, num_events: int = 20000,
+                  device_fraction: float = 0.5) -> ManagerTrace:
+    """Multi-turn speech sessions against a pool that holds about half of their
+    KV: contexts lognormal (median 64 blocks = 1024 tokens, sigma 1, clipped to
+    [4, 1024] blocks), playback horizons U[0, 30] s, reply intervals U[0.5, 8] s,
+    speech-to-LLM-stage windows U[0.1, 2] s, turns of U[1, 16] new blocks.
+    Blocks are the thinker's all-layer slab (48 layers x 4 KV heads x 128 dims x
+    16 tokens x K,V in bf16 = 1.5 MiB); host link 50 GB/s."""
+    rng = np.random.default_rng(seed)
+    ctx = np.clip(np.round(np.exp(np.log(64) + rng.standard_normal(num_sessions))), 4, 1024).astype(np.int64)
+    total = int(ctx.sum())
+    kinds = rng.choice(3, size=num_events, p=[0.6, 0.2, 0.2])
+    events = []
+    for k in kinds:
+        if k == 0:
+            events.append(("play", int(rng.integers(num_sessions)), float(rng.uniform(0, 30))))
+        elif k == 1:
+            events.append(("pressure", int(rng.integers(8, 65))))
+        else:
+            events.append(("turn", int(rng.integers(num_sessions)), float(rng.uniform(0.1, 2.0)),
+                           int(rng.integers(1, 17)), float(rng.uniform(0.5, 8.0)), float(rng.uniform(0, 30))))
+    return ManagerTrace("kv manager trace", seed, int(total * device_fraction), 2 * total, ctx, events,
+                        48 * 4 * 128 * 16 * 2 * 2.0, 50e9)
