@@ -212,6 +212,23 @@ ls_status kv_blocks_restore(ls_kv_pool *pool, int32_t n, const int32_t *block_id
                             const int32_t *block_ids_host, const void *staging,
                             int32_t staging_on_host, hipStream_t stream);
 
+/*
+ * kv_blocks_restore_layers — kv_blocks_restore of the layers
+ * [layer_begin, layer_begin + layer_count) only, from the same all-layer
+ * staging layout.  A next-turn prefill can then start on layer l as soon as
+ * layer l is back, while later layers are still being restored (the reload
+ * leaves the critical path, §5.2 and §7): the caller restores layer by layer
+ * on a copy stream and makes the compute stream wait on an event per layer.
+ * With host staging, each chunk is one strided host-to-device copy (the
+ * range of every block) into the ring, then the scatter kernel; the ring must
+ * hold the range of one block.  LS_EINVAL for a range outside [0, num_layers);
+ * otherwise as kv_blocks_restore.  Restoring every layer range of a set of
+ * blocks gives the same pool as one kv_blocks_restore.
+ */
+ls_status kv_blocks_restore_layers(ls_kv_pool *pool, int32_t layer_begin, int32_t layer_count, int32_t n,
+                                   const int32_t *block_ids, const int32_t *block_ids_host,
+                                   const void *staging, int32_t staging_on_host, hipStream_t stream);
+
 /* ------------------------------------------------------------------------
  * KV manager (host only): the policy that decides which blocks the
  * stash/restore calls above move — next-use-aware eviction (§5.1) with the

@@ -96,43 +96,54 @@ ls_status check_ids_host(const PoolGeom &p, int32_t n, const int32_t *ids) {
     return LS_OK;
 }
 
-ls_status copy_blocks(ls_kv_pool *pool, int32_t n, const int32_t *block_ids,
+// Copy the slabs of layers [lb, lb + lc) of n blocks between the pool and a
+// block-major all-layer staging array (device, or pinned host through the ring).
+ls_status copy_blocks(ls_kv_pool *pool, int32_t lb, int32_t lc, int32_t n, const int32_t *block_ids,
                       const int32_t *block_ids_host, void *staging, int32_t staging_on_host,
                       bool to_pool, hipStream_t stream) {
     if (ls_status st = check_pool(pool)) return st;
     const PoolGeom &p = pool->geom;
+    if (lb < 0 || lc < 1 || lb > p.num_layers - lc)
+        return fail(LS_EINVAL, "layer range [%d, %d + %d) outside [0, %d)", lb, lb, lc, p.num_layers);
     if (n < 0) return fail(LS_EINVAL, "n must be >= 0");
     if (n == 0) return LS_OK;
     if (!block_ids || !staging) return fail(LS_EINVAL, "block_ids and staging must not be NULL");
     if (n > p.num_blocks) return fail(LS_EINVAL, "n (%d) exceeds num_blocks", n);
     if (block_ids_host)
         if (ls_status st = check_ids_host(p, n, block_ids_host)) return st;
-    const size_t per_block = p.slab_bytes() * (size_t)p.num_layers;
-    if (staging_on_host && (!p.ring || p.ring_bytes < per_block))
-        return fail(LS_ENOMEM, "host staging needs a device staging ring of at least %zu bytes",
-                    per_block);
+    const size_t per_block = p.slab_bytes() * (size_t)p.num_layers;   // staging stride of a block
+    const size_t range = p.slab_bytes() * (size_t)lc;                   // bytes of the layer range
+    if (staging_on_host && (!p.ring || p.ring_bytes < range))
+        return fail(LS_ENOMEM, "host staging needs a device staging ring of at least %zu bytes", range);
     unsigned int *err = device_error_word();
     if (!err) return fail(LS_EHIP, "cannot resolve the device error word");
     if (!staging_on_host) {
-        hipError_t e = launch_block_copy(p, n, block_ids, static_cast<uint8_t *>(staging), to_pool, err, stream);
+        hipError_t e = launch_block_copy(p, n, block_ids, static_cast<uint8_t *>(staging), lb, lc,
+                                         p.num_layers, lb, to_pool, err, stream);
         return e == hipSuccess ? LS_OK : hip_fail(e, "block copy launch");
     }
-    // Whole blocks per chunk, in id order, all on the caller's stream.
-    const int32_t chunk = (int32_t)(p.ring_bytes / per_block);
-    uint8_t *host = static_cast<uint8_t *>(staging);
+    // Whole blocks per chunk, in id order, all on the caller's stream.  The
+    // ring holds the layer range of each block compactly; a range narrower
+    // than all layers moves as a strided (2D) copy of one row per block.
+    const int32_t chunk = (int32_t)(p.ring_bytes / range);
+    uint8_t *host = static_cast<uint8_t *>(staging) + p.slab_bytes() * (size_t)lb;
     for (int32_t i0 = 0; i0 < n; i0 += chunk) {
         const int32_t cnt = (n - i0) < chunk ? (n - i0) : chunk;
-        const size_t bytes = per_block * (size_t)cnt;
+        uint8_t *h = host + per_block * (size_t)i0;
         hipError_t e;
         if (to_pool) {
-            e = hipMemcpyAsync(p.ring, host + per_block * (size_t)i0, bytes, hipMemcpyHostToDevice, stream);
+            e = range == per_block
+                    ? hipMemcpyAsync(p.ring, h, range * (size_t)cnt, hipMemcpyHostToDevice, stream)
+                    : hipMemcpy2DAsync(p.ring, range, h, per_block, range, cnt, hipMemcpyHostToDevice, stream);
             if (e != hipSuccess) return hip_fail(e, "restore host-to-device copy");
-            e = launch_block_copy(p, cnt, block_ids + i0, p.ring, true, err, stream);
+            e = launch_block_copy(p, cnt, block_ids + i0, p.ring, lb, lc, lc, 0, true, err, stream);
             if (e != hipSuccess) return hip_fail(e, "restore scatter launch");
         } else {
-            e = launch_block_copy(p, cnt, block_ids + i0, p.ring, false, err, stream);
+            e = launch_block_copy(p, cnt, block_ids + i0, p.ring, lb, lc, lc, 0, false, err, stream);
             if (e != hipSuccess) return hip_fail(e, "stash gather launch");
-            e = hipMemcpyAsync(host + per_block * (size_t)i0, p.ring, bytes, hipMemcpyDeviceToHost, stream);
+            e = range == per_block
+                    ? hipMemcpyAsync(h, p.ring, range * (size_t)cnt, hipMemcpyDeviceToHost, stream)
+                    : hipMemcpy2DAsync(h, per_block, p.ring, range, range, cnt, hipMemcpyDeviceToHost, stream);
             if (e != hipSuccess) return hip_fail(e, "stash device-to-host copy");
         }
     }
@@ -300,14 +311,22 @@ ls_status paged_attn_prefill(ls_kv_pool *pool, int32_t layer, int32_t num_sessio
 ls_status kv_blocks_stash(ls_kv_pool *pool, int32_t n, const int32_t *block_ids,
                           const int32_t *block_ids_host, void *staging, int32_t staging_on_host,
                           hipStream_t stream) {
-    return copy_blocks(pool, n, block_ids, block_ids_host, staging, staging_on_host, false, stream);
+    return copy_blocks(pool, 0, pool ? pool->geom.num_layers : 1, n, block_ids, block_ids_host, staging,
+                       staging_on_host, false, stream);
 }
 
 ls_status kv_blocks_restore(ls_kv_pool *pool, int32_t n, const int32_t *block_ids,
                             const int32_t *block_ids_host, const void *staging,
                             int32_t staging_on_host, hipStream_t stream) {
-    return copy_blocks(pool, n, block_ids, block_ids_host, const_cast<void *>(staging),
-                       staging_on_host, true, stream);
+    return copy_blocks(pool, 0, pool ? pool->geom.num_layers : 1, n, block_ids, block_ids_host,
+                       const_cast<void *>(staging), staging_on_host, true, stream);
+}
+
+ls_status kv_blocks_restore_layers(ls_kv_pool *pool, int32_t layer_begin, int32_t layer_count, int32_t n,
+                                   const int32_t *block_ids, const int32_t *block_ids_host,
+                                   const void *staging, int32_t staging_on_host, hipStream_t stream) {
+    return copy_blocks(pool, layer_begin, layer_count, n, block_ids, block_ids_host,
+                       const_cast<void *>(staging), staging_on_host, true, stream);
 }
 
 ls_status ls_device_errors(uint32_t *bits, hipStream_t stream) {

@@ -58,8 +58,12 @@ DecodePlan plan_decode(const PoolGeom &p, int32_t num_sessions, int32_t num_q_he
                        int32_t max_blocks_per_session);
 
 // Kernel launchers (each returns the hipError_t of its launch).
+// Copies the slabs of layers [layer_begin, layer_begin + layer_count) of blocks
+// ids[0..n): staging block i holds stage_block_slabs slabs, layer_begin's is
+// its stage_layer0-th.
 hipError_t launch_block_copy(const PoolGeom &p, int32_t n, const int32_t *ids, uint8_t *staging,
-                             bool to_pool, unsigned int *err, hipStream_t stream);
+                             int32_t layer_begin, int32_t layer_count, int32_t stage_block_slabs,
+                             int32_t stage_layer0, bool to_pool, unsigned int *err, hipStream_t stream);
 hipError_t launch_append_decode(const PoolGeom &p, int layer, int32_t num_sessions,
                                 const uint16_t *k_new, const uint16_t *v_new,
                                 const int32_t *block_tables, int32_t max_blocks,

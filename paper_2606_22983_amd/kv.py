@@ -45,11 +45,13 @@ _lib.paged_attn_prefill.argtypes = [_p, _i32, _i32, _i32, _p, _p, _p, _p, _p, _i
                                     _i32, _f32, _p, _p]
 _lib.kv_blocks_stash.argtypes = [_p, _i32, _p, _p, _p, _i32, _p]
 _lib.kv_blocks_restore.argtypes = [_p, _i32, _p, _p, _p, _i32, _p]
+_lib.kv_blocks_restore_layers.argtypes = [_p, _i32, _i32, _i32, _p, _p, _p, _i32, _p]
 _lib.ls_device_errors.argtypes = [ctypes.POINTER(ctypes.c_uint32), _p]
 _lib.ls_last_error.restype = ctypes.c_char_p
 _lib.ls_version.restype = ctypes.c_char_p
 for _f in (_lib.kv_pool_create, _lib.kv_pool_destroy, _lib.paged_attn_decode,
            _lib.paged_attn_prefill, _lib.kv_blocks_stash, _lib.kv_blocks_restore,
+           _lib.kv_blocks_restore_layers,
            _lib.ls_device_errors):
     _f.restype = ctypes.c_int
 
@@ -232,6 +234,21 @@ def kv_blocks_restore(pool: KVPool, block_ids: torch.Tensor, staging: torch.Tens
     _check(_lib.kv_blocks_restore(pool.handle, block_ids.numel(), _ptr(block_ids), hp,
                                   _ptr(staging), 1 if on_host else 0, _stream(stream)),
            "kv_blocks_restore")
+    del keep
+
+
+def kv_blocks_restore_layers(pool: KVPool, layer_begin: int, layer_count: int, block_ids: torch.Tensor,
+                             staging: torch.Tensor, block_ids_host=None, stream=None):
+    """Restore layers [layer_begin, layer_begin + layer_count) of ``block_ids`` from an
+    all-layer ``staging`` (device or pinned host)."""
+    _dev(block_ids, "block_ids", torch.int32)
+    on_host = not staging.is_cuda
+    if on_host and not staging.is_pinned():
+        raise ValueError("host staging must be pinned memory")
+    keep, hp = _host_ids(block_ids_host)
+    _check(_lib.kv_blocks_restore_layers(pool.handle, layer_begin, layer_count, block_ids.numel(),
+                                         _ptr(block_ids), hp, _ptr(staging), 1 if on_host else 0,
+                                         _stream(stream)), "kv_blocks_restore_layers")
     del keep
 
 

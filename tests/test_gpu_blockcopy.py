@@ -148,3 +148,31 @@ def test_decode_unchanged_by_concurrent_restore(kv):
     got = dp.host()
     assert np.array_equal(got[:, free], host_bits(staging).transpose(1, 0, 2, 3, 4))
     log("decode bit-identical under a concurrent restore of %d blocks" % n)
+
+
+@pytest.mark.parametrize("on_host", [False, True])
+def test_restore_by_layer_ranges_equals_full_restore(kv, oracle_lib, on_host):
+    """Layer ranges [0,1), [1,4), [4,5) restored one by one (device staging, or
+    pinned host staging through a ring narrower than a whole block) give the
+    oracle's full restore, byte for byte."""
+    rng = np.random.default_rng(31 + on_host)
+    nl, hkv, d, nb, n = 5, 2, 64, 40, 13
+    pool = _random_pool(rng, nl, nb, hkv, d)
+    ids = rng.permutation(nb)[:n].astype(np.int32)
+    staging = _random_pool(rng, n, nl, hkv, d).reshape(n, nl, 2, hkv, 16 * d)
+    expect = oracle_lib.restore(pool.copy(), 16, d, ids, staging)
+    layer_bytes = 2 * hkv * 16 * d * 2
+    dp = DevicePool(kv, pool, d, ring_blocks=0)
+    if on_host:
+        ring = torch.empty(5 * layer_bytes, dtype=torch.uint8, device="cuda")   # 5 layer slabs
+        dp.pool = kv.kv_pool_create(dp.data, nl, nb, hkv, d, 16, ring)
+        st = torch.from_numpy(staging.view(np.int16)).pin_memory()
+    else:
+        st = bf16_dev(staging)
+    for lb, lc in ((0, 1), (1, 3), (4, 1)):
+        kv.kv_blocks_restore_layers(dp.pool, lb, lc, i32_dev(ids), st, block_ids_host=ids)
+    torch.cuda.synchronize()
+    assert np.array_equal(dp.host(), expect)
+    with pytest.raises(kv.LiveServeError):
+        kv.kv_blocks_restore_layers(dp.pool, 4, 2, i32_dev(ids), st)
+    assert kv.ls_device_errors() == 0

@@ -1,0 +1,90 @@
+"""Layer-pipelined restore -> next-turn prefill (§5.2: the reload leaves the
+critical path): layer l of a turn's context is restored on a copy stream and
+the prefill of layer l waits only for that layer's event.  The outputs equal,
+bit for bit, those of a full restore followed by the prefill of every layer,
+and match the oracle."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2606_22983_amd import workloads as W
+from tests.gpu_util import DevicePool, assert_attn_close, bf16_dev, i32_dev
+
+pytestmark = pytest.mark.gpu
+
+NL, HKV, HQ, D = 4, 4, 32, 128
+
+
+@pytest.fixture(scope="module")
+def kv():
+    from paper_2606_22983_amd import kv as kv_mod
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return kv_mod
+
+
+def _case(rng, n, c):
+    n, c = np.asarray(n), np.asarray(c)
+    need = (c + n + 15) // 16
+    ctx_blocks = (c + 15) // 16
+    nb = int(need.sum()) + 4
+    perm = rng.permutation(nb).astype(np.int32)
+    tables = np.full((len(n), int(need.max())), -1, np.int32)
+    pos = 0
+    for s, k in enumerate(need):
+        tables[s, :k] = perm[pos:pos + k]
+        pos += k
+    pool = W.normal_bf16(rng, (NL, nb, 2, HKV, 16 * D))
+    ctx_ids = np.concatenate([tables[s, :ctx_blocks[s]] for s in range(len(n))]).astype(np.int32)
+    t = int(n.sum())
+    q = [W.normal_bf16(rng, (t, HQ, D)) for _ in range(NL)]
+    kn = [W.normal_bf16(rng, (t, HKV, D)) for _ in range(NL)]
+    vn = [W.normal_bf16(rng, (t, HKV, D)) for _ in range(NL)]
+    return pool, tables, ctx_ids, q, kn, vn
+
+
+def test_layer_pipelined_restore_then_prefill(kv, oracle_lib):
+    rng = np.random.default_rng(41)
+    n, c = [64, 33], [300, 517]
+    pool, tables, ctx_ids, q, kn, vn = _case(rng, n, c)
+    cu = np.concatenate([[0], np.cumsum(n)]).astype(np.int32)
+    scale = 1 / math.sqrt(D)
+    args = (i32_dev(cu), i32_dev(c), max(n), i32_dev(tables), scale)
+    qd, knd, vnd = [bf16_dev(x) for x in q], [bf16_dev(x) for x in kn], [bf16_dev(x) for x in vn]
+
+    def run(pipelined):
+        dp = DevicePool(kv, pool, D, ring_blocks=8)
+        store = torch.empty((len(ctx_ids), NL, 2, HKV, 16 * D), dtype=torch.int16, pin_memory=True)
+        ids = i32_dev(ctx_ids)
+        kv.kv_blocks_stash(dp.pool, ids, store, block_ids_host=ctx_ids)       # offload the context
+        dp.data.view(NL, pool.shape[1], -1)[:, ids.long()] = float("nan")     # its blocks are reused
+        outs = [torch.empty_like(x) for x in qd]
+        main = torch.cuda.current_stream()
+        if pipelined:
+            copy = torch.cuda.Stream()
+            copy.wait_stream(main)
+            events = []
+            with torch.cuda.stream(copy):
+                for l in range(NL):
+                    kv.kv_blocks_restore_layers(dp.pool, l, 1, ids, store, block_ids_host=ctx_ids)
+                    e = torch.cuda.Event()
+                    e.record(copy)
+                    events.append(e)
+            for l in range(NL):
+                main.wait_event(events[l])
+                kv.paged_attn_prefill(dp.pool, l, qd[l], *args[:4], args[4], outs[l], knd[l], vnd[l])
+        else:
+            kv.kv_blocks_restore(dp.pool, ids, store, block_ids_host=ctx_ids)
+            for l in range(NL):
+                kv.paged_attn_prefill(dp.pool, l, qd[l], *args[:4], args[4], outs[l], knd[l], vnd[l])
+        torch.cuda.synchronize()
+        return outs
+
+    seq, pipe = run(False), run(True)
+    for l in range(NL):
+        assert torch.equal(seq[l].view(torch.int16), pipe[l].view(torch.int16)), "layer %d" % l
+    for l in (0, NL - 1):
+        ref = oracle_lib.prefill(pool, 16, D, l, q[l], kn[l], vn[l], cu, np.array(c), tables, scale)
+        assert_attn_close(pipe[l], ref, "pipelined prefill, layer %d" % l)
+    assert kv.ls_device_errors() == 0
