@@ -13,7 +13,7 @@ and the KV-block restore/stash scatter legs (48 layers x 4 KV heads x 128 dims,
 side stream.  Inputs are seeded synthetic sessions, resident in HBM before the
 timed region starts.  ``cpu_baseline`` is the CPU oracle timed on this host.
 
-Usage: python bench.py [--steps K] [--warmup W] [--legs decode,prefill,talker,restore,kvm,calib]
+Usage: python bench.py [--steps K] [--warmup W] [--legs decode,prefill,talker,restore,pipeline,kvm,calib]
 (decode always runs; "calib" adds a 1 GiB plain device copy used to scale the
 rocprofv3 HBM-traffic counters.)
 """
@@ -44,7 +44,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--legs", default="decode,prefill,talker,restore,kvm")
+    ap.add_argument("--legs", default="decode,prefill,talker,restore,pipeline,kvm")
     ap.add_argument("--prefill-reps", type=int, default=5)
     ap.add_argument("--restore-reps", type=int, default=5)
     ap.add_argument("--restore-sessions", type=int, default=128)
@@ -450,6 +450,108 @@ def restore_leg(torch, kv, W, args, dec):
             "host_leg": host}
 
 
+def pipeline_leg(torch, kv, W, args):
+    """Reload of an offloaded context followed by the next-turn prefill of all
+    48 layers: restore-then-prefill against the layer-pipelined form, where
+    layer l is restored on a copy stream and its prefill waits only for that
+    layer (kv_blocks_restore_layers + one event per layer).  Host staging (the
+    paper's DRAM path through the staging ring) and device staging."""
+    case = W.pipeline_turn()
+    NL, HKV, HQ, D, nb = case.num_layers, case.num_kv_heads, case.num_q_heads, case.head_dim, case.num_blocks
+    dev = "cuda"
+    g = torch.Generator(device=dev)
+    g.manual_seed(case.seed)
+    pool_t = torch.randn(NL * nb * 2 * HKV * 16 * D, generator=g, device=dev).to(torch.bfloat16)
+    ring = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+    pool = kv.kv_pool_create(pool_t, NL, nb, HKV, D, 16, ring)
+    ctx = case.context_block_ids
+    ids = torch.from_numpy(ctx).to(dev)
+    shape = (len(ctx), NL, 2, HKV, 16 * D)
+    store_host = torch.empty(shape, dtype=torch.int16, pin_memory=True)
+    store_dev = torch.empty(shape, dtype=torch.int16, device=dev)
+    kv.kv_blocks_stash(pool, ids, store_host, block_ids_host=ctx)
+    kv.kv_blocks_stash(pool, ids, store_dev, block_ids_host=ctx)
+    n, c = case.new_lens, case.reused_lens
+    t = int(n.sum())
+    cu = torch.from_numpy(np.concatenate([[0], np.cumsum(n)]).astype(np.int32)).to(dev)
+    c_d = torch.from_numpy(c).to(dev)
+    tables = torch.from_numpy(case.block_tables).to(dev)
+    q = torch.randn((t, HQ, D), generator=g, device=dev).to(torch.bfloat16)
+    kn = torch.randn((t, HKV, D), generator=g, device=dev).to(torch.bfloat16)
+    vn = torch.randn((t, HKV, D), generator=g, device=dev).to(torch.bfloat16)
+    out = torch.empty_like(q)
+    scale = 1 / math.sqrt(D)
+    main = torch.cuda.current_stream()
+    copy = torch.cuda.Stream()
+
+    def prefill(l):
+        kv.paged_attn_prefill(pool, l, q, cu, c_d, int(n.max()), tables, scale, out, kn, vn)
+
+    def timed(fn):
+        st, en = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        st.record(main)
+        fn()
+        en.record(main)
+        torch.cuda.synchronize()
+        return st.elapsed_time(en)
+
+    def restore(store):
+        kv.kv_blocks_restore(pool, ids, store, block_ids_host=ctx)
+
+    def prefill_all():
+        for l in range(NL):
+            prefill(l)
+
+    def sequential(store):
+        restore(store)
+        prefill_all()
+
+    def pipelined(store):
+        # Enqueue order interleaves the two streams (restore l+1, then the
+        # prefill of l), so the host never holds a prefill back behind the
+        # enqueueing of later restores.
+        copy.wait_stream(main)
+        events = []
+
+        def restore_layer(l):
+            with torch.cuda.stream(copy):
+                kv.kv_blocks_restore_layers(pool, l, 1, ids, store, block_ids_host=ctx)
+                e = torch.cuda.Event()
+                e.record(copy)
+                events.append(e)
+        restore_layer(0)
+        for l in range(NL):
+            if l + 1 < NL:
+                restore_layer(l + 1)
+            main.wait_event(events[l])
+            prefill(l)
+        main.wait_stream(copy)
+
+    res = {}
+    prefill_all()
+    for name, store in (("host_staging", store_host), ("device_staging", store_dev)):
+        runs = {"restore": [], "prefill": [], "sequential": [], "pipelined": []}
+        pipelined(store)
+        for _ in range(3):
+            runs["restore"].append(timed(lambda: restore(store)))
+            runs["prefill"].append(timed(prefill_all))
+            runs["sequential"].append(timed(lambda: sequential(store)))
+            runs["pipelined"].append(timed(lambda: pipelined(store)))
+        med = {k: float(np.median(v)) for k, v in runs.items()}
+        res[name] = {"restore_ms": round(med["restore"], 3), "prefill_48_layers_ms": round(med["prefill"], 3),
+                     "restore_then_prefill_ms": round(med["sequential"], 3),
+                     "pipelined_ms": round(med["pipelined"], 3),
+                     "hidden_ms": round(med["sequential"] - med["pipelined"], 3)}
+        log("pipeline (%s): restore %.2f ms, prefill %.2f ms, restore-then-prefill %.2f ms, pipelined %.2f ms" % (
+            name, med["restore"], med["prefill"], med["sequential"], med["pipelined"]))
+    pool.close()
+    gib = len(ctx) * NL * 2 * HKV * 16 * D * 2 / 2**30
+    return {"workload": "%d sessions, n=%s new tokens over c=%s reused tokens, 48 layers x 32/4 heads x D=128; "
+                        "%.2f GiB of context restored" % (len(n), list(map(int, n)), list(map(int, c)), gib),
+            **res}
+
+
 def _replay_manager(m, tr, limit, times):
     """Drive a KV manager (library or oracle: same calls) through a trace.
 
@@ -599,6 +701,9 @@ def main():
         torch.cuda.empty_cache()
     if "restore" in legs:
         extra["restore"] = restore_leg(torch, kv, W, args, dec)
+    if "pipeline" in legs:
+        extra["restore_prefill_pipeline"] = pipeline_leg(torch, kv, W, args)
+        torch.cuda.empty_cache()
     if "kvm" in legs:
         extra["kv_manager"] = kvm_leg(W)
     if calib:

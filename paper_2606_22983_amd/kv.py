@@ -12,6 +12,7 @@ import ctypes
 import os
 from typing import Optional
 
+import numpy as np
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -202,10 +203,11 @@ def paged_attn_prefill(pool: KVPool, layer: int, q: torch.Tensor, cu_new_lens: t
 
 
 def _host_ids(ids):
+    """Host int32 copy of the ids (kept alive by the caller) and its address."""
     if ids is None:
         return None, None
-    arr = (ctypes.c_int32 * len(ids))(*[int(x) for x in ids])
-    return arr, ctypes.cast(arr, ctypes.c_void_p)
+    arr = np.ascontiguousarray(ids, dtype=np.int32)
+    return arr, ctypes.c_void_p(arr.ctypes.data)
 
 
 def kv_blocks_stash(pool: KVPool, block_ids: torch.Tensor, staging: torch.Tensor,

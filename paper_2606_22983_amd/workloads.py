@@ -329,3 +329,36 @@ def manager_trace(seed: int = 26066, num_sessions: int = 4096, num_events: int =
                            int(rng.integers(1, 17)), float(rng.uniform(0.5, 8.0)), float(rng.uniform(0, 30))))
     return ManagerTrace("kv manager trace", seed, int(total * device_fraction), 2 * total, ctx, events,
                         48 * 4 * 128 * 16 * 2 * 2.0, 50e9)
+
+
+@dataclass
+class PipelineTurn:
+    """Next-turn prefill whose reused context was offloaded (every layer)."""
+    name: str
+    seed: int
+    num_layers: int
+    num_kv_heads: int
+    num_q_heads: int
+    head_dim: int
+    num_blocks: int
+    new_lens: np.ndarray
+    reused_lens: np.ndarray
+    block_tables: np.ndarray
+    context_block_ids: np.ndarray   # blocks holding reused context, session after session
+
+
+def pipeline_turn(seed: int = 26067, num_sessions: int = 4, num_layers: int = 48) -> PipelineTurn:
+    """Sessions of the thinker's geometry (48 layers, 32/4 heads, D = 128) come
+    back for a new turn of n ~ U[256, 1024] tokens over c ~ U[8192, 16384]
+    reused tokens that sit in host DRAM (the reload before prefill of §5.2 and
+    §7); block ids are a permutation of a pool 1.1x the blocks needed."""
+    rng = np.random.default_rng(seed)
+    n = rng.integers(256, 1025, size=num_sessions).astype(np.int32)
+    c = rng.integers(8192, 16385, size=num_sessions).astype(np.int32)
+    need = _blocks_for(c.astype(np.int64) + n)
+    nb = int(need.sum() * 1.1) + 1
+    perm = rng.permutation(nb).astype(np.int32)
+    tables = _tables(perm, need, int(need.max()))
+    ctx = np.concatenate([tables[s, :(int(c[s]) + BLOCK - 1) // BLOCK] for s in range(num_sessions)])
+    return PipelineTurn("layer-pipelined reload + next-turn prefill", seed, num_layers, 4, 32, 128, nb, n, c,
+                        tables, ctx.astype(np.int32))

@@ -65,15 +65,20 @@ def test_layer_pipelined_restore_then_prefill(kv, oracle_lib):
             copy = torch.cuda.Stream()
             copy.wait_stream(main)
             events = []
-            with torch.cuda.stream(copy):
-                for l in range(NL):
+
+            def restore_layer(l):
+                with torch.cuda.stream(copy):
                     kv.kv_blocks_restore_layers(dp.pool, l, 1, ids, store, block_ids_host=ctx_ids)
                     e = torch.cuda.Event()
                     e.record(copy)
                     events.append(e)
+            restore_layer(0)
             for l in range(NL):
+                if l + 1 < NL:
+                    restore_layer(l + 1)
                 main.wait_event(events[l])
                 kv.paged_attn_prefill(dp.pool, l, qd[l], *args[:4], args[4], outs[l], knd[l], vnd[l])
+            main.wait_stream(copy)
         else:
             kv.kv_blocks_restore(dp.pool, ids, store, block_ids_host=ctx_ids)
             for l in range(NL):
