@@ -13,7 +13,7 @@ and the KV-block restore/stash scatter legs (48 layers x 4 KV heads x 128 dims,
 side stream.  Inputs are seeded synthetic sessions, resident in HBM before the
 timed region starts.  ``cpu_baseline`` is the CPU oracle timed on this host.
 
-Usage: python bench.py [--steps K] [--warmup W] [--legs decode,prefill,talker,restore,pipeline,kvm,calib]
+Usage: python bench.py [--steps K] [--warmup W] [--legs decode,prefill,talker,restore,pipeline,kvm,sched,calib]
 (decode always runs; "calib" adds a 1 GiB plain device copy used to scale the
 rocprofv3 HBM-traffic counters.)
 """
@@ -44,7 +44,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--legs", default="decode,prefill,talker,restore,pipeline,kvm")
+    ap.add_argument("--legs", default="decode,prefill,talker,restore,pipeline,kvm,sched")
     ap.add_argument("--prefill-reps", type=int, default=5)
     ap.add_argument("--restore-reps", type=int, default=5)
     ap.add_argument("--restore-sessions", type=int, default=128)
@@ -653,6 +653,46 @@ def kvm_leg(W):
                              "5.311 / 8.270 ms with tail scanning (Python, their testbed)"}
 
 
+def sched_leg():
+    """Host cost of one interaction-aware scheduling round (§4's algorithm) for
+    ready sets of 256 and 1024 requests, through the Python binding, with the
+    plain oracle timed on the same rounds (orders must agree)."""
+    import time
+    from paper_2606_22983_amd import scheduler as S
+    from oracle.scheduler import schedule_round as ref_round
+    rng = np.random.default_rng(26068)
+    out = {}
+    for n in (256, 1024):
+        lib_t, ref_t = [], []
+        for _ in range(50):
+            t = S.requests(n)
+            t["playback_buffer_s"] = rng.uniform(0, 4, n)
+            t["ready_age_s"] = rng.uniform(0, 10, n)
+            t["first_audio_done"] = rng.random(n) < 0.7
+            t["kv_blocks_held"] = rng.integers(64, 2048, n)
+            t["tokens_needed"] = rng.integers(1, 64, n)
+            t["kv_blocks_needed"] = rng.integers(0, 4, n)
+            stage = (1.0, 1.0, 0.002, float(rng.uniform(0.5, 1.0)), 8192, 512)
+            t0 = time.perf_counter_ns()
+            order, adm, _, _ = S.ls_schedule_round(t, *stage)
+            lib_t.append(time.perf_counter_ns() - t0)
+            reqs = [dict(P=float(r["playback_buffer_s"]), age=float(r["ready_age_s"]),
+                         first_audio=bool(r["first_audio_done"]), K=int(r["kv_blocks_held"]),
+                         tokens=int(r["tokens_needed"]), blocks=int(r["kv_blocks_needed"])) for r in t]
+            t0 = time.perf_counter_ns()
+            r_order, r_adm, _, _ = ref_round(reqs, *stage)
+            ref_t.append(time.perf_counter_ns() - t0)
+            if list(map(int, order)) != r_order or adm != r_adm:
+                raise AssertionError("scheduler: library order differs from the oracle's")
+        out["ready_%d" % n] = {"library_us_avg": round(float(np.mean(lib_t)) / 1e3, 2),
+                               "library_us_p90": round(float(np.percentile(lib_t, 90)) / 1e3, 2),
+                               "oracle_us_avg": round(float(np.mean(ref_t)) / 1e3, 1)}
+    log("scheduler round: %s" % out)
+    return {"workload": "50 rounds each of 256 and 1024 ready requests (buffers U[0,4] s, 70% past first audio, "
+                        "KV U[64,2048] blocks), P_safe 1 s, alpha 1, beta 0.002, budgets 8192 tokens / 512 blocks",
+            **out}
+
+
 def calib_leg(torch, args):
     """A plain device copy of known size, the reference for HBM traffic counters
     (FETCH_SIZE / WRITE_SIZE of this kernel per launch should read 1 GiB each)."""
@@ -706,6 +746,8 @@ def main():
         torch.cuda.empty_cache()
     if "kvm" in legs:
         extra["kv_manager"] = kvm_leg(W)
+    if "sched" in legs:
+        extra["scheduler"] = sched_leg()
     if calib:
         extra["calibration_copy"] = calib
     cpu = None if args.no_cpu_baseline else cpu_baseline(dec, W)

@@ -371,6 +371,50 @@ ls_status kv_manager_table(ls_kv_manager *m, int32_t session, int32_t max_blocks
 ls_status kv_manager_counts(ls_kv_manager *m, int64_t *free_device_blocks, int64_t *free_host_slots,
                             int64_t *evictable_blocks, int64_t *warm_blocks);
 
+/* ------------------------------------------------------------------------
+ * Interaction-aware batch selection (host only; §4, the scheduling procedure
+ * and its algorithm): one stage, one scheduling round.  It orders the ready
+ * requests by urgency class and admits them into the next batch under the
+ * round's token and KV-block budgets; the batch is what paged_attn_decode /
+ * paged_attn_prefill then run.
+ * ---------------------------------------------------------------------- */
+
+typedef struct {
+    double playback_buffer_s;   /* stage-aware playback buffer P (s); NaN: unknown */
+    double ready_age_s;         /* time since the request became ready (A) */
+    int32_t first_audio_done;   /* 1 once it produced its first playable audio */
+    int32_t reserved;
+    int64_t kv_blocks_held;     /* GPU KV it occupies (K); < 0: unknown */
+    int64_t tokens_needed;      /* token budget it uses if admitted */
+    int64_t kv_blocks_needed;   /* KV blocks it allocates if admitted */
+} ls_sched_request;
+
+typedef struct {
+    double p_safe_s;            /* minimum safe buffer P_safe (> 0) */
+    double alpha;               /* weight of the barge-in exposure cost */
+    double beta;                /* weight of the KV-pressure benefit */
+    double kv_occupancy;        /* occupied / allocatable GPU KV of the stage (R_occ); NaN: unknown */
+    int64_t token_budget;       /* round budgets M */
+    int64_t kv_block_budget;
+} ls_sched_stage;
+
+/*
+ * Classes: 0 (U0) first audio done and P <= P_safe, ordered by P ascending;
+ * 1 (U1) no first audio yet, ordered by ready age descending; 2 (U2) the
+ * rest, ordered by U = beta * K * R_occ - alpha * max(0, P - P_safe) / P_safe
+ * descending.  order[0..n) receives the request indices in priority order
+ * (U0, then U1, then U2; ties to the smaller index); the scan admits them in
+ * that order and stops at the first one that does not fit the remaining
+ * budgets: order[0 .. *num_admitted) is the batch.  classes[i] and
+ * utility[i] (per request index; either may be NULL) give the class and, for
+ * U2, the utility.  Fail-closed: if any P is NaN, every request is class 1
+ * (ready-age order); if R_occ is NaN or a U2 request's K is negative, U2 is
+ * ordered by ready age.  LS_EINVAL for p_safe <= 0, NaN weights or ages,
+ * negative budgets or demands.
+ */
+ls_status ls_schedule_round(const ls_sched_stage *stage, int32_t n, const ls_sched_request *requests,
+                            int32_t *order, int32_t *classes, double *utility, int32_t *num_admitted);
+
 /*
  * Wait for `stream`, then return (and clear) the device error word of the
  * current device in *bits (LS_DEVERR_* bits; 0 when no kernel met a bad index).
