@@ -123,9 +123,10 @@ size_t ls_decode_workspace_bytes(const ls_kv_pool *pool, int32_t num_sessions,
  *
  *   q              device bf16 [num_sessions][num_q_heads][head_dim]: the step's query
  *   k_new, v_new   device bf16 [num_sessions][num_kv_heads][head_dim], or both NULL.
- *                  When given, the step's own K/V row is first written at logical
- *                  position context_lens[s] (its block must already be in the table)
- *                  and the query attends to context_lens[s] + 1 keys.
+ *                  When given, the step's own K/V row is appended: the query attends
+ *                  to context_lens[s] + 1 keys, the last being this row, and the row
+ *                  is written at logical position context_lens[s] (its block must
+ *                  already be in the table) by the same launch.
  *   block_tables   device int32 [num_sessions][max_blocks_per_session]
  *   context_lens   device int32 [num_sessions]: tokens already in the pool, >= 1
  *                  (>= 0 with append).  A length whose keys do not fit the table

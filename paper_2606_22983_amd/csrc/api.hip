@@ -256,14 +256,10 @@ ls_status paged_attn_decode(ls_kv_pool *pool, int32_t layer, int32_t num_session
         return fail(LS_ENOMEM, "workspace_bytes (%zu) < required (%zu)", workspace_bytes, plan.total());
     unsigned int *err = device_error_word();
     if (!err) return fail(LS_EHIP, "cannot resolve the device error word");
-    if (k_new) {
-        hipError_t e = launch_append_decode(p, layer, num_sessions, static_cast<const uint16_t *>(k_new),
-                                            static_cast<const uint16_t *>(v_new), block_tables,
-                                            max_blocks_per_session, context_lens, err, stream);
-        if (e != hipSuccess) return hip_fail(e, "append launch");
-    }
+    // The step's own K/V row is written by the decode kernel (no separate append launch).
     hipError_t e = launch_decode(p, layer, num_sessions, num_q_heads, static_cast<const uint16_t *>(q),
-                                 k_new != nullptr, block_tables, max_blocks_per_session, context_lens,
+                                 static_cast<const uint16_t *>(k_new), static_cast<const uint16_t *>(v_new),
+                                 block_tables, max_blocks_per_session, context_lens,
                                  scale, static_cast<uint16_t *>(out), workspace, plan, err, stream);
     return e == hipSuccess ? LS_OK : hip_fail(e, "decode launch");
 }

@@ -1,9 +1,8 @@
-// KV append: write the new tokens' K and V rows into their pool slots before
-// attention reads them — the decode step's own token (autoregressive decode,
-// LiveServe §2.1 / §6) and a next turn's tokens (prefill over reused context,
-// §5).  Slot of logical token t of session s: block block_tables[s][t / 16],
-// offset t % 16; K tiles are chunk-major ([D/8][16 tokens][8 dims]), V tiles
-// dim-major.
+// KV append of a next turn's tokens (prefill over reused context, §5): write
+// their K and V rows into their pool slots before attention reads them.  Slot
+// of logical token t of session s: block block_tables[s][t / 16], offset
+// t % 16; K tiles are chunk-major ([D/8][16 tokens][8 dims]), V tiles
+// dim-major.  (The decode step's own token is written by the decode kernel.)
 #include "common.h"
 
 namespace ls {
@@ -16,26 +15,19 @@ __global__ void append_kernel(uint16_t *__restrict__ layer_pool, int64_t num_blo
                               const uint16_t *__restrict__ k_new,
                               const uint16_t *__restrict__ v_new,
                               const int32_t *__restrict__ block_tables, int32_t max_blocks,
-                              const int32_t *__restrict__ context_lens,   // decode: position
-                              const int32_t *__restrict__ cu_new_lens,    // prefill: cu[S+1]
+                              const int32_t *__restrict__ cu_new_lens,    // cu[S+1]
                               const int32_t *__restrict__ reused_lens,
                               unsigned int *err) {
     const int32_t tok = blockIdx.x;
     const int32_t g = blockIdx.y;
-    int32_t s, pos;
-    if (cu_new_lens == nullptr) {
-        s = tok;
-        pos = context_lens[s];
-    } else {
-        // session of this token: largest s with cu[s] <= tok
-        int lo = 0, hi = num_sessions - 1;
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (cu_new_lens[mid] <= tok) lo = mid; else hi = mid - 1;
-        }
-        s = lo;
-        pos = reused_lens[s] + (tok - cu_new_lens[s]);
+    // session of this token: largest s with cu[s] <= tok
+    int lo = 0, hi = num_sessions - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (cu_new_lens[mid] <= tok) lo = mid; else hi = mid - 1;
     }
+    const int32_t s = lo;
+    const int32_t pos = reused_lens[s] + (tok - cu_new_lens[s]);
     const int32_t jb = pos / kBlock;
     if (pos < 0 || jb >= max_blocks) {
         if (threadIdx.x == 0) flag_error(err, LS_DEVERR_LENGTH);
@@ -59,19 +51,6 @@ __global__ void append_kernel(uint16_t *__restrict__ layer_pool, int64_t num_blo
 
 }  // namespace
 
-hipError_t launch_append_decode(const PoolGeom &p, int layer, int32_t num_sessions,
-                                const uint16_t *k_new, const uint16_t *v_new,
-                                const int32_t *block_tables, int32_t max_blocks,
-                                const int32_t *context_lens, unsigned int *err,
-                                hipStream_t stream) {
-    if (num_sessions <= 0) return hipSuccess;
-    hipLaunchKernelGGL(append_kernel, dim3(num_sessions, p.num_kv_heads), dim3(p.head_dim), 0,
-                       stream, p.layer_base(layer), p.num_blocks, p.num_kv_heads, p.head_dim,
-                       num_sessions, k_new, v_new, block_tables, max_blocks, context_lens,
-                       (const int32_t *)nullptr, (const int32_t *)nullptr, err);
-    return hipGetLastError();
-}
-
 hipError_t launch_append_prefill(const PoolGeom &p, int layer, int32_t num_sessions,
                                  int32_t total_tokens, const uint16_t *k_new,
                                  const uint16_t *v_new, const int32_t *cu_new_lens,
@@ -80,8 +59,8 @@ hipError_t launch_append_prefill(const PoolGeom &p, int layer, int32_t num_sessi
     if (total_tokens <= 0) return hipSuccess;
     hipLaunchKernelGGL(append_kernel, dim3(total_tokens, p.num_kv_heads), dim3(p.head_dim), 0,
                        stream, p.layer_base(layer), p.num_blocks, p.num_kv_heads, p.head_dim,
-                       num_sessions, k_new, v_new, block_tables, max_blocks,
-                       (const int32_t *)nullptr, cu_new_lens, reused_lens, err);
+                       num_sessions, k_new, v_new, block_tables, max_blocks, cu_new_lens,
+                       reused_lens, err);
     return hipGetLastError();
 }
 

@@ -64,18 +64,16 @@ DecodePlan plan_decode(const PoolGeom &p, int32_t num_sessions, int32_t num_q_he
 hipError_t launch_block_copy(const PoolGeom &p, int32_t n, const int32_t *ids, uint8_t *staging,
                              int32_t layer_begin, int32_t layer_count, int32_t stage_block_slabs,
                              int32_t stage_layer0, bool to_pool, unsigned int *err, hipStream_t stream);
-hipError_t launch_append_decode(const PoolGeom &p, int layer, int32_t num_sessions,
-                                const uint16_t *k_new, const uint16_t *v_new,
-                                const int32_t *block_tables, int32_t max_blocks,
-                                const int32_t *context_lens, unsigned int *err,
-                                hipStream_t stream);
 hipError_t launch_append_prefill(const PoolGeom &p, int layer, int32_t num_sessions,
                                  int32_t total_tokens, const uint16_t *k_new,
                                  const uint16_t *v_new, const int32_t *cu_new_lens,
                                  const int32_t *reused_lens, const int32_t *block_tables,
                                  int32_t max_blocks, unsigned int *err, hipStream_t stream);
+// With k_new / v_new (both non-null) the step's own token is attended from
+// them and written to its pool slot by the decode kernel itself.
 hipError_t launch_decode(const PoolGeom &p, int layer, int32_t num_sessions, int32_t num_q_heads,
-                         const uint16_t *q, bool appended, const int32_t *block_tables,
+                         const uint16_t *q, const uint16_t *k_new, const uint16_t *v_new,
+                         const int32_t *block_tables,
                          int32_t max_blocks, const int32_t *context_lens, float scale,
                          uint16_t *out, void *workspace, const DecodePlan &plan,
                          unsigned int *err, hipStream_t stream);

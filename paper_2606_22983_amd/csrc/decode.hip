@@ -26,6 +26,12 @@
 // stream never waits on an index fetch; a block that does not exist is loaded
 // through a zero-size buffer descriptor (no memory traffic, no branch).  Heads
 // beyond G in the 16-wide tile carry q = 0 and are never written.
+//
+// A step that appends its own token (k_new / v_new given) needs no separate
+// append launch: the wave that holds the session's last block masks the
+// token's (not yet written) pool slot, attends to the token as a one-token
+// tile built from k_new / v_new, and then writes it to the slot for the next
+// steps.
 #include <algorithm>
 
 #include "common.h"
@@ -67,7 +73,9 @@ struct DecodeArgs {
     const int32_t *block_tables;   // [S][max_blocks]
     int32_t max_blocks;
     const int32_t *lens;           // tokens already in the pool
-    int32_t appended;              // 1: the step's own token was appended at lens[s]
+    int32_t appended;              // 1: the step's own token sits at position lens[s]
+    const uint16_t *k_new;         // [S][Hkv][D] the step's own K/V (appended == 1), written
+    const uint16_t *v_new;         // to the pool by this kernel and attended from here
     float scale_log2;              // scale * log2(e)
     int32_t split_tokens;          // kPerWave * 64 of the instantiation launched
     int32_t max_splits;
@@ -218,6 +226,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
     __shared__ int sm_len[kMaxBatch];           // attended length of each session
     __shared__ int sm_porder[kMaxBatch];        // sessions of the short-split rows, in row order
     __shared__ int sm_key[kDecThreads];         // block count of a session's short split (-1: none)
+    __shared__ uint8_t sm_own[kMaxBatch];       // 1: the session's own new token is attended (fits the table)
     __shared__ unsigned sm_wave_tot[kDecWaves];
     // Per-item merge slots (double-buffered): each wave leaves its (m, l, O) of
     // the group's heads, the last wave to arrive merges them.
@@ -249,6 +258,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
     for (int s = s_begin; s < s_end; ++s) {
         const int L = attended_len(a, s, blockIdx.x == 0);
         sm_len[s] = L;
+        sm_own[s] = a.appended && a.lens[s] >= 0 && a.lens[s] + 1 <= a.max_blocks * kBlock;
         mine += (unsigned)(L / T) + (has_short(L) ? 1u << 20 : 0u);
     }
     unsigned packed_total = 0;
@@ -377,6 +387,8 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
     for (int k = 0; item < total_items; ++k, item = item_of(k)) {
         const int g = item % a.num_kv_heads;
         const int L = sm_len[s];
+        const int own = sm_own[s];
+        const int Lp = L - own;            // keys read from the pool; the own token comes from k_new
         const int cur_s = s, cur_split = split;
         const int cur_ids = lane < kMaxSplitTokens / kBlock ? sm_ids[wave][k & 1][lane] : -1;
         // Next item: its (session, split) and block ids, fetched now.
@@ -410,10 +422,45 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
             if (i >= my_n) break;
             const int j = i % kDepth;
             const int tb = (blk0 + wave + i * kDecWaves) * kBlock;
-            process_block<D>(r[j], qop, tb, bb[j] >= 0 ? L : 0, a.scale_log2, g4, m, lsum, o);
+            process_block<D>(r[j], qop, tb, bb[j] >= 0 ? Lp : 0, a.scale_log2, g4, m, lsum, o);
             if (i + kDepth < kMaxPerWave) {
                 bb[j] = bid(i + kDepth);
                 load_block<D>(r[j], a.pool, a.num_kv_heads, g, bb[j], koff, voff);
+            }
+        }
+        // The step's own token (position Lp): the wave that held its block attends
+        // to it as a one-token tile built from k_new / v_new (its pool slot was
+        // masked above) and writes it to that slot for later steps.  No other
+        // workgroup reads the slot in this launch, and the same wave already
+        // loaded the block, so the write races with no read that matters.
+        if (own && cur_split == nsplit - 1) {
+            const int bl = Lp / kBlock - blk0;             // the token's block within the split
+            if (wave == bl % kDecWaves) {
+                const int64_t row = ((int64_t)cur_s * a.num_kv_heads + g) * D;
+                BlockRegs<D> nr;
+#pragma unroll
+                for (int ks = 0; ks < D / 32; ++ks) {
+                    const u32x4 kv = *reinterpret_cast<const u32x4 *>(a.k_new + row + ks * 32 + g4 * 8);
+                    nr.k[ks] = c16 == 0 ? kv : u32x4{0u, 0u, 0u, 0u};
+                }
+#pragma unroll
+                for (int dt = 0; dt < D / 16; ++dt) {
+                    const uint32_t v0 = a.v_new[row + dt * 16 + c16];
+                    nr.v[dt] = u32x2{g4 == 0 ? v0 : 0u, 0u};
+                }
+                process_block<D>(nr, qop, Lp, Lp + 1, a.scale_log2, g4, m, lsum, o);
+                const int blk = checked_id(cur_ids, bl, nblk);
+                if (blk >= 0) {
+                    const int t = Lp % kBlock;
+                    uint16_t *pool = const_cast<uint16_t *>(a.pool);
+                    const int64_t tile = (int64_t)kBlock * D;
+                    uint16_t *kt = pool + ((int64_t)blk * 2 * a.num_kv_heads + g) * tile;
+                    uint16_t *vt = kt + (int64_t)a.num_kv_heads * tile;
+                    for (int d = lane; d < D; d += kWave) {
+                        kt[((d >> 3) * kBlock + t) * 8 + (d & 7)] = a.k_new[row + d];
+                        vt[d * kBlock + t] = a.v_new[row + d];
+                    }
+                }
             }
         }
         // Request the next item's first blocks and q before merging this one.
@@ -596,7 +643,8 @@ DecodePlan plan_decode(const PoolGeom &p, int32_t num_sessions, int32_t num_q_he
 }
 
 hipError_t launch_decode(const PoolGeom &p, int layer, int32_t num_sessions, int32_t num_q_heads,
-                         const uint16_t *q, bool appended, const int32_t *block_tables,
+                         const uint16_t *q, const uint16_t *k_new, const uint16_t *v_new,
+                         const int32_t *block_tables,
                          int32_t max_blocks, const int32_t *context_lens, float scale,
                          uint16_t *out, void *workspace, const DecodePlan &plan,
                          unsigned int *err, hipStream_t stream) {
@@ -610,7 +658,9 @@ hipError_t launch_decode(const PoolGeom &p, int layer, int32_t num_sessions, int
     a.block_tables = block_tables;
     a.max_blocks = max_blocks;
     a.lens = context_lens;
-    a.appended = appended ? 1 : 0;
+    a.appended = k_new != nullptr ? 1 : 0;
+    a.k_new = k_new;
+    a.v_new = v_new;
     a.scale_log2 = scale * kLog2e;
     a.err = err;
     a.split_tokens = plan.split_tokens;
