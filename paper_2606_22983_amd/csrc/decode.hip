@@ -545,12 +545,15 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
 }
 
 // Log-sum-exp merge of the splits of every (session, KV head) with more than
-// one.  1024 threads per (session, KV head): each wave reduces one head's split
-// statistics with shuffles, then four groups of 256 threads each sum a quarter
-// of the splits for 4 consecutive outputs (their loads issued together) and the
-// groups are added through LDS.
+// one.  1024 threads per (session, KV head): four groups of 256 threads each
+// sum a quarter of the splits for 4 consecutive outputs, and the groups are
+// added through LDS.  The first splits' outputs are requested before the split
+// statistics (which do not depend on them), so the two loads share one memory
+// latency; meanwhile each of the first G waves reduces one head's statistics
+// with shuffles.
 constexpr int kCombThreads = 1024;
 constexpr int kCombParts = kCombThreads / 256;
+constexpr int kCombPre = 8;                  // splits per thread loaded up front (32 per row)
 
 template <int D>
 __global__ __launch_bounds__(kCombThreads) void decode_combine_kernel(DecodeArgs a) {
@@ -568,6 +571,18 @@ __global__ __launch_bounds__(kCombThreads) void decode_combine_kernel(DecodeArgs
     const int64_t part = ((int64_t)s * a.num_kv_heads + g) * a.max_splits;
     const int tid = threadIdx.x;
     const int wave = tid / kWave, lane = tid % kWave;
+    const int c = tid % 256;                 // 4 consecutive outputs: base = 4c
+    const int pidx = tid / 256;              // this thread sums splits pidx, pidx + 4, ...
+    const int base = c * 4;
+    const bool active = base < G * D;
+    const float *src = a.part_acc + (part * G) * D + base;
+    f32x4 pre[kCombPre];
+#pragma unroll
+    for (int i = 0; i < kCombPre; ++i) {
+        const int k = pidx + i * kCombParts;
+        pre[i] = active && k < nsplit ? *reinterpret_cast<const f32x4 *>(src + (int64_t)k * G * D)
+                                      : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
 
     if (wave < G) {
         const int h = wave;
@@ -587,15 +602,15 @@ __global__ __launch_bounds__(kCombThreads) void decode_combine_kernel(DecodeArgs
     }
     __syncthreads();
 
-    const int c = tid % 256;                 // 4 consecutive outputs: base = 4c
-    const int pidx = tid / 256;              // this thread sums splits pidx, pidx + 4, ...
-    const int base = c * 4;
-    const bool active = base < G * D;
     const int h = active ? base / D : 0;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     if (active) {
-        const float *src = a.part_acc + (part * G) * D + base;
-        int k = pidx;
+#pragma unroll
+        for (int i = 0; i < kCombPre; ++i) {
+            const int k = pidx + i * kCombParts;
+            if (k < nsplit) acc += sm_e[k][h] * pre[i];
+        }
+        int k = pidx + kCombPre * kCombParts;
         for (; k + 3 * kCombParts < nsplit; k += 4 * kCombParts) {
             const f32x4 v0 = *reinterpret_cast<const f32x4 *>(src + (int64_t)k * G * D);
             const f32x4 v1 = *reinterpret_cast<const f32x4 *>(src + (int64_t)(k + kCombParts) * G * D);
