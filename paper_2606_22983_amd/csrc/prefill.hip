@@ -546,6 +546,10 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     //   A1: scores of unit 2j+2 | P of unit 2j+1    | read V of unit 2j+1
     //   -- barrier: stage j+1 has landed and every read of stage j is done --
     //   B1: P V of unit 2j+1    | max of unit 2j+2  | read K of unit 2j+3
+    // A wave in a B phase runs at raised issue priority: of the two waves
+    // sharing a SIMD, the one feeding P V (light VALU) then issues its MFMAs
+    // first while the other's exp work fills the VALU slots (3.5-4% faster
+    // than equal priorities; raising A instead is no faster).
     f32x4 sa[kRT][2], sb2[kRT][2];
     int32_t idk = id_k(-1), idv = id_v(-1);
     load_k(k2, idk);                      // stage -1: K unit 0 (its V part is empty)
@@ -587,11 +591,13 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
             order_phase<0, kPhaseMfma, NDT, kExpTrans, kExpValu>();
             pin(pop);
             mask_unit(sb2, j * kKeyTile + 32);
+            __builtin_amdgcn_s_setprio(1);          // B phases issue first
             pv_mfma(pop);                           // B0
             const bool r0 = max_test(sb2);
             scale_unit(sb2);
             read_k(ks + C::kUnitBytes);
             order_phase<0, kPhaseMfma, 2 * KS, 0, kMaxValu>();
+            __builtin_amdgcn_s_setprio(0);
             if (__any(r0)) rescale(sb2);
             qk_mfma(sa);                            // A1
             exp_unit(sb2, pop);
@@ -602,11 +608,13 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
         }
         stage_barrier<D>();
         if (live) {
+            __builtin_amdgcn_s_setprio(1);
             pv_mfma(pop);                           // B1
             const bool r1 = max_test(sa);
             scale_unit(sa);
             read_k(knext);                          // (unused when tile j+1 is past the end)
             order_phase<0, kPhaseMfma, 2 * KS, 0, kMaxValu>();
+            __builtin_amdgcn_s_setprio(0);
             if (__any(r1)) rescale(sa);
         }
     };
