@@ -3,11 +3,15 @@
 // autoregressive decoders (LiveServe §2.1; continuous-batching decode loop of
 // §6) over per-session block tables (block-level KV allocation, §5.1).
 //
-// Work decomposition (split-K): workgroup = (split k, KV head g, session s),
-// covering tokens [k*T, (k+1)*T) of the session.  Its 4 wavefronts take the
-// split's 16-token blocks round-robin; each keeps a wavefront-level online
-// softmax state (running max m, running sum l, unnormalised output O) for the
-// G query heads of group g.  The waves merge through LDS.  A session that fits
+// Work decomposition (split-K): an item = (split k, KV head g, session s),
+// covering tokens [k*T, (k+1)*T) of the session (T = 1024 on large batches).
+// A persistent grid holds one 8-wave workgroup per CU (one workgroup, so no
+// two workgroups on a CU compete for its issue slots: with two 4-wave
+// workgroups the second ran ~15% slower and lengthened the tail).  The 8
+// wavefronts of a workgroup take an item's 16-token blocks round-robin; each
+// keeps a wavefront-level online softmax state (running max m, running sum l,
+// unnormalised output O) for the G query heads of group g.  The waves merge
+// through LDS.  A session that fits
 // one split is written directly; otherwise each split leaves (m, l, O) in the
 // workspace and a second, small kernel merges the splits with the log-sum-exp
 // rule (kernel boundaries order the two, so no cross-workgroup fences).
@@ -46,9 +50,9 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kDecThreads = 256;
+constexpr int kDecThreads = 512;
 constexpr int kDecWaves = kDecThreads / kWave;
-constexpr int kMaxSplitTokens = 512;         // 8 blocks per wave (the unrolled sequence)
+constexpr int kMaxSplitTokens = 1024;        // 8 blocks per wave (the unrolled sequence)
 constexpr int kMaxSplits = 256;              // combine kernel's LDS capacity
 constexpr int kMaxBatch = 2048;              // sessions per decode call (LDS prefix sums)
 constexpr int kMaxGroup = 8;                 // query heads per KV head
@@ -77,7 +81,7 @@ struct DecodeArgs {
     const uint16_t *k_new;         // [S][Hkv][D] the step's own K/V (appended == 1), written
     const uint16_t *v_new;         // to the pool by this kernel and attended from here
     float scale_log2;              // scale * log2(e)
-    int32_t split_tokens;          // kPerWave * 64 of the instantiation launched
+    int32_t split_tokens;          // at most kPerWave * kDecWaves * kBlock of the instantiation
     int32_t max_splits;
     float *part_ml;                // [S][Hkv][max_splits][G][2]
     float *part_acc;               // [S][Hkv][max_splits][G][D]
@@ -640,10 +644,11 @@ DecodePlan plan_decode(const PoolGeom &p, int32_t num_sessions, int32_t num_q_he
     DecodePlan plan{};
     const int64_t max_tokens = (int64_t)max_blocks_per_session * kBlock;
     const int64_t work = (int64_t)num_sessions * p.num_kv_heads * max_tokens;
-    // Splits of 256 or 512 tokens: long enough to amortise a workgroup's start-up,
-    // short enough to give several workgroups per CU on a large batch.
-    int T = 512;
-    if (work < 256LL * 2 * 4 * 512) T = 256;
+    // Splits of 512 or 1024 tokens (4 or 8 blocks per wave): long enough to
+    // amortise an item's start-up, short enough to give every CU several items
+    // on a large batch.
+    int T = 1024;
+    if (work < 256LL * 2 * 4 * 512) T = 512;
     while (T < kMaxSplitTokens && (max_tokens + T - 1) / T > kMaxSplits) T *= 2;
     plan.split_tokens = T;
     plan.max_splits = (int)((max_tokens + T - 1) / T);
@@ -685,9 +690,9 @@ hipError_t launch_decode(const PoolGeom &p, int layer, int32_t num_sessions, int
     a.part_acc = reinterpret_cast<float *>(ws + plan.ml_bytes);
     a.num_sessions = num_sessions;
     const int64_t upper = (int64_t)num_sessions * p.num_kv_heads * plan.max_splits;
-    // Persistent grid: two 256-thread workgroups (this kernel's occupancy) on
-    // every CU the stream may use.
-    const int64_t resident = 2 * (int64_t)stream_cus(p, stream);
+    // Persistent grid: one 512-thread workgroup (8 waves, this kernel's
+    // occupancy) on every CU the stream may use.
+    const int64_t resident = (int64_t)stream_cus(p, stream);
     dim3 grid((unsigned)std::min<int64_t>(upper, resident));
 #define LS_DECODE(DD, PW) \
     hipLaunchKernelGGL((decode_kernel<DD, 2, PW>), grid, dim3(kDecThreads), 0, stream, a)
