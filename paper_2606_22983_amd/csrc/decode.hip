@@ -481,7 +481,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
         }
         lsum = wave_sum_xor_16_32(lsum);
 
-        // ---- asynchronous merge of the 4 waves: no workgroup barrier.
+        // ---- asynchronous merge of the item's waves: no workgroup barrier.
         const int slot = k & 1;
         // The slot is free once the merge of the item two steps back is done.
         // (Bounded: a wait that never ends would be a bug; it is flagged, not hung on.)
