@@ -56,6 +56,7 @@ constexpr int kMaxSplitTokens = 1024;        // 8 blocks per wave (the unrolled 
 constexpr int kMaxSplits = 256;              // combine kernel's LDS capacity
 constexpr int kMaxBatch = 2048;              // sessions per decode call (LDS prefix sums)
 constexpr int kMaxGroup = 8;                 // query heads per KV head
+constexpr int kKeyBins = kMaxSplitTokens / kBlock + 1;   // short-split block counts 0..64
 static_assert(kMaxBatch * kMaxSplits <= 0xFFFFF && kMaxBatch < 4096,
               "work-row counts must fit the packed scan (20 + 12 bits)");
 constexpr int kSpinLimit = 1 << 22;          // bound of the merge-slot wait (~0.1 s)
@@ -213,7 +214,7 @@ __device__ __forceinline__ unsigned block_exclusive_scan(unsigned v, unsigned *s
     return before + x - v;
 }
 
-// Persistent decode: a fixed grid (about two workgroups per CU) walks the work
+// Persistent decode: a fixed grid (one workgroup per CU) walks the work
 // items (session s, split k, KV head g).  Each workgroup first orders, in LDS,
 // the work rows (session, split) longest first: every full split (T tokens),
 // then each session's last, shorter split by block count, largest first (an
@@ -229,7 +230,9 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
     __shared__ int sm_cum[kMaxBatch + 1];       // first full-split row of each session
     __shared__ int sm_len[kMaxBatch];           // attended length of each session
     __shared__ int sm_porder[kMaxBatch];        // sessions of the short-split rows, in row order
-    __shared__ int sm_key[kDecThreads];         // block count of a session's short split (-1: none)
+    __shared__ __attribute__((aligned(16))) int sm_key[kDecThreads];   // block count of a session's short split (-1: none)
+    __shared__ unsigned long long sm_kmask[kKeyBins][kDecThreads / 64];  // sessions per short-split key
+    __shared__ int sm_kabove[kKeyBins + 1];     // sessions with a larger key (suffix counts)
     __shared__ uint8_t sm_own[kMaxBatch];       // 1: the session's own new token is attended (fits the table)
     __shared__ unsigned sm_wave_tot[kDecWaves];
     // Per-item merge slots (double-buffered): each wave leaves its (m, l, O) of
@@ -250,6 +253,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
         sm_arrived[tid] = 0;
         sm_merged[tid] = 0;
     }
+    for (int i = tid; i < kKeyBins * (kDecThreads / 64); i += kDecThreads) sm_kmask[i / (kDecThreads / 64)][i % (kDecThreads / 64)] = 0ull;
     // ---- work rows: full splits per session (prefix sum) and short splits.
     // Both counts share one unsigned scan: full rows in bits 0..19 (at most
     // kMaxBatch * kMaxSplits = 2^19 in total), short rows (at most kMaxBatch)
@@ -287,14 +291,41 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
     }
     if (tid == 0) sm_cum[S] = full_rows;
     __syncthreads();
-    if (S <= kDecThreads && tid < S && sm_key[tid] >= 0) {
-        // rank among short rows: larger block count first, then session order
-        const int key = sm_key[tid];
-        int rank = 0;
-        for (int j = 0; j < S; ++j) {
-            const int kj = sm_key[j];
-            rank += (kj > key) || (kj == key && j < tid);
+    // Rank of each short row: rows with a larger block count first, then
+    // session order.  Keys are block counts 0..T/16, so the rank is the number
+    // of sessions with a larger key (suffix sums of per-key counts) plus the
+    // sessions before this one with the same key (a popcount of that key's
+    // session bitmask); both are built with order-independent LDS atomics, so
+    // every workgroup derives the same order.
+    const bool ranked = S <= kDecThreads && tid < S && sm_key[tid] >= 0;
+    if (ranked) __hip_atomic_fetch_or(&sm_kmask[sm_key[tid]][tid / 64], 1ull << (tid % 64), __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_WORKGROUP);
+    __syncthreads();
+    if (S <= kDecThreads && tid < kWave) {
+        // Suffix sums over the key bins, one wave: bins 64*c + lane in chunk c.
+        int carry = 0;
+        for (int c = (kKeyBins + kWave - 1) / kWave - 1; c >= 0; --c) {
+            const int bin = c * kWave + tid;
+            int cnt = 0;
+            if (bin < kKeyBins)
+                for (int w = 0; w < kDecThreads / 64; ++w) cnt += __popcll(sm_kmask[bin][w]);
+            // inclusive suffix scan of cnt over the lanes (higher lanes first)
+            int x = cnt;
+#pragma unroll
+            for (int off = 1; off < kWave; off <<= 1) {
+                const int y = __shfl_down(x, off);
+                if (tid + off < kWave) x += y;
+            }
+            if (bin < kKeyBins) sm_kabove[bin] = carry + x - cnt;
+            carry += __shfl(x, 0);
         }
+    }
+    __syncthreads();
+    if (ranked) {
+        const int key = sm_key[tid];
+        int rank = sm_kabove[key];
+        for (int w = 0; w < tid / 64; ++w) rank += __popcll(sm_kmask[key][w]);
+        rank += __popcll(sm_kmask[key][tid / 64] & ((1ull << (tid % 64)) - 1ull));
         sm_porder[rank] = tid;
     }
     __syncthreads();

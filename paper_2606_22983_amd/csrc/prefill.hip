@@ -204,7 +204,7 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     __shared__ __attribute__((aligned(1024))) uint8_t v0[C::kStageBytes];
     __shared__ __attribute__((aligned(1024))) uint8_t v1[C::kStageBytes];
     __shared__ __attribute__((aligned(1024))) uint8_t v2[C::kStageBytes];
-    __shared__ int64_t sm_work[kMaxPairs];
+    __shared__ __attribute__((aligned(16))) int64_t sm_work[kMaxPairs];
     __shared__ int sm_items[kMaxPairs];
     __shared__ int sm_order[kMaxPairs];
 
@@ -232,13 +232,17 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
             sm_items[p] = items;
             sm_work[p] = (int64_t)items * (2 * (int64_t)max(a.ctx[sp], 0) + nt);
         }
+        if (tid == 0 && (P & 1)) sm_work[P] = -1;              // pad to 2 (never counts)
         __syncthreads();
         for (int p = tid; p < P; p += kPreThreads) {
+            // Two works per LDS read and four reads in flight.
             const int64_t w = sm_work[p];
             int r = 0;
-            for (int q = 0; q < P; ++q) {
-                const int64_t wq = sm_work[q];
-                r += (wq > w) || (wq == w && q < p);
+#pragma unroll 4
+            for (int q = 0; q < P; q += 2) {
+                const longlong2 w2 = *reinterpret_cast<const longlong2 *>(&sm_work[q]);
+                r += (w2.x > w) || (w2.x == w && q < p);
+                r += (w2.y > w) || (w2.y == w && q + 1 < p);
             }
             sm_order[r] = p;
         }
