@@ -86,6 +86,21 @@ def test_decode_lengths_and_groups(kv, oracle_lib, d, hq, hkv, append):
     assert kv.ls_device_errors() == 0
 
 
+@pytest.mark.parametrize("num_sessions", [255, 256, 257, 512, 513, 700])
+def test_decode_batch_sizes_and_equal_short_splits(kv, oracle_lib, num_sessions):
+    """Batches around the schedule's limits: up to 512 sessions the short
+    splits are ranked by block count (many equal counts here), beyond that
+    they run in session order; every item must run exactly once."""
+    rng = np.random.default_rng(num_sessions)
+    lens = rng.choice([1, 16, 17, 100, 1024, 1025, 1100, 2048, 2100], size=num_sessions)
+    pool, tables, q, _, _ = _synthetic(rng, lens, 8, 2, 64, False)
+    dp = DevicePool(kv, pool, 64)
+    out, _ = run_decode(kv, dp, bf16_dev(q), i32_dev(tables), i32_dev(lens), 0.125)
+    ref = oracle_lib.decode(pool, 16, 64, 0, q, tables, lens, 0.125)
+    assert_attn_close(out, ref, "decode %d sessions" % num_sessions)
+    assert kv.ls_device_errors() == 0
+
+
 @pytest.mark.parametrize("shape", ["rising", "spike", "falling"])
 def test_decode_peaky_scores(kv, oracle_lib, shape):
     """Large, uneven scores (key norms rising along the context, one late block of
