@@ -230,7 +230,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
     __shared__ int sm_cum[kMaxBatch + 1];       // first full-split row of each session
     __shared__ int sm_len[kMaxBatch];           // attended length of each session
     __shared__ int sm_porder[kMaxBatch];        // sessions of the short-split rows, in row order
-    __shared__ __attribute__((aligned(16))) int sm_key[kDecThreads];   // block count of a session's short split (-1: none)
+    __shared__ int sm_key[kDecThreads];         // block count of a session's short split (-1: none)
     __shared__ unsigned long long sm_kmask[kKeyBins][kDecThreads / 64];  // sessions per short-split key
     __shared__ int sm_kabove[kKeyBins + 1];     // sessions with a larger key (suffix counts)
     __shared__ uint8_t sm_own[kMaxBatch];       // 1: the session's own new token is attended (fits the table)
@@ -253,7 +253,8 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
         sm_arrived[tid] = 0;
         sm_merged[tid] = 0;
     }
-    for (int i = tid; i < kKeyBins * (kDecThreads / 64); i += kDecThreads) sm_kmask[i / (kDecThreads / 64)][i % (kDecThreads / 64)] = 0ull;
+    constexpr int kMaskWords = kDecThreads / 64;
+    for (int i = tid; i < kKeyBins * kMaskWords; i += kDecThreads) sm_kmask[i / kMaskWords][i % kMaskWords] = 0ull;
     // ---- work rows: full splits per session (prefix sum) and short splits.
     // Both counts share one unsigned scan: full rows in bits 0..19 (at most
     // kMaxBatch * kMaxSplits = 2^19 in total), short rows (at most kMaxBatch)
