@@ -329,7 +329,7 @@ def restore_leg(torch, kv, W, args, dec):
     gen.manual_seed(rc.seed)
     pool_t.random_(-32768, 32767, generator=gen)
     ring = torch.empty(128 * per_block, dtype=torch.uint8, device="cuda")
-    pool = kv.kv_pool_create(pool_t, nl, nb, hkv, d, 16, ring)
+    pool = kv.kv_pool_create(pool_t, nl, nb, hkv, d, 16)
     a = dev32(torch, rc.stash_ids)
     b = dev32(torch, rc.restore_ids)
     stream = torch.cuda.current_stream()
@@ -427,10 +427,10 @@ def restore_leg(torch, kv, W, args, dec):
     if hb > 0:
         hbuf = torch.empty(hb * per_block // 2, dtype=torch.int16, pin_memory=True)
         ids_h = b[:hb]
-        kv.kv_blocks_stash(pool, ids_h, hbuf)
+        kv.kv_blocks_stash(pool, ids_h, hbuf, ring=ring)
         torch.cuda.synchronize()
-        h2d = timed(lambda: kv.kv_blocks_restore(pool, ids_h, hbuf), 2)
-        d2h = timed(lambda: kv.kv_blocks_stash(pool, ids_h, hbuf), 2)
+        h2d = timed(lambda: kv.kv_blocks_restore(pool, ids_h, hbuf, ring=ring), 2)
+        d2h = timed(lambda: kv.kv_blocks_stash(pool, ids_h, hbuf, ring=ring), 2)
         host = {"blocks": hb, "gib": round(hb * per_block / 2 ** 30, 2),
                 "restore_gbs": round(hb * per_block / (h2d * 1e-3) / 1e9, 2),
                 "stash_gbs": round(hb * per_block / (d2h * 1e-3) / 1e9, 2),
@@ -439,7 +439,7 @@ def restore_leg(torch, kv, W, args, dec):
             host["restore_gbs"], host["stash_gbs"], host["gib"]))
         # The preload of the paper's path (host DRAM -> HBM, PCIe-bound) on a
         # side stream while the thinker decode runs on the main stream.
-        hdec = overlap_decode(lambda st: kv.kv_blocks_restore(pool, ids_h, hbuf, stream=st))
+        hdec = overlap_decode(lambda st: kv.kv_blocks_restore(pool, ids_h, hbuf, ring=ring, stream=st))
         host_overlap = {"restore_side_stream_ms": hdec["side_ms"], "gib": host["gib"],
                         "decode_steps": hdec["steps"], "decode_us_alone": round(dec_alone_ms * 1e3, 2),
                         "decode_us_concurrent": hdec["us"],
@@ -483,13 +483,13 @@ def pipeline_leg(torch, kv, W, args):
     g.manual_seed(case.seed)
     pool_t = torch.randn(NL * nb * 2 * HKV * 16 * D, generator=g, device=dev).to(torch.bfloat16)
     ring = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
-    pool = kv.kv_pool_create(pool_t, NL, nb, HKV, D, 16, ring)
+    pool = kv.kv_pool_create(pool_t, NL, nb, HKV, D, 16)
     ctx = case.context_block_ids
     ids = torch.from_numpy(ctx).to(dev)
     shape = (len(ctx), NL, 2, HKV, 16 * D)
     store_host = torch.empty(shape, dtype=torch.int16, pin_memory=True)
     store_dev = torch.empty(shape, dtype=torch.int16, device=dev)
-    kv.kv_blocks_stash(pool, ids, store_host, block_ids_host=ctx)
+    kv.kv_blocks_stash(pool, ids, store_host, block_ids_host=ctx, ring=ring)
     kv.kv_blocks_stash(pool, ids, store_dev, block_ids_host=ctx)
     n, c = case.new_lens, case.reused_lens
     t = int(n.sum())
@@ -517,7 +517,7 @@ def pipeline_leg(torch, kv, W, args):
         return st.elapsed_time(en)
 
     def restore(store):
-        kv.kv_blocks_restore(pool, ids, store, block_ids_host=ctx)
+        kv.kv_blocks_restore(pool, ids, store, block_ids_host=ctx, ring=ring)
 
     def prefill_all():
         for l in range(NL):
@@ -536,7 +536,7 @@ def pipeline_leg(torch, kv, W, args):
 
         def restore_layer(l):
             with torch.cuda.stream(copy):
-                kv.kv_blocks_restore_layers(pool, l, 1, ids, store, block_ids_host=ctx)
+                kv.kv_blocks_restore_layers(pool, l, 1, ids, store, block_ids_host=ctx, ring=ring)
                 e = torch.cuda.Event()
                 e.record(copy)
                 events.append(e)

@@ -29,10 +29,11 @@
  *     ls_device_errors() returns.  A result computed with such an id is not
  *     meaningful.
  *   - Concurrency: calls on different streams may run concurrently only on
- *     disjoint sets of blocks; ordering between streams is the caller's
- *     (events).  Blocks being restored must not be read by attention until the
- *     restore's stream has been waited on — the same rule the paper's KV
- *     manager follows before reusing preloaded KV (§5.2).
+ *     disjoint sets of blocks and with their own scratch buffers (a decode
+ *     workspace, a copy's staging ring); ordering between streams is the
+ *     caller's (events).  Blocks being restored must not be read by attention
+ *     until the restore's stream has been waited on — the same rule the
+ *     paper's KV manager follows before reusing preloaded KV (§5.2).
  *   - Data types: K, V, Q and outputs are bfloat16 (bf16); arithmetic inside
  *     attention accumulates in fp32.
  *
@@ -71,7 +72,9 @@ typedef enum {
 
 /* Bits of the device error word (ls_device_errors). */
 #define LS_DEVERR_BLOCK_ID 0x1u     /* a block id outside [0, num_blocks) was skipped */
-#define LS_DEVERR_LENGTH   0x2u     /* a length exceeded its block table and was clipped */
+#define LS_DEVERR_LENGTH   0x2u     /* a length outside what the call can attend (an empty
+                                       decode context, a context past its block table, a
+                                       turn longer than max_new_len); see each call */
 #define LS_DEVERR_INTERNAL 0x4u     /* an internal bounded wait expired (a library bug) */
 
 typedef struct ls_kv_pool ls_kv_pool;
@@ -84,9 +87,6 @@ typedef struct {
     int64_t num_blocks;        /* blocks per layer */
     void *kv_base;             /* device, >= ls_kv_pool_bytes(...) bytes, 256-byte aligned */
     size_t kv_bytes;
-    void *staging_ring;        /* device ring used when stash/restore staging is host memory;
-                                  may be NULL (then only device staging is accepted) */
-    size_t staging_ring_bytes; /* a multiple of one block's all-layer slab is used */
 } ls_kv_pool_desc;
 
 /* Bytes of pool memory for the given geometry (0 on overflow or bad geometry). */
@@ -129,8 +129,17 @@ size_t ls_decode_workspace_bytes(const ls_kv_pool *pool, int32_t num_sessions,
  *                  already be in the table) by the same launch.
  *   block_tables   device int32 [num_sessions][max_blocks_per_session]
  *   context_lens   device int32 [num_sessions]: tokens already in the pool, >= 1
- *                  (>= 0 with append).  A length whose keys do not fit the table
- *                  is clipped to it and flagged (LS_DEVERR_LENGTH).
+ *                  (>= 0 with append).  An empty context (no key to attend) gives a
+ *                  zero output row and is flagged (LS_DEVERR_LENGTH); so is a length
+ *                  whose keys do not fit the table, which is clipped to it.
+ *   context_lens_host  optional host copy of context_lens (NULL: the kernel plans the
+ *                  split-K schedule from the device lengths).  When given it must hold
+ *                  the same values; the host then rejects empty or over-long contexts
+ *                  (LS_EINVAL) and plans the splits itself: sessions are split only as
+ *                  far as the batch needs to fill the GPU, and the split merge is
+ *                  launched only when some session was split.  A device length that
+ *                  differs from its host copy so that the plan no longer covers it is
+ *                  flagged (LS_DEVERR_LENGTH).
  *   scale          softmax scale applied to q.k (normally 1/sqrt(head_dim))
  *   out            device bf16 [num_sessions][num_q_heads][head_dim]:
  *                  out = softmax(scale * q K^T) V over the session's keys, per query
@@ -139,15 +148,15 @@ size_t ls_decode_workspace_bytes(const ls_kv_pool *pool, int32_t num_sessions,
  *
  * Supported: num_q_heads / num_kv_heads in {1, 2, 4, 8}.  Errors: LS_EINVAL
  * (NULL pointer, layer out of range, num_q_heads not a multiple of num_kv_heads,
- * only one of k_new / v_new), LS_ENOMEM (workspace too small), LS_EUNSUPPORTED
- * (group size), LS_EHIP (launch failure).
+ * only one of k_new / v_new, a bad host length), LS_ENOMEM (workspace too
+ * small), LS_EUNSUPPORTED (group size, batch limits), LS_EHIP (launch failure).
  */
 ls_status paged_attn_decode(ls_kv_pool *pool, int32_t layer, int32_t num_sessions,
                             int32_t num_q_heads, const void *q, const void *k_new,
                             const void *v_new, const int32_t *block_tables,
                             int32_t max_blocks_per_session, const int32_t *context_lens,
-                            float scale, void *out, void *workspace, size_t workspace_bytes,
-                            hipStream_t stream);
+                            const int32_t *context_lens_host, float scale, void *out,
+                            void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * paged_attn_prefill — next-turn (chunked) prefill over reused multi-turn
@@ -163,7 +172,13 @@ ls_status paged_attn_decode(ls_kv_pool *pool, int32_t layer, int32_t num_session
  *                  NULL when the turn's K/V is already in the pool
  *   cu_new_lens    device int32 [num_sessions + 1]: prefix sums of n_s (cu[0] = 0)
  *   reused_lens    device int32 [num_sessions]: c_s >= 0
- *   total_new_tokens, max_new_len   host ints: cu[S] and max_s n_s (grid sizing)
+ *   lens_host      optional host int32 [num_sessions][2] = (n_s, c_s), the same values
+ *                  as the device arrays (NULL: nothing is checked on the host).  When
+ *                  given, the host checks every turn against max_new_len, the table
+ *                  and total_new_tokens (LS_EINVAL) before anything is enqueued.
+ *   total_new_tokens, max_new_len   host ints: cu[S] and max_s n_s (grid sizing).
+ *                  A turn longer than max_new_len (device lengths only) is flagged
+ *                  (LS_DEVERR_LENGTH) and its rows past max_new_len are not written.
  *   block_tables   device int32 [num_sessions][max_blocks_per_session], covering
  *                  c_s + n_s tokens
  *   out            device bf16 [total_new_tokens][num_q_heads][head_dim]
@@ -174,29 +189,46 @@ ls_status paged_attn_decode(ls_kv_pool *pool, int32_t layer, int32_t num_session
 ls_status paged_attn_prefill(ls_kv_pool *pool, int32_t layer, int32_t num_sessions,
                              int32_t num_q_heads, const void *q, const void *k_new,
                              const void *v_new, const int32_t *cu_new_lens,
-                             const int32_t *reused_lens, int32_t total_new_tokens,
-                             int32_t max_new_len, const int32_t *block_tables,
-                             int32_t max_blocks_per_session, float scale, void *out,
-                             hipStream_t stream);
+                             const int32_t *reused_lens, const int32_t *lens_host,
+                             int32_t total_new_tokens, int32_t max_new_len,
+                             const int32_t *block_tables, int32_t max_blocks_per_session,
+                             float scale, void *out, hipStream_t stream);
+
+/*
+ * Arguments shared by the three block-copy calls below.
+ *
+ *   block_ids       device int32 [n]: distinct ids in [0, num_blocks)
+ *   block_ids_host  optional host copy of the same ids; when given, range and
+ *                   distinctness are checked on the host (LS_EINVAL)
+ *   staging         device memory, or pinned host memory when staging_on_host != 0,
+ *                   of staging_bytes >= n x (one block's all-layer slab) bytes
+ *                   (LS_ENOMEM otherwise), layout above
+ *   ring            with host staging: caller-owned device memory (16-byte aligned)
+ *                   that the copy moves through in whole-block chunks: a DMA and a
+ *                   copy kernel per chunk, on the caller's stream.  It must hold the
+ *                   copied layer range of at least one block (LS_ENOMEM otherwise).
+ *                   Two copies that may run at the same time (different streams)
+ *                   need different rings.  Ignored (may be NULL) with device staging.
+ *   max_workgroups  0: full rate (a persistent grid of four workgroups per CU the
+ *                   stream may use).  k > 0: at most k workgroups, which bounds the
+ *                   copy's share of the GPU — its HBM traffic and CU slots — when it
+ *                   runs beside live decode as background work (§5.2: preloads must
+ *                   not interfere with live requests); the copy is then slower.
+ * Bit-exact byte copies.  n == 0 is a no-op.
+ */
 
 /*
  * kv_blocks_stash — offload: copy every layer's K/V slab of blocks ids[0..n-1]
  * into staging (layout above), the HBM-to-DRAM eviction of idle multi-turn KV
  * (§5, §5.1; eviction stays block-level, suffix blocks first — the order is
  * the caller's).  The pool is left unchanged; freeing the ids is the caller's
- * decision once the stream has passed this call.
- *
- *   block_ids       device int32 [n]: distinct ids in [0, num_blocks)
- *   block_ids_host  optional host copy of the same ids; when given, range and
- *                   distinctness are checked on the host (LS_EINVAL)
- *   staging         device memory, or pinned host memory when staging_on_host != 0
- *                   (then the copy runs through the pool's staging_ring in whole-block
- *                   chunks: gather kernel, then a device-to-host DMA, per chunk)
- * Bit-exact byte copy.  n == 0 is a no-op.
+ * decision once the stream has passed this call.  With host staging each
+ * chunk is a gather kernel into the ring, then a device-to-host DMA.
  */
 ls_status kv_blocks_stash(ls_kv_pool *pool, int32_t n, const int32_t *block_ids,
-                          const int32_t *block_ids_host, void *staging,
-                          int32_t staging_on_host, hipStream_t stream);
+                          const int32_t *block_ids_host, void *staging, size_t staging_bytes,
+                          int32_t staging_on_host, void *ring, size_t ring_bytes,
+                          int32_t max_workgroups, hipStream_t stream);
 
 /*
  * kv_blocks_restore — reload / speech-triggered preload: copy staging (layout
@@ -204,14 +236,14 @@ ls_status kv_blocks_stash(ls_kv_pool *pool, int32_t n, const int32_t *block_ids,
  * asynchronous transfer path, §6).  Blocks are written in id order, so a
  * restore cut short by the caller (a cancelled preload) leaves a complete
  * prefix, and restoring the remaining ids afterwards (the synchronous
- * fallback of §5.2) gives the same pool as one full restore.
- * Arguments as for kv_blocks_stash; with staging_on_host != 0 each chunk is a
- * host-to-device DMA into the staging ring followed by the scatter kernel.
- * Bit-exact byte copy.  n == 0 is a no-op.
+ * fallback of §5.2) gives the same pool as one full restore.  With host
+ * staging each chunk is a host-to-device DMA into the ring, then the scatter
+ * kernel.
  */
 ls_status kv_blocks_restore(ls_kv_pool *pool, int32_t n, const int32_t *block_ids,
                             const int32_t *block_ids_host, const void *staging,
-                            int32_t staging_on_host, hipStream_t stream);
+                            size_t staging_bytes, int32_t staging_on_host, void *ring,
+                            size_t ring_bytes, int32_t max_workgroups, hipStream_t stream);
 
 /*
  * kv_blocks_restore_layers — kv_blocks_restore of the layers
@@ -228,7 +260,9 @@ ls_status kv_blocks_restore(ls_kv_pool *pool, int32_t n, const int32_t *block_id
  */
 ls_status kv_blocks_restore_layers(ls_kv_pool *pool, int32_t layer_begin, int32_t layer_count, int32_t n,
                                    const int32_t *block_ids, const int32_t *block_ids_host,
-                                   const void *staging, int32_t staging_on_host, hipStream_t stream);
+                                   const void *staging, size_t staging_bytes, int32_t staging_on_host,
+                                   void *ring, size_t ring_bytes, int32_t max_workgroups,
+                                   hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * KV manager (host only): the policy that decides which blocks the
@@ -417,10 +451,12 @@ ls_status ls_schedule_round(const ls_sched_stage *stage, int32_t n, const ls_sch
                             int32_t *order, int32_t *classes, double *utility, int32_t *num_admitted);
 
 /*
- * Wait for `stream`, then return (and clear) the device error word of the
- * current device in *bits (LS_DEVERR_* bits; 0 when no kernel met a bad index).
+ * Wait for all work on the current device (every stream), then return and
+ * clear its device error word in *bits: the LS_DEVERR_* bits raised by every
+ * call enqueued on the device before this one (0 when none met a bad index or
+ * length).  The word is shared by all pools on the device.
  */
-ls_status ls_device_errors(uint32_t *bits, hipStream_t stream);
+ls_status ls_device_errors(uint32_t *bits);
 
 /* Message of the calling thread's most recent non-OK status ("" if none). */
 const char *ls_last_error(void);

@@ -3,6 +3,7 @@
 // status means the stream is untouched.
 #include <cstdarg>
 #include <cstdio>
+#include <algorithm>
 #include <cstring>
 #include <mutex>
 #include <new>
@@ -17,23 +18,42 @@ struct ls_kv_pool {
 namespace ls {
 
 namespace {
-// One error word per device, in the library's own code object.
+// One error word per device, in the library's own code object, and the slot
+// that ls_device_errors exchanges it into.
 __device__ unsigned int g_device_errors = 0;
-}  // namespace
+__device__ unsigned int g_device_errors_taken = 0;
 
-unsigned int *device_error_word() {
+// Read and clear the error word in one atomic step, so that a bit raised by a
+// kernel running at the same time is either returned now or kept for the next
+// query, never lost.
+__global__ void take_errors_kernel(unsigned int *word, unsigned int *taken) {
+    *taken = atomicExch(word, 0u);
+}
+
+struct ErrorWords {
+    unsigned int *word = nullptr;
+    unsigned int *taken = nullptr;
+};
+
+ErrorWords error_words() {
     static std::mutex mu;
-    static unsigned int *addr[64] = {};
+    static ErrorWords addr[64];
     int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return {};
     std::lock_guard<std::mutex> lock(mu);
-    if (!addr[dev]) {
-        void *p = nullptr;
-        if (hipGetSymbolAddress(&p, HIP_SYMBOL(g_device_errors)) == hipSuccess)
-            addr[dev] = static_cast<unsigned int *>(p);
+    if (!addr[dev].word) {
+        void *w = nullptr, *t = nullptr;
+        if (hipGetSymbolAddress(&w, HIP_SYMBOL(g_device_errors)) == hipSuccess &&
+            hipGetSymbolAddress(&t, HIP_SYMBOL(g_device_errors_taken)) == hipSuccess) {
+            addr[dev].word = static_cast<unsigned int *>(w);
+            addr[dev].taken = static_cast<unsigned int *>(t);
+        }
     }
     return addr[dev];
 }
+}  // namespace
+
+unsigned int *device_error_word() { return error_words().word; }
 
 int stream_cus(const PoolGeom &p, hipStream_t stream) {
     const int dev_cus = p.num_cus > 0 ? p.num_cus : 256;
@@ -97,35 +117,45 @@ ls_status check_ids_host(const PoolGeom &p, int32_t n, const int32_t *ids) {
 }
 
 // Copy the slabs of layers [lb, lb + lc) of n blocks between the pool and a
-// block-major all-layer staging array (device, or pinned host through the ring).
+// block-major all-layer staging array (device, or pinned host through the
+// caller's ring).
 ls_status copy_blocks(ls_kv_pool *pool, int32_t lb, int32_t lc, int32_t n, const int32_t *block_ids,
-                      const int32_t *block_ids_host, void *staging, int32_t staging_on_host,
-                      bool to_pool, hipStream_t stream) {
+                      const int32_t *block_ids_host, void *staging, size_t staging_bytes,
+                      int32_t staging_on_host, void *ring_ptr, size_t ring_bytes,
+                      int32_t max_workgroups, bool to_pool, hipStream_t stream) {
     if (ls_status st = check_pool(pool)) return st;
     const PoolGeom &p = pool->geom;
     if (lb < 0 || lc < 1 || lb > p.num_layers - lc)
         return fail(LS_EINVAL, "layer range [%d, %d + %d) outside [0, %d)", lb, lb, lc, p.num_layers);
     if (n < 0) return fail(LS_EINVAL, "n must be >= 0");
+    if (max_workgroups < 0) return fail(LS_EINVAL, "max_workgroups must be >= 0");
     if (n == 0) return LS_OK;
     if (!block_ids || !staging) return fail(LS_EINVAL, "block_ids and staging must not be NULL");
     if (n > p.num_blocks) return fail(LS_EINVAL, "n (%d) exceeds num_blocks", n);
-    if (block_ids_host)
-        if (ls_status st = check_ids_host(p, n, block_ids_host)) return st;
     const size_t per_block = p.slab_bytes() * (size_t)p.num_layers;   // staging stride of a block
     const size_t range = p.slab_bytes() * (size_t)lc;                   // bytes of the layer range
-    if (staging_on_host && (!p.ring || p.ring_bytes < range))
-        return fail(LS_ENOMEM, "host staging needs a device staging ring of at least %zu bytes", range);
+    if (staging_bytes / per_block < (size_t)n)
+        return fail(LS_ENOMEM, "staging_bytes (%zu) < %d blocks x %zu bytes", staging_bytes, n, per_block);
+    uint8_t *ring = static_cast<uint8_t *>(ring_ptr);
+    if (staging_on_host) {
+        if (!ring || ring_bytes < range)
+            return fail(LS_ENOMEM, "host staging needs a device ring of at least %zu bytes", range);
+        if (reinterpret_cast<uintptr_t>(ring) % 16 != 0)
+            return fail(LS_EINVAL, "the ring must be 16-byte aligned");
+    }
+    if (block_ids_host)
+        if (ls_status st = check_ids_host(p, n, block_ids_host)) return st;
     unsigned int *err = device_error_word();
     if (!err) return fail(LS_EHIP, "cannot resolve the device error word");
     if (!staging_on_host) {
         hipError_t e = launch_block_copy(p, n, block_ids, static_cast<uint8_t *>(staging), lb, lc,
-                                         p.num_layers, lb, to_pool, err, stream);
+                                         p.num_layers, lb, to_pool, max_workgroups, err, stream);
         return e == hipSuccess ? LS_OK : hip_fail(e, "block copy launch");
     }
     // Whole blocks per chunk, in id order, all on the caller's stream.  The
     // ring holds the layer range of each block compactly; a range narrower
     // than all layers moves as a strided (2D) copy of one row per block.
-    const int32_t chunk = (int32_t)(p.ring_bytes / range);
+    const int32_t chunk = (int32_t)std::min<size_t>(ring_bytes / range, (size_t)n);
     uint8_t *host = static_cast<uint8_t *>(staging) + p.slab_bytes() * (size_t)lb;
     for (int32_t i0 = 0; i0 < n; i0 += chunk) {
         const int32_t cnt = (n - i0) < chunk ? (n - i0) : chunk;
@@ -133,20 +163,58 @@ ls_status copy_blocks(ls_kv_pool *pool, int32_t lb, int32_t lc, int32_t n, const
         hipError_t e;
         if (to_pool) {
             e = range == per_block
-                    ? hipMemcpyAsync(p.ring, h, range * (size_t)cnt, hipMemcpyHostToDevice, stream)
-                    : hipMemcpy2DAsync(p.ring, range, h, per_block, range, cnt, hipMemcpyHostToDevice, stream);
+                    ? hipMemcpyAsync(ring, h, range * (size_t)cnt, hipMemcpyHostToDevice, stream)
+                    : hipMemcpy2DAsync(ring, range, h, per_block, range, cnt, hipMemcpyHostToDevice, stream);
             if (e != hipSuccess) return hip_fail(e, "restore host-to-device copy");
-            e = launch_block_copy(p, cnt, block_ids + i0, p.ring, lb, lc, lc, 0, true, err, stream);
+            e = launch_block_copy(p, cnt, block_ids + i0, ring, lb, lc, lc, 0, true, max_workgroups, err,
+                                  stream);
             if (e != hipSuccess) return hip_fail(e, "restore scatter launch");
         } else {
-            e = launch_block_copy(p, cnt, block_ids + i0, p.ring, lb, lc, lc, 0, false, err, stream);
+            e = launch_block_copy(p, cnt, block_ids + i0, ring, lb, lc, lc, 0, false, max_workgroups, err,
+                                  stream);
             if (e != hipSuccess) return hip_fail(e, "stash gather launch");
             e = range == per_block
-                    ? hipMemcpyAsync(h, p.ring, range * (size_t)cnt, hipMemcpyDeviceToHost, stream)
-                    : hipMemcpy2DAsync(h, per_block, p.ring, range, range, cnt, hipMemcpyDeviceToHost, stream);
+                    ? hipMemcpyAsync(h, ring, range * (size_t)cnt, hipMemcpyDeviceToHost, stream)
+                    : hipMemcpy2DAsync(h, per_block, ring, range, range, cnt, hipMemcpyDeviceToHost, stream);
             if (e != hipSuccess) return hip_fail(e, "stash device-to-host copy");
         }
     }
+    return LS_OK;
+}
+
+// Host check of decode lengths: every session attends to at least one key,
+// and its keys (the appended one included) fit its block table.
+ls_status check_decode_lens_host(int32_t S, const int32_t *lens, int32_t appended, int32_t max_blocks) {
+    const int64_t cap = (int64_t)max_blocks * kBlock;
+    for (int32_t s = 0; s < S; ++s) {
+        const int64_t L = (int64_t)lens[s] + appended;
+        if (lens[s] < 0 || L < 1)
+            return fail(LS_EINVAL, "session %d: context length %d leaves no key to attend", s, lens[s]);
+        if (L > cap)
+            return fail(LS_EINVAL, "session %d: %lld keys do not fit its %d-block table", s, (long long)L,
+                        max_blocks);
+    }
+    return LS_OK;
+}
+
+// Host check of prefill lengths (n_s, c_s): turns within max_new_len and the
+// table, adding up to total_new_tokens.
+ls_status check_prefill_lens_host(int32_t S, const int32_t *lens, int32_t total, int32_t max_new_len,
+                                  int32_t max_blocks) {
+    const int64_t cap = (int64_t)max_blocks * kBlock;
+    int64_t sum = 0;
+    for (int32_t s = 0; s < S; ++s) {
+        const int32_t n = lens[2 * s], c = lens[2 * s + 1];
+        if (n < 0 || c < 0) return fail(LS_EINVAL, "session %d: negative length (n %d, c %d)", s, n, c);
+        if (n > max_new_len)
+            return fail(LS_EINVAL, "session %d: turn of %d tokens exceeds max_new_len (%d)", s, n, max_new_len);
+        if ((int64_t)n + c > cap)
+            return fail(LS_EINVAL, "session %d: %lld keys do not fit its %d-block table", s,
+                        (long long)n + c, max_blocks);
+        sum += n;
+    }
+    if (sum != total)
+        return fail(LS_EINVAL, "turn lengths add up to %lld, not total_new_tokens (%d)", (long long)sum, total);
     return LS_OK;
 }
 
@@ -197,8 +265,6 @@ ls_status kv_pool_create(const ls_kv_pool_desc *desc, ls_kv_pool **out) {
     if (desc->kv_bytes < need)
         return fail(LS_ENOMEM, "kv_bytes (%zu) is smaller than the layout needs (%zu)",
                     desc->kv_bytes, need);
-    if (desc->staging_ring && reinterpret_cast<uintptr_t>(desc->staging_ring) % 16 != 0)
-        return fail(LS_EINVAL, "staging_ring must be 16-byte aligned");
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess) dev = -1;
     if (dev >= 0 && hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
@@ -210,8 +276,6 @@ ls_status kv_pool_create(const ls_kv_pool_desc *desc, ls_kv_pool **out) {
     pool->geom.head_dim = desc->head_dim;
     pool->geom.num_blocks = desc->num_blocks;
     pool->geom.base = static_cast<uint16_t *>(desc->kv_base);
-    pool->geom.ring = static_cast<uint8_t *>(desc->staging_ring);
-    pool->geom.ring_bytes = desc->staging_ring ? desc->staging_ring_bytes : 0;
     pool->geom.device = dev;
     pool->geom.num_cus = cus;
     *out = pool;
@@ -233,8 +297,8 @@ ls_status paged_attn_decode(ls_kv_pool *pool, int32_t layer, int32_t num_session
                             int32_t num_q_heads, const void *q, const void *k_new,
                             const void *v_new, const int32_t *block_tables,
                             int32_t max_blocks_per_session, const int32_t *context_lens,
-                            float scale, void *out, void *workspace, size_t workspace_bytes,
-                            hipStream_t stream) {
+                            const int32_t *context_lens_host, float scale, void *out,
+                            void *workspace, size_t workspace_bytes, hipStream_t stream) {
     if (ls_status st = check_pool(pool)) return st;
     const PoolGeom &p = pool->geom;
     if (layer < 0 || layer >= p.num_layers)
@@ -248,6 +312,10 @@ ls_status paged_attn_decode(ls_kv_pool *pool, int32_t layer, int32_t num_session
         return fail(LS_EINVAL, "k_new and v_new must both be given or both be NULL");
     if (max_blocks_per_session <= 0) return fail(LS_EINVAL, "max_blocks_per_session must be > 0");
     if (!(scale > 0.f) || scale != scale) return fail(LS_EINVAL, "scale must be a positive number");
+    if (context_lens_host)
+        if (ls_status st = check_decode_lens_host(num_sessions, context_lens_host, k_new ? 1 : 0,
+                                                  max_blocks_per_session))
+            return st;
     const DecodePlan plan = plan_decode(p, num_sessions, num_q_heads, max_blocks_per_session);
     if (!plan.supported)
         return fail(LS_EUNSUPPORTED, "batch of %d sessions with %d blocks each exceeds the decode "
@@ -267,10 +335,10 @@ ls_status paged_attn_decode(ls_kv_pool *pool, int32_t layer, int32_t num_session
 ls_status paged_attn_prefill(ls_kv_pool *pool, int32_t layer, int32_t num_sessions,
                              int32_t num_q_heads, const void *q, const void *k_new,
                              const void *v_new, const int32_t *cu_new_lens,
-                             const int32_t *reused_lens, int32_t total_new_tokens,
-                             int32_t max_new_len, const int32_t *block_tables,
-                             int32_t max_blocks_per_session, float scale, void *out,
-                             hipStream_t stream) {
+                             const int32_t *reused_lens, const int32_t *lens_host,
+                             int32_t total_new_tokens, int32_t max_new_len,
+                             const int32_t *block_tables, int32_t max_blocks_per_session,
+                             float scale, void *out, hipStream_t stream) {
     if (ls_status st = check_pool(pool)) return st;
     const PoolGeom &p = pool->geom;
     if (layer < 0 || layer >= p.num_layers)
@@ -288,6 +356,10 @@ ls_status paged_attn_prefill(ls_kv_pool *pool, int32_t layer, int32_t num_sessio
         return fail(LS_EINVAL, "max_new_len (%d) exceeds total_new_tokens (%d)", max_new_len,
                     total_new_tokens);
     if (!(scale > 0.f) || scale != scale) return fail(LS_EINVAL, "scale must be a positive number");
+    if (lens_host)
+        if (ls_status st = check_prefill_lens_host(num_sessions, lens_host, total_new_tokens, max_new_len,
+                                                   max_blocks_per_session))
+            return st;
     unsigned int *err = device_error_word();
     if (!err) return fail(LS_EHIP, "cannot resolve the device error word");
     if (k_new) {
@@ -305,37 +377,44 @@ ls_status paged_attn_prefill(ls_kv_pool *pool, int32_t layer, int32_t num_sessio
 }
 
 ls_status kv_blocks_stash(ls_kv_pool *pool, int32_t n, const int32_t *block_ids,
-                          const int32_t *block_ids_host, void *staging, int32_t staging_on_host,
-                          hipStream_t stream) {
+                          const int32_t *block_ids_host, void *staging, size_t staging_bytes,
+                          int32_t staging_on_host, void *ring, size_t ring_bytes,
+                          int32_t max_workgroups, hipStream_t stream) {
     return copy_blocks(pool, 0, pool ? pool->geom.num_layers : 1, n, block_ids, block_ids_host, staging,
-                       staging_on_host, false, stream);
+                       staging_bytes, staging_on_host, ring, ring_bytes, max_workgroups, false, stream);
 }
 
 ls_status kv_blocks_restore(ls_kv_pool *pool, int32_t n, const int32_t *block_ids,
                             const int32_t *block_ids_host, const void *staging,
-                            int32_t staging_on_host, hipStream_t stream) {
+                            size_t staging_bytes, int32_t staging_on_host, void *ring,
+                            size_t ring_bytes, int32_t max_workgroups, hipStream_t stream) {
     return copy_blocks(pool, 0, pool ? pool->geom.num_layers : 1, n, block_ids, block_ids_host,
-                       const_cast<void *>(staging), staging_on_host, true, stream);
+                       const_cast<void *>(staging), staging_bytes, staging_on_host, ring, ring_bytes,
+                       max_workgroups, true, stream);
 }
 
 ls_status kv_blocks_restore_layers(ls_kv_pool *pool, int32_t layer_begin, int32_t layer_count, int32_t n,
                                    const int32_t *block_ids, const int32_t *block_ids_host,
-                                   const void *staging, int32_t staging_on_host, hipStream_t stream) {
+                                   const void *staging, size_t staging_bytes, int32_t staging_on_host,
+                                   void *ring, size_t ring_bytes, int32_t max_workgroups,
+                                   hipStream_t stream) {
     return copy_blocks(pool, layer_begin, layer_count, n, block_ids, block_ids_host,
-                       const_cast<void *>(staging), staging_on_host, true, stream);
+                       const_cast<void *>(staging), staging_bytes, staging_on_host, ring, ring_bytes,
+                       max_workgroups, true, stream);
 }
 
-ls_status ls_device_errors(uint32_t *bits, hipStream_t stream) {
+ls_status ls_device_errors(uint32_t *bits) {
     if (!bits) return fail(LS_EINVAL, "bits must not be NULL");
-    hipError_t e = hipStreamSynchronize(stream);
-    if (e != hipSuccess) return hip_fail(e, "stream synchronize");
-    unsigned int *word = device_error_word();
-    if (!word) return fail(LS_EHIP, "cannot resolve the device error word");
-    unsigned int v = 0, zero = 0;
-    e = hipMemcpy(&v, word, sizeof v, hipMemcpyDeviceToHost);
+    const ErrorWords w = error_words();
+    if (!w.word) return fail(LS_EHIP, "cannot resolve the device error word");
+    hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) return hip_fail(e, "device synchronize");
+    hipLaunchKernelGGL(take_errors_kernel, dim3(1), dim3(1), 0, nullptr, w.word, w.taken);
+    e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "error word exchange launch");
+    unsigned int v = 0;
+    e = hipMemcpy(&v, w.taken, sizeof v, hipMemcpyDeviceToHost);
     if (e != hipSuccess) return hip_fail(e, "read device error word");
-    e = hipMemcpy(word, &zero, sizeof zero, hipMemcpyHostToDevice);
-    if (e != hipSuccess) return hip_fail(e, "clear device error word");
     *bits = v;
     return LS_OK;
 }

@@ -67,10 +67,12 @@ __global__ __launch_bounds__(kCopyThreads) void block_copy_kernel(
 
 hipError_t launch_block_copy(const PoolGeom &p, int32_t n, const int32_t *ids, uint8_t *staging,
                              int32_t layer_begin, int32_t layer_count, int32_t stage_block_slabs,
-                             int32_t stage_layer0, bool to_pool, unsigned int *err, hipStream_t stream) {
+                             int32_t stage_layer0, bool to_pool, int32_t max_workgroups,
+                             unsigned int *err, hipStream_t stream) {
     if (n <= 0 || layer_count <= 0) return hipSuccess;
     const int64_t units = (int64_t)n * layer_count;
-    const int64_t grid = std::min<int64_t>(units, (int64_t)kCopyWorkgroupsPerCu * stream_cus(p, stream));
+    int64_t grid = std::min<int64_t>(units, (int64_t)kCopyWorkgroupsPerCu * stream_cus(p, stream));
+    if (max_workgroups > 0) grid = std::min<int64_t>(grid, max_workgroups);
     hipLaunchKernelGGL(block_copy_kernel, dim3((unsigned)grid), dim3(kCopyThreads), 0, stream,
                        reinterpret_cast<uint8_t *>(p.base), ids, staging, p.num_blocks, layer_begin,
                        layer_count, stage_block_slabs, stage_layer0, (int64_t)p.slab_bytes(), units,

@@ -20,8 +20,6 @@ struct PoolGeom {
     int32_t head_dim;
     int64_t num_blocks;
     uint16_t *base;                 // bf16 bit patterns
-    uint8_t *ring;                  // device staging ring (may be null)
-    size_t ring_bytes;
     int device;
     int num_cus;                    // compute units of that device (0 if unknown)
 
@@ -61,9 +59,11 @@ DecodePlan plan_decode(const PoolGeom &p, int32_t num_sessions, int32_t num_q_he
 // Copies the slabs of layers [layer_begin, layer_begin + layer_count) of blocks
 // ids[0..n): staging block i holds stage_block_slabs slabs, layer_begin's is
 // its stage_layer0-th.
+// max_workgroups > 0 caps the persistent grid (a bounded-interference copy).
 hipError_t launch_block_copy(const PoolGeom &p, int32_t n, const int32_t *ids, uint8_t *staging,
                              int32_t layer_begin, int32_t layer_count, int32_t stage_block_slabs,
-                             int32_t stage_layer0, bool to_pool, unsigned int *err, hipStream_t stream);
+                             int32_t stage_layer0, bool to_pool, int32_t max_workgroups,
+                             unsigned int *err, hipStream_t stream);
 hipError_t launch_append_prefill(const PoolGeom &p, int layer, int32_t num_sessions,
                                  int32_t total_tokens, const uint16_t *k_new,
                                  const uint16_t *v_new, const int32_t *cu_new_lens,

@@ -112,13 +112,14 @@ __device__ __forceinline__ float wave_sum_xor_16_32(float x) {
     return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
-// Tokens of session s that attention covers (clipped to the table, flagged).
-// Kept branch-free so that the compiler sees a wave-uniform value.
+// Tokens of session s that attention covers, clipped to [0, table]; an empty
+// context (softmax over no key) and an over-long one are flagged.  Kept
+// branch-free so that the compiler sees a wave-uniform value.
 __device__ __forceinline__ int attended_len(const DecodeArgs &a, int s, bool may_flag) {
     const int raw = a.lens[s] + a.appended;
     const int cap = a.max_blocks * kBlock;
-    if (may_flag && raw > cap) flag_error(a.err, LS_DEVERR_LENGTH);
-    return min(raw, cap);
+    if (may_flag && (raw > cap || raw <= 0)) flag_error(a.err, LS_DEVERR_LENGTH);
+    return max(min(raw, cap), 0);
 }
 
 // Issue the loads of one block (blk < 0: a zero-size descriptor, nothing fetched).
@@ -544,7 +545,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
             // Last wave in: merge the item (4 consecutive outputs per lane per step).
             const int64_t part = ((int64_t)cur_s * a.num_kv_heads + g) * a.max_splits + cur_split;
             for (int base = lane * 4; base < G * D && L <= 0; base += kWave * 4)
-                // Softmax over no key is undefined: the output is zero (length flagged).
+                // Softmax over no key is undefined: the output is zero (flagged in attended_len).
                 *reinterpret_cast<uint2 *>(a.out + ((int64_t)cur_s * hq_total + g * G) * D + base) =
                     make_uint2(0u, 0u);
             for (int base = lane * 4; base < G * D && L > 0; base += kWave * 4) {

@@ -223,12 +223,20 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     // first.  Workgroup i is dispatched to XCD i % 8 and is the (i / 8)-th
     // item there; every workgroup derives the same schedule from the lengths.
     const int P = S * Hkv;
+    // A turn longer than the grid's query tiles (max_new_len understated), a
+    // negative turn or a negative context cannot be attended as given: flagged
+    // once, by the first workgroup (its rows past the tiles are not written).
+    if (blockIdx.x == 0)
+        for (int sp = tid; sp < S; sp += kPreThreads) {
+            const int nt = a.cu[sp + 1] - a.cu[sp];
+            if (nt < 0 || nt > QT * qtok || a.ctx[sp] < 0) flag_error(a.err, LS_DEVERR_LENGTH);
+        }
     int s, g, qt;
     if (P <= kMaxPairs) {
         for (int p = tid; p < P; p += kPreThreads) {
             const int sp = p / Hkv;
             const int nt = max(a.cu[sp + 1] - a.cu[sp], 0);
-            const int items = (nt + qtok - 1) / qtok;
+            const int items = min((nt + qtok - 1) / qtok, QT);
             sm_items[p] = items;
             sm_work[p] = (int64_t)items * (2 * (int64_t)max(a.ctx[sp], 0) + nt);
         }

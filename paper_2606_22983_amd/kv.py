@@ -30,8 +30,7 @@ class _PoolDesc(ctypes.Structure):
     _fields_ = [("num_layers", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("block_size", ctypes.c_int32),
                 ("num_blocks", ctypes.c_int64), ("kv_base", ctypes.c_void_p),
-                ("kv_bytes", ctypes.c_size_t), ("staging_ring", ctypes.c_void_p),
-                ("staging_ring_bytes", ctypes.c_size_t)]
+                ("kv_bytes", ctypes.c_size_t)]
 
 
 _lib.ls_kv_pool_bytes.argtypes = [_i32, _i64, _i32, _i32, _i32]
@@ -40,14 +39,15 @@ _lib.kv_pool_create.argtypes = [ctypes.POINTER(_PoolDesc), ctypes.POINTER(_p)]
 _lib.kv_pool_destroy.argtypes = [_p]
 _lib.ls_decode_workspace_bytes.argtypes = [_p, _i32, _i32, _i32]
 _lib.ls_decode_workspace_bytes.restype = _sz
-_lib.paged_attn_decode.argtypes = [_p, _i32, _i32, _i32, _p, _p, _p, _p, _i32, _p, _f32, _p, _p,
-                                   _sz, _p]
-_lib.paged_attn_prefill.argtypes = [_p, _i32, _i32, _i32, _p, _p, _p, _p, _p, _i32, _i32, _p,
+_lib.paged_attn_decode.argtypes = [_p, _i32, _i32, _i32, _p, _p, _p, _p, _i32, _p, _p, _f32, _p,
+                                   _p, _sz, _p]
+_lib.paged_attn_prefill.argtypes = [_p, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _i32, _i32, _p,
                                     _i32, _f32, _p, _p]
-_lib.kv_blocks_stash.argtypes = [_p, _i32, _p, _p, _p, _i32, _p]
-_lib.kv_blocks_restore.argtypes = [_p, _i32, _p, _p, _p, _i32, _p]
-_lib.kv_blocks_restore_layers.argtypes = [_p, _i32, _i32, _i32, _p, _p, _p, _i32, _p]
-_lib.ls_device_errors.argtypes = [ctypes.POINTER(ctypes.c_uint32), _p]
+_lib.kv_blocks_stash.argtypes = [_p, _i32, _p, _p, _p, _sz, _i32, _p, _sz, _i32, _p]
+_lib.kv_blocks_restore.argtypes = [_p, _i32, _p, _p, _p, _sz, _i32, _p, _sz, _i32, _p]
+_lib.kv_blocks_restore_layers.argtypes = [_p, _i32, _i32, _i32, _p, _p, _p, _sz, _i32, _p, _sz,
+                                          _i32, _p]
+_lib.ls_device_errors.argtypes = [ctypes.POINTER(ctypes.c_uint32)]
 _lib.ls_last_error.restype = ctypes.c_char_p
 _lib.ls_version.restype = ctypes.c_char_p
 for _f in (_lib.kv_pool_create, _lib.kv_pool_destroy, _lib.paged_attn_decode,
@@ -76,14 +76,28 @@ def _ptr(t: Optional[torch.Tensor]):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
+def _shape(t: torch.Tensor, name: str, shape, dtype=None):
+    """Check shape (None = any extent) and dtype; no device access."""
+    if dtype is not None and t.dtype not in (dtype if isinstance(dtype, tuple) else (dtype,)):
+        raise ValueError("%s must have dtype %s (got %s)" % (name, dtype, t.dtype))
+    if len(t.shape) != len(shape) or any(e is not None and e != a for e, a in zip(shape, t.shape)):
+        want = "[" + "][".join("*" if e is None else str(e) for e in shape) + "]"
+        raise ValueError("%s must have shape %s (got %s)" % (name, want, list(t.shape)))
+    return t
+
+
 def _dev(t: torch.Tensor, name: str, dtype=None):
+    if dtype is not None and t.dtype not in (dtype if isinstance(dtype, tuple) else (dtype,)):
+        raise ValueError("%s must have dtype %s (got %s)" % (name, dtype, t.dtype))
     if not t.is_cuda:
         raise ValueError("%s must be a device tensor" % name)
     if not t.is_contiguous():
         raise ValueError("%s must be contiguous" % name)
-    if dtype is not None and t.dtype not in (dtype if isinstance(dtype, tuple) else (dtype,)):
-        raise ValueError("%s must have dtype %s (got %s)" % (name, dtype, t.dtype))
     return t
+
+
+def _nbytes(t: torch.Tensor) -> int:
+    return t.numel() * t.element_size()
 
 
 def _stream(stream) -> ctypes.c_void_p:
@@ -104,13 +118,11 @@ def ls_kv_pool_bytes(num_layers, num_blocks, num_kv_heads, head_dim, block_size=
 
 
 class KVPool:
-    """Handle of a pool created by :func:`kv_pool_create` (keeps its tensors alive)."""
+    """Handle of a pool created by :func:`kv_pool_create` (keeps its tensor alive)."""
 
-    def __init__(self, handle, kv, ring, num_layers, num_blocks, num_kv_heads, head_dim,
-                 block_size):
+    def __init__(self, handle, kv, num_layers, num_blocks, num_kv_heads, head_dim, block_size):
         self.handle = handle
         self.kv = kv
-        self.ring = ring
         self.num_layers = num_layers
         self.num_blocks = num_blocks
         self.num_kv_heads = num_kv_heads
@@ -119,7 +131,13 @@ class KVPool:
 
     @property
     def slab_bytes(self) -> int:
+        """Bytes of one (layer, block) slab: K and V tiles of every KV head."""
         return 2 * self.num_kv_heads * self.block_size * self.head_dim * 2
+
+    @property
+    def block_bytes(self) -> int:
+        """Bytes of one block's all-layer staging record."""
+        return self.num_layers * self.slab_bytes
 
     def close(self):
         if self.handle:
@@ -134,20 +152,14 @@ class KVPool:
 
 
 def kv_pool_create(kv: torch.Tensor, num_layers: int, num_blocks: int, num_kv_heads: int,
-                   head_dim: int, block_size: int = 16,
-                   staging_ring: Optional[torch.Tensor] = None) -> KVPool:
+                   head_dim: int, block_size: int = 16) -> KVPool:
     """Wrap ``kv`` (device memory of at least ``ls_kv_pool_bytes`` bytes) as a pool."""
     _dev(kv, "kv")
-    if staging_ring is not None:
-        _dev(staging_ring, "staging_ring")
     desc = _PoolDesc(num_layers, num_kv_heads, head_dim, block_size, num_blocks,
-                     kv.data_ptr(), kv.numel() * kv.element_size(),
-                     None if staging_ring is None else staging_ring.data_ptr(),
-                     0 if staging_ring is None else staging_ring.numel() * staging_ring.element_size())
+                     kv.data_ptr(), _nbytes(kv))
     handle = ctypes.c_void_p()
     _check(_lib.kv_pool_create(ctypes.byref(desc), ctypes.byref(handle)), "kv_pool_create")
-    return KVPool(handle, kv, staging_ring, num_layers, num_blocks, num_kv_heads, head_dim,
-                  block_size)
+    return KVPool(handle, kv, num_layers, num_blocks, num_kv_heads, head_dim, block_size)
 
 
 def decode_workspace_bytes(pool: KVPool, num_sessions: int, num_q_heads: int,
@@ -156,49 +168,81 @@ def decode_workspace_bytes(pool: KVPool, num_sessions: int, num_q_heads: int,
                                               max_blocks_per_session))
 
 
+def _host_i32(a, name: str, n: int):
+    """Host int32 copy (kept alive by the caller) of an optional length array."""
+    if a is None:
+        return None, None
+    arr = np.ascontiguousarray(np.asarray(a).reshape(-1), dtype=np.int32)
+    if arr.size != n:
+        raise ValueError("%s must hold %d values (got %d)" % (name, n, arr.size))
+    return arr, ctypes.c_void_p(arr.ctypes.data)
+
+
 def paged_attn_decode(pool: KVPool, layer: int, q: torch.Tensor, block_tables: torch.Tensor,
                       context_lens: torch.Tensor, scale: float, out: torch.Tensor,
                       workspace: torch.Tensor, k_new: Optional[torch.Tensor] = None,
-                      v_new: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    """q/out: [S][Hq][D] bf16; block_tables int32 [S][maxb]; context_lens int32 [S]."""
-    _dev(q, "q", _BF16)
-    _dev(out, "out", _BF16)
-    _dev(block_tables, "block_tables", torch.int32)
-    _dev(context_lens, "context_lens", torch.int32)
-    _dev(workspace, "workspace")
-    if k_new is not None:
-        _dev(k_new, "k_new", _BF16)
-    if v_new is not None:
-        _dev(v_new, "v_new", _BF16)
+                      v_new: Optional[torch.Tensor] = None, context_lens_host=None,
+                      stream=None) -> torch.Tensor:
+    """q/out: [S][Hq][D] bf16; block_tables int32 [S][maxb]; context_lens int32 [S];
+    k_new/v_new [S][Hkv][D] bf16; context_lens_host: optional host copy of context_lens."""
+    if q.dim() != 3:
+        raise ValueError("q must be [S][Hq][D]")
     s, hq = q.shape[0], q.shape[1]
+    d, hkv = pool.head_dim, pool.num_kv_heads
+    _shape(q, "q", (s, hq, d), _BF16)
+    _shape(out, "out", (s, hq, d), _BF16)
+    _shape(block_tables, "block_tables", (s, None), torch.int32)
+    _shape(context_lens, "context_lens", (s,), torch.int32)
+    for t, name in ((k_new, "k_new"), (v_new, "v_new")):
+        if t is not None:
+            _shape(t, name, (s, hkv, d), _BF16)
+    for t, name in ((q, "q"), (out, "out"), (block_tables, "block_tables"),
+                    (context_lens, "context_lens"), (workspace, "workspace"), (k_new, "k_new"),
+                    (v_new, "v_new")):
+        if t is not None:
+            _dev(t, name)
+    keep, hl = _host_i32(context_lens_host, "context_lens_host", s)
     _check(_lib.paged_attn_decode(pool.handle, layer, s, hq, _ptr(q), _ptr(k_new), _ptr(v_new),
-                                  _ptr(block_tables), block_tables.shape[1], _ptr(context_lens),
-                                  float(scale), _ptr(out), _ptr(workspace),
-                                  workspace.numel() * workspace.element_size(), _stream(stream)),
+                                  _ptr(block_tables), block_tables.shape[1], _ptr(context_lens), hl,
+                                  float(scale), _ptr(out), _ptr(workspace), _nbytes(workspace),
+                                  _stream(stream)),
            "paged_attn_decode")
+    del keep
     return out
 
 
 def paged_attn_prefill(pool: KVPool, layer: int, q: torch.Tensor, cu_new_lens: torch.Tensor,
                        reused_lens: torch.Tensor, max_new_len: int, block_tables: torch.Tensor,
                        scale: float, out: torch.Tensor, k_new: Optional[torch.Tensor] = None,
-                       v_new: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    """q/out: [T][Hq][D] bf16; cu_new_lens int32 [S+1]; reused_lens int32 [S]."""
-    _dev(q, "q", _BF16)
-    _dev(out, "out", _BF16)
-    _dev(cu_new_lens, "cu_new_lens", torch.int32)
-    _dev(reused_lens, "reused_lens", torch.int32)
-    _dev(block_tables, "block_tables", torch.int32)
-    if k_new is not None:
-        _dev(k_new, "k_new", _BF16)
-    if v_new is not None:
-        _dev(v_new, "v_new", _BF16)
-    s = reused_lens.shape[0]
-    _check(_lib.paged_attn_prefill(pool.handle, layer, s, q.shape[1], _ptr(q), _ptr(k_new),
-                                   _ptr(v_new), _ptr(cu_new_lens), _ptr(reused_lens), q.shape[0],
+                       v_new: Optional[torch.Tensor] = None, lens_host=None,
+                       stream=None) -> torch.Tensor:
+    """q/out: [T][Hq][D] bf16; cu_new_lens int32 [S+1]; reused_lens int32 [S];
+    k_new/v_new [T][Hkv][D] bf16; lens_host: optional host [S][2] of (n_s, c_s)."""
+    if q.dim() != 3:
+        raise ValueError("q must be [T][Hq][D]")
+    total, hq = q.shape[0], q.shape[1]
+    s = reused_lens.shape[0] if reused_lens.dim() == 1 else -1
+    d, hkv = pool.head_dim, pool.num_kv_heads
+    _shape(q, "q", (total, hq, d), _BF16)
+    _shape(out, "out", (total, hq, d), _BF16)
+    _shape(reused_lens, "reused_lens", (None,), torch.int32)
+    _shape(cu_new_lens, "cu_new_lens", (s + 1,), torch.int32)
+    _shape(block_tables, "block_tables", (s, None), torch.int32)
+    for t, name in ((k_new, "k_new"), (v_new, "v_new")):
+        if t is not None:
+            _shape(t, name, (total, hkv, d), _BF16)
+    for t, name in ((q, "q"), (out, "out"), (cu_new_lens, "cu_new_lens"),
+                    (reused_lens, "reused_lens"), (block_tables, "block_tables"), (k_new, "k_new"),
+                    (v_new, "v_new")):
+        if t is not None:
+            _dev(t, name)
+    keep, hl = _host_i32(lens_host, "lens_host", 2 * s)
+    _check(_lib.paged_attn_prefill(pool.handle, layer, s, hq, _ptr(q), _ptr(k_new), _ptr(v_new),
+                                   _ptr(cu_new_lens), _ptr(reused_lens), hl, total,
                                    int(max_new_len), _ptr(block_tables), block_tables.shape[1],
                                    float(scale), _ptr(out), _stream(stream)),
            "paged_attn_prefill")
+    del keep
     return out
 
 
@@ -210,54 +254,73 @@ def _host_ids(ids):
     return arr, ctypes.c_void_p(arr.ctypes.data)
 
 
-def kv_blocks_stash(pool: KVPool, block_ids: torch.Tensor, staging: torch.Tensor,
-                    block_ids_host=None, stream=None) -> torch.Tensor:
-    """Copy every layer's slab of ``block_ids`` into ``staging`` (device or pinned host)."""
-    _dev(block_ids, "block_ids", torch.int32)
+def _copy_args(pool: KVPool, block_ids: torch.Tensor, staging: torch.Tensor, ring, max_workgroups):
+    """Checks shared by the block copies; returns (on_host, ring pointer, ring bytes)."""
+    _shape(block_ids, "block_ids", (None,), torch.int32)
+    if not staging.is_contiguous():
+        raise ValueError("staging must be contiguous")
+    if _nbytes(staging) < block_ids.numel() * pool.block_bytes:
+        raise ValueError("staging holds %d bytes; %d blocks need %d" % (
+            _nbytes(staging), block_ids.numel(), block_ids.numel() * pool.block_bytes))
+    if max_workgroups < 0:
+        raise ValueError("max_workgroups must be >= 0")
+    _dev(block_ids, "block_ids")
     on_host = not staging.is_cuda
     if on_host and not staging.is_pinned():
         raise ValueError("host staging must be pinned memory")
+    if ring is not None:
+        _dev(ring, "ring")
+    return on_host, _ptr(ring), 0 if ring is None else _nbytes(ring)
+
+
+def kv_blocks_stash(pool: KVPool, block_ids: torch.Tensor, staging: torch.Tensor,
+                    block_ids_host=None, ring: Optional[torch.Tensor] = None,
+                    max_workgroups: int = 0, stream=None) -> torch.Tensor:
+    """Copy every layer's slab of ``block_ids`` into ``staging`` (device, or pinned host
+    through the device ``ring``)."""
+    on_host, rp, rb = _copy_args(pool, block_ids, staging, ring, max_workgroups)
     keep, hp = _host_ids(block_ids_host)
-    _check(_lib.kv_blocks_stash(pool.handle, block_ids.numel(), _ptr(block_ids), hp,
-                                _ptr(staging), 1 if on_host else 0, _stream(stream)),
+    _check(_lib.kv_blocks_stash(pool.handle, block_ids.numel(), _ptr(block_ids), hp, _ptr(staging),
+                                _nbytes(staging), 1 if on_host else 0, rp, rb, max_workgroups,
+                                _stream(stream)),
            "kv_blocks_stash")
     del keep
     return staging
 
 
 def kv_blocks_restore(pool: KVPool, block_ids: torch.Tensor, staging: torch.Tensor,
-                      block_ids_host=None, stream=None):
-    """Copy ``staging`` (device or pinned host) back into pool blocks ``block_ids``."""
-    _dev(block_ids, "block_ids", torch.int32)
-    on_host = not staging.is_cuda
-    if on_host and not staging.is_pinned():
-        raise ValueError("host staging must be pinned memory")
+                      block_ids_host=None, ring: Optional[torch.Tensor] = None,
+                      max_workgroups: int = 0, stream=None):
+    """Copy ``staging`` (device, or pinned host through the device ``ring``) back into
+    pool blocks ``block_ids``."""
+    on_host, rp, rb = _copy_args(pool, block_ids, staging, ring, max_workgroups)
     keep, hp = _host_ids(block_ids_host)
     _check(_lib.kv_blocks_restore(pool.handle, block_ids.numel(), _ptr(block_ids), hp,
-                                  _ptr(staging), 1 if on_host else 0, _stream(stream)),
+                                  _ptr(staging), _nbytes(staging), 1 if on_host else 0, rp, rb,
+                                  max_workgroups, _stream(stream)),
            "kv_blocks_restore")
     del keep
 
 
 def kv_blocks_restore_layers(pool: KVPool, layer_begin: int, layer_count: int, block_ids: torch.Tensor,
-                             staging: torch.Tensor, block_ids_host=None, stream=None):
+                             staging: torch.Tensor, block_ids_host=None,
+                             ring: Optional[torch.Tensor] = None, max_workgroups: int = 0,
+                             stream=None):
     """Restore layers [layer_begin, layer_begin + layer_count) of ``block_ids`` from an
-    all-layer ``staging`` (device or pinned host)."""
-    _dev(block_ids, "block_ids", torch.int32)
-    on_host = not staging.is_cuda
-    if on_host and not staging.is_pinned():
-        raise ValueError("host staging must be pinned memory")
+    all-layer ``staging`` (device, or pinned host through the device ``ring``)."""
+    on_host, rp, rb = _copy_args(pool, block_ids, staging, ring, max_workgroups)
     keep, hp = _host_ids(block_ids_host)
     _check(_lib.kv_blocks_restore_layers(pool.handle, layer_begin, layer_count, block_ids.numel(),
-                                         _ptr(block_ids), hp, _ptr(staging), 1 if on_host else 0,
+                                         _ptr(block_ids), hp, _ptr(staging), _nbytes(staging),
+                                         1 if on_host else 0, rp, rb, max_workgroups,
                                          _stream(stream)), "kv_blocks_restore_layers")
     del keep
 
 
-def ls_device_errors(stream=None) -> int:
-    """Wait for the stream, then read and clear the device error word."""
+def ls_device_errors() -> int:
+    """Wait for all work on the device, then read and clear its error word."""
     bits = ctypes.c_uint32()
-    _check(_lib.ls_device_errors(ctypes.byref(bits), _stream(stream)), "ls_device_errors")
+    _check(_lib.ls_device_errors(ctypes.byref(bits)), "ls_device_errors")
     return int(bits.value)
 
 

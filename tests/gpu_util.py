@@ -46,7 +46,8 @@ def assert_attn_close(gpu: torch.Tensor, ref: np.ndarray, what: str):
 
 
 class DevicePool:
-    """A pool uploaded to the GPU and wrapped by kv_pool_create."""
+    """A pool uploaded to the GPU and wrapped by kv_pool_create, with an optional
+    device ring (whole all-layer blocks) for host-staged copies."""
 
     def __init__(self, kv_mod, pool_host: np.ndarray, head_dim: int, ring_blocks: int = 0):
         nl, nb, _, hkv, _ = pool_host.shape
@@ -56,7 +57,7 @@ class DevicePool:
         if ring_blocks:
             per_block = nl * 2 * hkv * 16 * head_dim * 2
             self.ring = torch.empty(ring_blocks * per_block, dtype=torch.uint8, device="cuda")
-        self.pool = kv_mod.kv_pool_create(self.data, nl, nb, hkv, head_dim, 16, self.ring)
+        self.pool = kv_mod.kv_pool_create(self.data, nl, nb, hkv, head_dim, 16)
         self.shape = pool_host.shape
 
     def host(self) -> np.ndarray:

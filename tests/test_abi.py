@@ -23,8 +23,7 @@ class Desc(ctypes.Structure):
     _fields_ = [("num_layers", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("block_size", ctypes.c_int32),
                 ("num_blocks", ctypes.c_int64), ("kv_base", ctypes.c_void_p),
-                ("kv_bytes", ctypes.c_size_t), ("staging_ring", ctypes.c_void_p),
-                ("staging_ring_bytes", ctypes.c_size_t)]
+                ("kv_bytes", ctypes.c_size_t)]
 
 
 @pytest.fixture(scope="module")
@@ -63,8 +62,7 @@ def test_version_and_pool_bytes(lib):
 
 def _desc(**kw):
     d = dict(num_layers=2, num_kv_heads=4, head_dim=128, block_size=16, num_blocks=100,
-             kv_base=0x100000, kv_bytes=2 * 100 * 2 * 4 * 16 * 128 * 2, staging_ring=None,
-             staging_ring_bytes=0)
+             kv_base=0x100000, kv_bytes=2 * 100 * 2 * 4 * 16 * 128 * 2)
     d.update(kw)
     return Desc(**d)
 
@@ -96,15 +94,20 @@ def pool(lib):
 F = 0x200000  # a fake, never dereferenced, device address
 
 
+def _i32s(v):
+    return None if v is None else (ctypes.c_int32 * len(v))(*v)
+
+
 def _decode(lib, pool, **kw):
-    a = dict(layer=0, S=4, hq=32, q=F, kn=None, vn=None, bt=F, maxb=8, lens=F, scale=0.088,
-             out=F, ws=F, wsb=1 << 30)
+    a = dict(layer=0, S=4, hq=32, q=F, kn=None, vn=None, bt=F, maxb=8, lens=F, lens_host=None,
+             scale=0.088, out=F, ws=F, wsb=1 << 30)
     a.update(kw)
     return lib.paged_attn_decode(pool, a["layer"], a["S"], a["hq"], ctypes.c_void_p(a["q"]),
                                  ctypes.c_void_p(a["kn"]), ctypes.c_void_p(a["vn"]),
                                  ctypes.c_void_p(a["bt"]), a["maxb"], ctypes.c_void_p(a["lens"]),
-                                 ctypes.c_float(a["scale"]), ctypes.c_void_p(a["out"]),
-                                 ctypes.c_void_p(a["ws"]), ctypes.c_size_t(a["wsb"]), None)
+                                 _i32s(a["lens_host"]), ctypes.c_float(a["scale"]),
+                                 ctypes.c_void_p(a["out"]), ctypes.c_void_p(a["ws"]),
+                                 ctypes.c_size_t(a["wsb"]), None)
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -117,9 +120,15 @@ def _decode(lib, pool, **kw):
     (dict(scale=0.0), LS_EINVAL),
     (dict(scale=float("nan")), LS_EINVAL),
     (dict(wsb=16), LS_ENOMEM),
+    # host lengths: an empty context, a negative one, keys past the 8-block table
+    (dict(lens_host=[5, 0, 7, 9]), LS_EINVAL),
+    (dict(lens_host=[5, -1, 7, 9], kn=F, vn=F), LS_EINVAL),
+    (dict(lens_host=[5, 129, 7, 9]), LS_EINVAL),
+    (dict(lens_host=[5, 128, 7, 9], kn=F, vn=F), LS_EINVAL),
 ])
 def test_decode_rejects_before_launch(lib, pool, kw, status):
     assert _decode(lib, pool, **kw) == status
+    assert lib.ls_last_error() != b""
 
 
 def test_decode_zero_sessions_is_noop(lib, pool):
@@ -137,14 +146,15 @@ def test_workspace_query(lib, pool):
 
 
 def _prefill(lib, pool, **kw):
-    a = dict(layer=0, S=2, hq=32, q=F, kn=None, vn=None, cu=F, ctx=F, total=100, maxn=60, bt=F,
-             maxb=8, scale=0.088, out=F)
+    a = dict(layer=0, S=2, hq=32, q=F, kn=None, vn=None, cu=F, ctx=F, lens_host=None, total=100,
+             maxn=60, bt=F, maxb=8, scale=0.088, out=F)
     a.update(kw)
     return lib.paged_attn_prefill(pool, a["layer"], a["S"], a["hq"], ctypes.c_void_p(a["q"]),
                                   ctypes.c_void_p(a["kn"]), ctypes.c_void_p(a["vn"]),
-                                  ctypes.c_void_p(a["cu"]), ctypes.c_void_p(a["ctx"]), a["total"],
-                                  a["maxn"], ctypes.c_void_p(a["bt"]), a["maxb"],
-                                  ctypes.c_float(a["scale"]), ctypes.c_void_p(a["out"]), None)
+                                  ctypes.c_void_p(a["cu"]), ctypes.c_void_p(a["ctx"]),
+                                  _i32s(a["lens_host"]), a["total"], a["maxn"],
+                                  ctypes.c_void_p(a["bt"]), a["maxb"], ctypes.c_float(a["scale"]),
+                                  ctypes.c_void_p(a["out"]), None)
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -154,13 +164,32 @@ def _prefill(lib, pool, **kw):
     (dict(vn=F), LS_EINVAL),
     (dict(maxn=200), LS_EINVAL),
     (dict(total=-1), LS_EINVAL),
+    # host (n, c) pairs: a turn above max_new_len, lengths not adding up to the
+    # total, keys past the 8-block table, a negative context
+    (dict(lens_host=[61, 0, 39, 5]), LS_EINVAL),
+    (dict(lens_host=[60, 0, 39, 5]), LS_EINVAL),
+    (dict(lens_host=[60, 70, 40, 5]), LS_EINVAL),
+    (dict(lens_host=[60, 0, 40, -1]), LS_EINVAL),
 ])
 def test_prefill_rejects_before_launch(lib, pool, kw, status):
     assert _prefill(lib, pool, **kw) == status
+    assert lib.ls_last_error() != b""
 
 
 def test_prefill_empty_is_noop(lib, pool):
     assert _prefill(lib, pool, total=0, maxn=0, q=None) == LS_OK
+
+
+BLOCK = 2 * 2 * 4 * 16 * 128 * 2        # all-layer bytes of one block of the test pool
+
+
+def _copy(lib, fn, pool, n, ids=F, ids_host=None, staging=F, staging_bytes=None, on_host=0,
+          ring=None, ring_bytes=0, budget=0):
+    if staging_bytes is None:
+        staging_bytes = max(n, 0) * BLOCK
+    return getattr(lib, fn)(pool, n, ctypes.c_void_p(ids), ids_host, ctypes.c_void_p(staging),
+                            ctypes.c_size_t(staging_bytes), on_host, ctypes.c_void_p(ring),
+                            ctypes.c_size_t(ring_bytes), budget, None)
 
 
 @pytest.mark.parametrize("fn", ["kv_blocks_restore", "kv_blocks_stash"])
@@ -168,19 +197,105 @@ def test_prefill_empty_is_noop(lib, pool):
                                         ([-1], LS_EINVAL)])
 def test_copy_rejects_bad_host_ids(lib, pool, fn, ids, status):
     arr = (ctypes.c_int32 * len(ids))(*ids)
-    r = getattr(lib, fn)(pool, len(ids), ctypes.c_void_p(F), arr, ctypes.c_void_p(F), 0, None)
-    assert r == status
+    assert _copy(lib, fn, pool, len(ids), ids_host=arr) == status
     msg = lib.ls_last_error()
     assert b"twice" in msg or b"outside" in msg
 
 
 @pytest.mark.parametrize("fn", ["kv_blocks_restore", "kv_blocks_stash"])
-def test_copy_host_staging_needs_ring(lib, pool, fn):
+@pytest.mark.parametrize("kw,status,word", [
+    (dict(on_host=1), LS_ENOMEM, b"ring"),                                   # no ring
+    (dict(on_host=1, ring=F, ring_bytes=BLOCK - 16), LS_ENOMEM, b"ring"),    # ring below one block
+    (dict(on_host=1, ring=F + 8, ring_bytes=BLOCK), LS_EINVAL, b"aligned"),
+    (dict(staging_bytes=2 * BLOCK - 1), LS_ENOMEM, b"staging_bytes"),       # staging short of 2 blocks
+    (dict(budget=-1), LS_EINVAL, b"max_workgroups"),
+])
+def test_copy_rejects_staging_ring_and_budget(lib, pool, fn, kw, status, word):
     arr = (ctypes.c_int32 * 2)(1, 2)
-    assert getattr(lib, fn)(pool, 2, ctypes.c_void_p(F), arr, ctypes.c_void_p(F), 1, None) == LS_ENOMEM
+    assert _copy(lib, fn, pool, 2, ids_host=arr, **kw) == status
+    assert word in lib.ls_last_error()
+
+
+def test_restore_layers_checks_range_and_staging(lib, pool):
+    arr = (ctypes.c_int32 * 2)(1, 2)
+    L = lib.kv_blocks_restore_layers
+
+    def call(lb, lc, staging_bytes=2 * BLOCK, on_host=0, ring_bytes=0):
+        return L(pool, lb, lc, 2, ctypes.c_void_p(F), arr, ctypes.c_void_p(F),
+                 ctypes.c_size_t(staging_bytes), on_host, ctypes.c_void_p(F),
+                 ctypes.c_size_t(ring_bytes), 0, None)
+    assert call(1, 2) == LS_EINVAL                   # layers [1, 3) of 2
+    assert call(-1, 1) == LS_EINVAL
+    assert call(1, 1, staging_bytes=2 * BLOCK - 2) == LS_ENOMEM   # all-layer stride even for one layer
+    assert call(1, 1, on_host=1, ring_bytes=BLOCK // 2 - 1) == LS_ENOMEM   # ring below one layer slab
 
 
 @pytest.mark.parametrize("fn", ["kv_blocks_restore", "kv_blocks_stash"])
 def test_copy_zero_blocks_is_noop(lib, pool, fn):
-    assert getattr(lib, fn)(pool, 0, None, None, None, 0, None) == LS_OK
-    assert getattr(lib, fn)(pool, -1, None, None, None, 0, None) == LS_EINVAL
+    assert _copy(lib, fn, pool, 0, ids=None, staging=None) == LS_OK
+    assert _copy(lib, fn, pool, -1, ids=None, staging=None) == LS_EINVAL
+
+
+# ---- the Python binding checks every tensor's shape before any device access
+@pytest.fixture()
+def binding():
+    try:
+        from paper_2606_22983_amd import kv
+    except ImportError as e:  # the library is built by the session fixture in other tests
+        pytest.skip(str(e))
+    return kv
+
+
+def _fake_pool(kv, nl=1, hkv=4, d=128):
+    return kv.KVPool(None, None, nl, 100, hkv, d, 16)
+
+
+def _bf(*shape):
+    import torch
+    return torch.zeros(shape, dtype=torch.bfloat16)
+
+
+def _i32(*shape):
+    import torch
+    return torch.zeros(shape, dtype=torch.int32)
+
+
+@pytest.mark.parametrize("bad", ["out", "k_new", "v_new", "tables", "lens", "head_dim", "lens_host"])
+def test_binding_decode_shape_checks(built_lib, binding, bad):
+    kv = binding
+    S, hq, hkv, d = 4, 32, 4, 128
+    a = dict(q=_bf(S, hq, d), out=_bf(S, hq, d), k_new=_bf(S, hkv, d), v_new=_bf(S, hkv, d),
+             tables=_i32(S, 8), lens=_i32(S), lens_host=[5, 6, 7, 8])
+    a[{"out": "out", "k_new": "k_new", "v_new": "v_new", "tables": "tables", "lens": "lens",
+       "head_dim": "q", "lens_host": "lens_host"}[bad]] = {
+        "out": _bf(S, hq + 1, d), "k_new": _bf(S, hkv, d + 1), "v_new": _bf(S - 1, hkv, d),
+        "tables": _i32(S + 1, 8), "lens": _i32(S, 1), "head_dim": _bf(S, hq, 64),
+        "lens_host": [5, 6, 7]}[bad]
+    if bad == "head_dim":
+        a["out"] = _bf(S, hq, 64)
+    with pytest.raises(ValueError):
+        kv.paged_attn_decode(_fake_pool(kv), 0, a["q"], a["tables"], a["lens"], 0.1, a["out"],
+                             _bf(16), a["k_new"], a["v_new"], context_lens_host=a["lens_host"])
+
+
+@pytest.mark.parametrize("bad", ["cu", "out", "k_new", "tables"])
+def test_binding_prefill_shape_checks(built_lib, binding, bad):
+    kv = binding
+    S, T, hq, hkv, d = 3, 50, 32, 4, 128
+    a = dict(q=_bf(T, hq, d), out=_bf(T, hq, d), k_new=_bf(T, hkv, d), cu=_i32(S + 1),
+             tables=_i32(S, 8))
+    a[bad] = {"cu": _i32(S), "out": _bf(T - 1, hq, d), "k_new": _bf(T, hkv + 1, d),
+              "tables": _i32(S - 1, 8)}[bad]
+    with pytest.raises(ValueError):
+        kv.paged_attn_prefill(_fake_pool(kv), 0, a["q"], a["cu"], _i32(S), 30, a["tables"], 0.1,
+                              a["out"], a["k_new"], _bf(T, hkv, d))
+
+
+def test_binding_copy_checks_staging_size(built_lib, binding):
+    kv = binding
+    pool = _fake_pool(kv, nl=2)
+    with pytest.raises(ValueError, match="staging"):
+        kv.kv_blocks_restore(pool, _i32(3), _bf(3 * pool.block_bytes // 2 - 1))
+    with pytest.raises(ValueError, match="max_workgroups"):
+        kv.kv_blocks_stash(pool, _i32(3), _bf(3 * pool.block_bytes // 2),
+                           max_workgroups=-2)

@@ -71,13 +71,13 @@ def test_pinned_host_staging_through_ring(kv, oracle_lib):
     ids = rng.permutation(nb)[:n].astype(np.int32)
     dp = DevicePool(kv, pool, d, ring_blocks=3)
     host = torch.empty((n, nl, 2, hkv, 16 * d), dtype=torch.int16, pin_memory=True)
-    kv.kv_blocks_stash(dp.pool, i32_dev(ids), host, block_ids_host=ids)
+    kv.kv_blocks_stash(dp.pool, i32_dev(ids), host, block_ids_host=ids, ring=dp.ring)
     torch.cuda.synchronize()
     assert np.array_equal(host.numpy().view(np.uint16), oracle_lib.stash(pool, 16, d, ids))
     fresh = _random_pool(rng, n, nl, hkv, d).reshape(n, nl, 2, hkv, 16 * d)
     host.copy_(torch.from_numpy(fresh.view(np.int16)))
     ids2 = rng.permutation(nb)[:n].astype(np.int32)
-    kv.kv_blocks_restore(dp.pool, i32_dev(ids2), host, block_ids_host=ids2)
+    kv.kv_blocks_restore(dp.pool, i32_dev(ids2), host, block_ids_host=ids2, ring=dp.ring)
     torch.cuda.synchronize()
     assert np.array_equal(dp.host(), oracle_lib.restore(pool.copy(), 16, d, ids2, fresh))
 
@@ -163,16 +163,100 @@ def test_restore_by_layer_ranges_equals_full_restore(kv, oracle_lib, on_host):
     expect = oracle_lib.restore(pool.copy(), 16, d, ids, staging)
     layer_bytes = 2 * hkv * 16 * d * 2
     dp = DevicePool(kv, pool, d, ring_blocks=0)
+    ring = None
     if on_host:
         ring = torch.empty(5 * layer_bytes, dtype=torch.uint8, device="cuda")   # 5 layer slabs
-        dp.pool = kv.kv_pool_create(dp.data, nl, nb, hkv, d, 16, ring)
         st = torch.from_numpy(staging.view(np.int16)).pin_memory()
     else:
         st = bf16_dev(staging)
     for lb, lc in ((0, 1), (1, 3), (4, 1)):
-        kv.kv_blocks_restore_layers(dp.pool, lb, lc, i32_dev(ids), st, block_ids_host=ids)
+        kv.kv_blocks_restore_layers(dp.pool, lb, lc, i32_dev(ids), st, block_ids_host=ids, ring=ring)
     torch.cuda.synchronize()
     assert np.array_equal(dp.host(), expect)
     with pytest.raises(kv.LiveServeError):
-        kv.kv_blocks_restore_layers(dp.pool, 4, 2, i32_dev(ids), st)
+        kv.kv_blocks_restore_layers(dp.pool, 4, 2, i32_dev(ids), st, ring=ring)
+    assert kv.ls_device_errors() == 0
+
+
+def test_host_staged_stash_and_restore_on_two_streams(kv, oracle_lib):
+    """An eviction stash to pinned host memory on one stream and a preload restore
+    from pinned host memory on another, at the same time, on disjoint blocks, each
+    through its own ring (a ring narrower than either copy, so both cycle it):
+    both bit-exact against the oracle."""
+    rng = np.random.default_rng(51)
+    nl, hkv, d, nb, n = 6, 4, 128, 120, 40
+    pool = _random_pool(rng, nl, nb, hkv, d)
+    perm = rng.permutation(nb).astype(np.int32)
+    out_ids, in_ids = perm[:n], perm[n:2 * n]
+    incoming = _random_pool(rng, n, nl, hkv, d).reshape(n, nl, 2, hkv, 16 * d)
+    dp = DevicePool(kv, pool, d)
+    per_block = nl * 2 * hkv * 16 * d * 2
+    rings = [torch.empty(3 * per_block, dtype=torch.uint8, device="cuda") for _ in range(2)]
+    evicted = torch.empty((n, nl, 2, hkv, 16 * d), dtype=torch.int16, pin_memory=True)
+    preload = torch.from_numpy(incoming.view(np.int16)).pin_memory()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    for rep in range(3):
+        with torch.cuda.stream(streams[0]):
+            kv.kv_blocks_stash(dp.pool, i32_dev(out_ids), evicted, block_ids_host=out_ids, ring=rings[0])
+        with torch.cuda.stream(streams[1]):
+            kv.kv_blocks_restore(dp.pool, i32_dev(in_ids), preload, block_ids_host=in_ids, ring=rings[1])
+        torch.cuda.synchronize()
+        assert np.array_equal(evicted.numpy().view(np.uint16), oracle_lib.stash(pool, 16, d, out_ids)), rep
+        assert np.array_equal(dp.host(), oracle_lib.restore(pool.copy(), 16, d, in_ids, incoming)), rep
+    assert kv.ls_device_errors() == 0
+
+
+@pytest.mark.parametrize("budget", [1, 3, 64])
+def test_budgeted_copies_are_bit_exact(kv, oracle_lib, budget):
+    """A bounded-interference copy (at most `budget` workgroups) moves the same bytes."""
+    rng = np.random.default_rng(60 + budget)
+    nl, hkv, d, nb, n = 5, 4, 128, 90, 70
+    pool = _random_pool(rng, nl, nb, hkv, d)
+    ids = rng.permutation(nb)[:n].astype(np.int32)
+    dp = DevicePool(kv, pool, d, ring_blocks=4)
+    st = torch.empty((n, nl, 2, hkv, 16 * d), dtype=torch.int16, device="cuda")
+    kv.kv_blocks_stash(dp.pool, i32_dev(ids), st, max_workgroups=budget)
+    assert np.array_equal(host_bits(st), oracle_lib.stash(pool, 16, d, ids))
+    fresh = _random_pool(rng, n, nl, hkv, d).reshape(n, nl, 2, hkv, 16 * d)
+    host = torch.from_numpy(fresh.view(np.int16)).pin_memory()
+    ids2 = rng.permutation(nb)[:n].astype(np.int32)
+    kv.kv_blocks_restore(dp.pool, i32_dev(ids2), host, block_ids_host=ids2, ring=dp.ring,
+                         max_workgroups=budget)
+    assert np.array_equal(dp.host(), oracle_lib.restore(pool.copy(), 16, d, ids2, fresh))
+    assert kv.ls_device_errors() == 0
+
+
+def test_restore_at_preload_geometry_10k_blocks(kv, oracle_lib):
+    """The preload workload's geometry (48 layers x 4 KV heads x D = 128, 1.5 MiB
+    per block) at 10,000 blocks (15 GiB; byte offsets far past 2^32): stash a
+    random slot set, poison the pool, restore into a fresh permutation, bit-exact
+    against the oracle's byte copies.  Contents come from a seeded device generator
+    and are copied to the host for the oracle."""
+    nl, hkv, d, n, nb = 48, 4, 128, 10000, 10240
+    elems = nl * nb * 2 * hkv * 16 * d
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(26065)
+    data = torch.empty(elems, dtype=torch.int16, device="cuda")
+    data.random_(-32768, 32767, generator=gen)
+    pool = data.cpu().numpy().view(np.uint16).reshape(nl, nb, 2, hkv, 16 * d)
+    rng = np.random.default_rng(26065)
+    a = rng.permutation(nb)[:n].astype(np.int32)
+    b = rng.permutation(nb)[:n].astype(np.int32)
+    log("restore at the preload geometry: %d of %d blocks, %.1f GiB" % (n, nb, n * nl * 32768 / 2 ** 30))
+    p = kv.kv_pool_create(data, nl, nb, hkv, d, 16)
+    st = torch.empty((n, nl, 2, hkv, 16 * d), dtype=torch.int16, device="cuda")
+    kv.kv_blocks_stash(p, i32_dev(a), st, block_ids_host=a)
+    st_host = st.cpu().numpy().view(np.uint16)
+    assert np.array_equal(st_host, oracle_lib.stash(pool, 16, d, a))
+    data.fill_(0x7FC0)                                   # poison every block
+    kv.kv_blocks_restore(p, i32_dev(b), st, block_ids_host=b)
+    del st
+    torch.cuda.synchronize()
+    expect = np.full_like(pool, 0x7FC0)
+    del pool
+    oracle_lib.restore(expect, 16, d, b, st_host)
+    del st_host
+    got = data.cpu().numpy().view(np.uint16).reshape(expect.shape)
+    assert np.array_equal(got, expect)
     assert kv.ls_device_errors() == 0

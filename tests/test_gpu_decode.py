@@ -191,3 +191,53 @@ def test_out_of_range_block_id_is_flagged_not_read(kv):
     out, _ = run_decode(kv, dp, bf16_dev(q), i32_dev(bad), i32_dev([100, 40]), 0.125)
     assert kv.ls_device_errors() & kv.LS_DEVERR_BLOCK_ID
     torch.cuda.synchronize()
+
+
+def test_empty_context_is_flagged_with_zero_output(kv, oracle_lib):
+    """A session with no key (length 0, no append) gets a zero output row and
+    LS_DEVERR_LENGTH; the other sessions are unaffected.  With host lengths the
+    call is refused before anything is enqueued."""
+    rng = np.random.default_rng(10)
+    lens = [40, 0, 1100, 3]
+    pool, tables, q, _, _ = _synthetic(rng, lens, 32, 4, 128, False)
+    dp = DevicePool(kv, pool, 128)
+    kv.ls_device_errors()
+    out, ws = run_decode(kv, dp, bf16_dev(q), i32_dev(tables), i32_dev(lens), 0.0884)
+    assert kv.ls_device_errors() & kv.LS_DEVERR_LENGTH
+    got = out.float().cpu().numpy()
+    assert (got[1] == 0).all()
+    keep = [0, 2, 3]
+    ref = oracle_lib.decode(pool, 16, 128, 0, q, tables, np.array(lens), 0.0884, sessions=keep)
+    assert_attn_close(out[keep], ref, "decode beside an empty context")
+    with pytest.raises(kv.LiveServeError):
+        kv.paged_attn_decode(dp.pool, 0, bf16_dev(q), i32_dev(tables), i32_dev(lens), 0.0884, out, ws,
+                             context_lens_host=np.array(lens))
+    # the same session with its own token appended has one key: fine
+    kn, vn = W.normal_bf16(rng, (4, 4, 128)), W.normal_bf16(rng, (4, 4, 128))
+    out2, _ = run_decode(kv, dp, bf16_dev(q), i32_dev(tables), i32_dev(lens), 0.0884, bf16_dev(kn),
+                         bf16_dev(vn))
+    ref2 = oracle_lib.decode(pool, 16, 128, 0, q, tables, np.array(lens), 0.0884, k_new=kn, v_new=vn)
+    assert_attn_close(out2, ref2, "decode with append, context 0 included")
+    assert kv.ls_device_errors() == 0
+
+
+@pytest.mark.parametrize("append", [False, True])
+def test_decode_with_host_lengths_matches_oracle(kv, oracle_lib, append):
+    """context_lens_host given (host-side checks and split planning)."""
+    rng = np.random.default_rng(20 + append)
+    lens = rng.integers(1, 5000, size=96)
+    lens[:4] = [1, 16, 1024, 4097]
+    pool, tables, q, kn, vn = _synthetic(rng, lens, 16, 2, 128, append)
+    dp = DevicePool(kv, pool, 128)
+    ws = torch.zeros(kv.decode_workspace_bytes(dp.pool, 96, 16, tables.shape[1]), dtype=torch.uint8,
+                     device="cuda")
+    out = torch.empty((96, 16, 128), dtype=torch.bfloat16, device="cuda")
+    kv.paged_attn_decode(dp.pool, 0, bf16_dev(q), i32_dev(tables), i32_dev(lens), 0.0884, out, ws,
+                         None if kn is None else bf16_dev(kn), None if vn is None else bf16_dev(vn),
+                         context_lens_host=lens)
+    ref, ref_pool = oracle_lib.decode(pool, 16, 128, 0, q, tables, lens, 0.0884, k_new=kn, v_new=vn,
+                                      pool_out=True)
+    assert_attn_close(out, ref, "decode with host lengths, append=%s" % append)
+    if append:
+        assert np.array_equal(dp.host(), ref_pool)
+    assert kv.ls_device_errors() == 0

@@ -1,12 +1,13 @@
-"""The talker's 32-step decode loop (append + decode + split merge per step)
-captured as one HIP graph and replayed: every replay gives bit for bit the
-eager outputs and pool, with eager work between the replays."""
+"""The talker's decode loop (each step appends its token, attends, merges its
+splits) captured as one HIP graph and replayed: every replay gives bit for bit
+the eager outputs and pool, with eager work between the replays, and the
+replayed steps match the oracle."""
 import numpy as np
 import pytest
 import torch
 
 from paper_2606_22983_amd import workloads as W
-from tests.gpu_util import DevicePool, bf16_dev, i32_dev
+from tests.gpu_util import DevicePool, assert_attn_close, bf16_dev, i32_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -18,7 +19,7 @@ def kv():
     return kv_mod
 
 
-def test_captured_talker_steps_replay_exactly(kv):
+def test_captured_talker_steps_replay_exactly(kv, oracle_lib):
     case = W.talker_decode(num_sessions=64, steps=8)
     dp = DevicePool(kv, case.pool.data, 128)
     tables = i32_dev(case.block_tables)
@@ -51,3 +52,16 @@ def test_captured_talker_steps_replay_exactly(kv):
             assert torch.equal(outs[t].view(torch.int16), eager[t].view(torch.int16)), (r, t)
         assert torch.equal(dp.data.view(torch.int16), pool_after.view(torch.int16)), r
     assert kv.ls_device_errors() == 0
+    # The replayed steps against the oracle (each step appends its token first).
+    ref_pool = case.pool.data.copy()
+    for t in range(case.steps):
+        lens_t = case.lens_at(t)
+        if t in (0, 1, 4, 7):
+            ref, ref_pool = oracle_lib.decode(ref_pool, 16, 128, 0, case.q[t], case.block_tables, lens_t,
+                                              case.scale, k_new=case.k_new[t], v_new=case.v_new[t],
+                                              pool_out=True)
+            assert_attn_close(outs[t], ref, "graph replay, step %d" % t)
+        else:
+            oracle_lib.append(ref_pool, 16, 128, 0, case.block_tables, np.arange(S), lens_t,
+                              case.k_new[t], case.v_new[t])
+    assert np.array_equal(dp.host(), ref_pool), "pool after the replays differs from the oracle's"

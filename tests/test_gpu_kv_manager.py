@@ -37,12 +37,14 @@ def _runs(moves: np.ndarray):
 
 def _stash(kv, dp, store, moves):
     for h, ids in _runs(moves):
-        kv.kv_blocks_stash(dp.pool, i32_dev(ids), store[h:h + len(ids)], block_ids_host=ids)
+        kv.kv_blocks_stash(dp.pool, i32_dev(ids), store[h:h + len(ids)], block_ids_host=ids,
+                           ring=dp.ring)
 
 
 def _restore(kv, dp, store, moves):
     for h, ids in _runs(moves):
-        kv.kv_blocks_restore(dp.pool, i32_dev(ids), store[h:h + len(ids)], block_ids_host=ids)
+        kv.kv_blocks_restore(dp.pool, i32_dev(ids), store[h:h + len(ids)], block_ids_host=ids,
+                             ring=dp.ring)
 
 
 def _tables(m, sessions, maxb):
@@ -97,7 +99,7 @@ def test_manager_drives_stash_reuse_preload_restore(kv):
     assert ok and len(r) == 5
     first = _runs(r)[0]
     kv.kv_blocks_restore(dp.pool, i32_dev(first[1][:2]), store[first[0]:first[0] + 2],
-                         block_ids_host=first[1][:2])
+                         block_ids_host=first[1][:2], ring=dp.ring)
     torch.cuda.synchronize()
     m.preload_cancel(1)
     r, e = m.load_sync(1)

@@ -57,7 +57,7 @@ def test_layer_pipelined_restore_then_prefill(kv, oracle_lib):
         dp = DevicePool(kv, pool, D, ring_blocks=8)
         store = torch.empty((len(ctx_ids), NL, 2, HKV, 16 * D), dtype=torch.int16, pin_memory=True)
         ids = i32_dev(ctx_ids)
-        kv.kv_blocks_stash(dp.pool, ids, store, block_ids_host=ctx_ids)       # offload the context
+        kv.kv_blocks_stash(dp.pool, ids, store, block_ids_host=ctx_ids, ring=dp.ring)       # offload the context
         dp.data.view(NL, pool.shape[1], -1)[:, ids.long()] = float("nan")     # its blocks are reused
         outs = [torch.empty_like(x) for x in qd]
         main = torch.cuda.current_stream()
@@ -68,7 +68,8 @@ def test_layer_pipelined_restore_then_prefill(kv, oracle_lib):
 
             def restore_layer(l):
                 with torch.cuda.stream(copy):
-                    kv.kv_blocks_restore_layers(dp.pool, l, 1, ids, store, block_ids_host=ctx_ids)
+                    kv.kv_blocks_restore_layers(dp.pool, l, 1, ids, store, block_ids_host=ctx_ids,
+                                                ring=dp.ring)
                     e = torch.cuda.Event()
                     e.record(copy)
                     events.append(e)
@@ -80,7 +81,7 @@ def test_layer_pipelined_restore_then_prefill(kv, oracle_lib):
                 kv.paged_attn_prefill(dp.pool, l, qd[l], *args[:4], args[4], outs[l], knd[l], vnd[l])
             main.wait_stream(copy)
         else:
-            kv.kv_blocks_restore(dp.pool, ids, store, block_ids_host=ctx_ids)
+            kv.kv_blocks_restore(dp.pool, ids, store, block_ids_host=ctx_ids, ring=dp.ring)
             for l in range(NL):
                 kv.paged_attn_prefill(dp.pool, l, qd[l], *args[:4], args[4], outs[l], knd[l], vnd[l])
         torch.cuda.synchronize()

@@ -63,19 +63,84 @@ def test_prefill_ragged(kv, oracle_lib, d, hq, hkv):
     assert kv.ls_device_errors() == 0
 
 
-def test_prefill_many_sessions(kv, oracle_lib):
-    """More sessions than the in-kernel longest-first ordering handles (index
-    order), with empty turns mixed in."""
-    rng = np.random.default_rng(140)
-    d, hq, hkv = 64, 8, 2
+@pytest.mark.parametrize("hkv", [2, 4])
+def test_prefill_many_sessions(kv, oracle_lib, hkv):
+    """140 sessions with empty turns mixed in.  With 2 KV heads (280 session/KV-head
+    pairs) the in-kernel longest-first XCD schedule runs; with 4 KV heads (560
+    pairs, above the 512 it orders) the workgroups take their items in index order."""
+    rng = np.random.default_rng(140 + hkv)
+    d, hq = 64, 8
     n = rng.integers(0, 40, size=140)
     n[0] = 39
     c = rng.integers(0, 200, size=140)
+    assert (140 * hkv > 512) == (hkv == 4)
     pool, tables, q, kn, vn = _case(rng, n, c, hq, hkv, d)
     dp = DevicePool(kv, pool, d)
     out, cu = _run(kv, dp, q, kn, vn, n, c, tables, 0.125)
     ref = oracle_lib.prefill(pool, 16, d, 0, q, kn, vn, cu, c, tables, 0.125)
-    assert_attn_close(out, ref, "prefill, 140 sessions")
+    assert_attn_close(out, ref, "prefill, 140 sessions x %d KV heads" % hkv)
+    assert kv.ls_device_errors() == 0
+
+
+def test_prefill_index_order_long_turns(kv, oracle_lib):
+    """The index-order schedule (600 pairs) with turns spanning several query
+    tiles and contexts spanning several key tiles, ragged tails everywhere."""
+    rng = np.random.default_rng(600)
+    d, hq, hkv = 128, 16, 4
+    S = 150
+    n = rng.integers(0, 200, size=S)
+    n[:3] = [199, 64, 65]
+    c = rng.integers(0, 700, size=S)
+    pool, tables, q, kn, vn = _case(rng, n, c, hq, hkv, d)
+    dp = DevicePool(kv, pool, d)
+    out, cu = _run(kv, dp, q, kn, vn, n, c, tables, 1 / math.sqrt(d))
+    ref = oracle_lib.prefill(pool, 16, d, 0, q, kn, vn, cu, c, tables, 1 / math.sqrt(d))
+    assert_attn_close(out, ref, "prefill, %d pairs in index order" % (S * hkv))
+    assert kv.ls_device_errors() == 0
+
+
+def test_prefill_turn_longer_than_max_new_len_is_flagged(kv, oracle_lib):
+    """max_new_len understated: the grid has tiles for max_new_len tokens only.
+    The device flags LS_DEVERR_LENGTH; rows inside the tiles are still right, and
+    the whole turn is appended."""
+    rng = np.random.default_rng(41)
+    d, hq, hkv = 128, 32, 4                   # 256 rows / G = 32 tokens per query tile
+    n, c = np.array([100, 40]), np.array([70, 300])
+    pool, tables, q, kn, vn = _case(rng, n, c, hq, hkv, d)
+    dp = DevicePool(kv, pool, d)
+    kv.ls_device_errors()
+    cu = np.concatenate([[0], np.cumsum(n)]).astype(np.int32)
+    out = torch.zeros((q.shape[0], hq, d), dtype=torch.bfloat16, device="cuda")
+    kv.paged_attn_prefill(dp.pool, 0, bf16_dev(q), i32_dev(cu), i32_dev(c), 40, i32_dev(tables),
+                          0.0884, out, bf16_dev(kn), bf16_dev(vn))
+    assert kv.ls_device_errors() & kv.LS_DEVERR_LENGTH
+    covered = np.concatenate([np.arange(0, 64), np.arange(100, 140)])   # 2 tiles of 32 tokens
+    ref, ref_pool = oracle_lib.prefill(pool, 16, d, 0, q, kn, vn, cu, c, tables, 0.0884, rows=covered,
+                                       pool_out=True)
+    assert_attn_close(out[torch.from_numpy(covered).cuda()], ref, "prefill rows inside the tiles")
+    assert np.array_equal(dp.host(), ref_pool)
+    with pytest.raises(kv.LiveServeError):     # with host lengths it is refused before launch
+        kv.paged_attn_prefill(dp.pool, 0, bf16_dev(q), i32_dev(cu), i32_dev(c), 40, i32_dev(tables),
+                              0.0884, out, bf16_dev(kn), bf16_dev(vn),
+                              lens_host=np.stack([n, c], 1))
+
+
+def test_prefill_host_lengths_same_result(kv):
+    """Host (n, c) pairs change validation and grid sizing only: same bits."""
+    rng = np.random.default_rng(43)
+    d, hq, hkv = 128, 32, 4
+    n, c = np.array([300, 1, 77, 0, 150]), np.array([900, 16, 0, 40, 333])
+    pool, tables, q, kn, vn = _case(rng, n, c, hq, hkv, d)
+    cu = np.concatenate([[0], np.cumsum(n)]).astype(np.int32)
+    outs = []
+    for lens_host in (None, np.stack([n, c], 1)):
+        dp = DevicePool(kv, pool, d)
+        out = torch.empty((q.shape[0], hq, d), dtype=torch.bfloat16, device="cuda")
+        kv.paged_attn_prefill(dp.pool, 0, bf16_dev(q), i32_dev(cu), i32_dev(c), int(n.max()),
+                              i32_dev(tables), 0.0884, out, bf16_dev(kn), bf16_dev(vn),
+                              lens_host=lens_host)
+        outs.append(out)
+    assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
     assert kv.ls_device_errors() == 0
 
 
@@ -124,13 +189,14 @@ def test_next_turn_prefill_full_sampled(kv, oracle_lib):
     out, cu = _run(kv, dp, case.q, case.k_new, case.v_new, n, case.reused_lens, case.block_tables,
                    case.scale)
     torch.cuda.synchronize()
-    # Sampled rows: first and last token of every session, tile edges of session 0,
-    # and random rows.
+    # Sampled rows: the first and last row of every query tile of every session
+    # (a tile holds 256 / G = 32 new tokens), plus random rows.
+    qtok = 256 // (case.num_q_heads // case.pool.num_kv_heads)
     rng = np.random.default_rng(33)
     rows = set()
     for s in range(case.num_sessions):
-        rows.update([int(cu[s]), int(cu[s + 1] - 1)])
-    rows.update(int(cu[0]) + j for j in (15, 16, 17, 31, 32, 33, 63, 64, 127, 128))
+        for j0 in range(0, int(n[s]), qtok):
+            rows.update([int(cu[s]) + j0, int(cu[s]) + min(j0 + qtok, int(n[s])) - 1])
     rows.update(rng.integers(0, int(cu[-1]), size=40).tolist())
     rows = np.array(sorted(rows))
     ref = oracle_lib.prefill(case.pool.data, 16, 128, 0, case.q, case.k_new, case.v_new, cu,

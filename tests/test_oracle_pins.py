@@ -25,7 +25,8 @@ GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_cases.json")
 
 # ----------------------------------------------------------------------------
 # test-side paged placement, written from the documented layout:
-#   pool[layer][block][kv][head][tile]; K tile [token][dim], V tile [dim][token]
+#   pool[layer][block][kv][head][tile]; K tile chunk-major [dim/8][token][8 dims],
+#   V tile dim-major [dim][token]
 # ----------------------------------------------------------------------------
 def make_paged(rng, lens, hkv, d, spare=3, nl=1, layer=0, k=None, v=None):
     """Place logical K/V [S][L][Hkv][D] (bf16 bits) into a shuffled paged pool."""
