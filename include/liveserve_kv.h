@@ -158,6 +158,28 @@ ls_status paged_attn_decode(ls_kv_pool *pool, int32_t layer, int32_t num_session
                             const int32_t *context_lens_host, float scale, void *out,
                             void *workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* Bytes of the static split scratch behind paged_attn_decode_static. */
+#define LS_DECODE_STATIC_SCRATCH_BYTES ((size_t)32 << 20)
+
+/*
+ * paged_attn_decode_static — paged_attn_decode without a workspace argument,
+ * for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation).  The split
+ * partials go to a static buffer of LS_DECODE_STATIC_SCRATCH_BYTES inside the
+ * library: one per GPU, resolved on the first call on that GPU and held until
+ * the process ends.  The call allocates nothing and calls no allocating
+ * routine.  LS_ENOMEM when the shape needs more scratch than that
+ * (ls_decode_workspace_bytes of the same shape).  Every call on a GPU shares
+ * its buffer, so calls that may overlap on one GPU (different streams) race:
+ * serialise them.  Other arguments, results and errors as paged_attn_decode.
+ */
+ls_status paged_attn_decode_static(ls_kv_pool *pool, int32_t layer, int32_t num_sessions,
+                                   int32_t num_q_heads, const void *q, const void *k_new,
+                                   const void *v_new, const int32_t *block_tables,
+                                   int32_t max_blocks_per_session, const int32_t *context_lens,
+                                   const int32_t *context_lens_host, float scale, void *out,
+                                   hipStream_t stream);
+
 /*
  * paged_attn_prefill — next-turn (chunked) prefill over reused multi-turn
  * context (§5: reusing LLM-stage KV avoids re-prefilling conversation history;

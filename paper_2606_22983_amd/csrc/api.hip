@@ -55,6 +55,33 @@ ErrorWords error_words() {
 
 unsigned int *device_error_word() { return error_words().word; }
 
+namespace {
+// Split-K scratch of paged_attn_decode_static: a fixed buffer in the
+// library's code object, one per GPU, so that the call allocates nothing.  In
+// host code `scratch` only names the symbol; its device address (different on
+// every GPU) comes from hipGetSymbolAddress with that GPU current.
+constexpr size_t kDecodeScratchBytes = LS_DECODE_STATIC_SCRATCH_BYTES;
+__device__ __align__(256) uint8_t scratch[kDecodeScratchBytes];
+
+// Device address of this GPU's scratch (resolved once per device), or null.
+void *decode_scratch() {
+    static std::mutex mu;
+    static void *addr[64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void *ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess) {
+            (void)hipGetLastError();
+            return nullptr;
+        }
+        addr[dev] = ptr;
+    }
+    return addr[dev];
+}
+}  // namespace
+
 int stream_cus(const PoolGeom &p, hipStream_t stream) {
     const int dev_cus = p.num_cus > 0 ? p.num_cus : 256;
     if (!stream) return dev_cus;
@@ -330,6 +357,26 @@ ls_status paged_attn_decode(ls_kv_pool *pool, int32_t layer, int32_t num_session
                                  block_tables, max_blocks_per_session, context_lens,
                                  scale, static_cast<uint16_t *>(out), workspace, plan, err, stream);
     return e == hipSuccess ? LS_OK : hip_fail(e, "decode launch");
+}
+
+ls_status paged_attn_decode_static(ls_kv_pool *pool, int32_t layer, int32_t num_sessions,
+                                   int32_t num_q_heads, const void *q, const void *k_new,
+                                   const void *v_new, const int32_t *block_tables,
+                                   int32_t max_blocks_per_session, const int32_t *context_lens,
+                                   const int32_t *context_lens_host, float scale, void *out,
+                                   hipStream_t stream) {
+    if (ls_status st = check_pool(pool)) return st;
+    if (num_sessions > 0 && max_blocks_per_session > 0 && num_q_heads > 0) {
+        const size_t need = ls_decode_workspace_bytes(pool, num_sessions, num_q_heads, max_blocks_per_session);
+        if (need > kDecodeScratchBytes)
+            return fail(LS_ENOMEM, "this batch needs %zu bytes of split scratch; the static buffer holds %zu",
+                        need, kDecodeScratchBytes);
+    }
+    void *ws = decode_scratch();
+    if (!ws) return fail(LS_EHIP, "cannot resolve the static decode scratch on this device");
+    return paged_attn_decode(pool, layer, num_sessions, num_q_heads, q, k_new, v_new, block_tables,
+                             max_blocks_per_session, context_lens, context_lens_host, scale, out, ws,
+                             kDecodeScratchBytes, stream);
 }
 
 ls_status paged_attn_prefill(ls_kv_pool *pool, int32_t layer, int32_t num_sessions,

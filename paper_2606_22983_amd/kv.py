@@ -41,6 +41,8 @@ _lib.ls_decode_workspace_bytes.argtypes = [_p, _i32, _i32, _i32]
 _lib.ls_decode_workspace_bytes.restype = _sz
 _lib.paged_attn_decode.argtypes = [_p, _i32, _i32, _i32, _p, _p, _p, _p, _i32, _p, _p, _f32, _p,
                                    _p, _sz, _p]
+_lib.paged_attn_decode_static.argtypes = [_p, _i32, _i32, _i32, _p, _p, _p, _p, _i32, _p, _p, _f32,
+                                          _p, _p]
 _lib.paged_attn_prefill.argtypes = [_p, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _i32, _i32, _p,
                                     _i32, _f32, _p, _p]
 _lib.kv_blocks_stash.argtypes = [_p, _i32, _p, _p, _p, _sz, _i32, _p, _sz, _i32, _p]
@@ -51,6 +53,7 @@ _lib.ls_device_errors.argtypes = [ctypes.POINTER(ctypes.c_uint32)]
 _lib.ls_last_error.restype = ctypes.c_char_p
 _lib.ls_version.restype = ctypes.c_char_p
 for _f in (_lib.kv_pool_create, _lib.kv_pool_destroy, _lib.paged_attn_decode,
+           _lib.paged_attn_decode_static,
            _lib.paged_attn_prefill, _lib.kv_blocks_stash, _lib.kv_blocks_restore,
            _lib.kv_blocks_restore_layers,
            _lib.ls_device_errors):
@@ -207,6 +210,35 @@ def paged_attn_decode(pool: KVPool, layer: int, q: torch.Tensor, block_tables: t
                                   float(scale), _ptr(out), _ptr(workspace), _nbytes(workspace),
                                   _stream(stream)),
            "paged_attn_decode")
+    del keep
+    return out
+
+
+def paged_attn_decode_static(pool: KVPool, layer: int, q: torch.Tensor, block_tables: torch.Tensor,
+                             context_lens: torch.Tensor, scale: float, out: torch.Tensor,
+                             k_new: Optional[torch.Tensor] = None, v_new: Optional[torch.Tensor] = None,
+                             context_lens_host=None, stream=None) -> torch.Tensor:
+    """paged_attn_decode with the library's static split scratch (no workspace)."""
+    if q.dim() != 3:
+        raise ValueError("q must be [S][Hq][D]")
+    s, hq = q.shape[0], q.shape[1]
+    d, hkv = pool.head_dim, pool.num_kv_heads
+    _shape(q, "q", (s, hq, d), _BF16)
+    _shape(out, "out", (s, hq, d), _BF16)
+    _shape(block_tables, "block_tables", (s, None), torch.int32)
+    _shape(context_lens, "context_lens", (s,), torch.int32)
+    for t, name in ((k_new, "k_new"), (v_new, "v_new")):
+        if t is not None:
+            _shape(t, name, (s, hkv, d), _BF16)
+    for t, name in ((q, "q"), (out, "out"), (block_tables, "block_tables"),
+                    (context_lens, "context_lens"), (k_new, "k_new"), (v_new, "v_new")):
+        if t is not None:
+            _dev(t, name)
+    keep, hl = _host_i32(context_lens_host, "context_lens_host", s)
+    _check(_lib.paged_attn_decode_static(pool.handle, layer, s, hq, _ptr(q), _ptr(k_new), _ptr(v_new),
+                                         _ptr(block_tables), block_tables.shape[1], _ptr(context_lens),
+                                         hl, float(scale), _ptr(out), _stream(stream)),
+           "paged_attn_decode_static")
     del keep
     return out
 
