@@ -45,11 +45,15 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--legs", default="decode,prefill,talker,restore,pipeline,kvm,sched")
-    ap.add_argument("--prefill-reps", type=int, default=5)
-    ap.add_argument("--restore-reps", type=int, default=5)
+    ap.add_argument("--reps", type=int, default=60, help="repetitions of the timed unit per leg")
+    ap.add_argument("--prefill-reps", type=int, default=60)
+    ap.add_argument("--restore-reps", type=int, default=50)
     ap.add_argument("--restore-sessions", type=int, default=128)
     ap.add_argument("--host-leg-gib", type=float, default=4.0)
     ap.add_argument("--restore-cus", type=int, default=32)
+    ap.add_argument("--rates", type=lambda v: [float(x) for x in v.split(",")],
+                    default=[50.0, 100.0, 200.0, 250.0, 300.0, 400.0, 800.0, 0.0],
+                    help="payload GB/s caps of the bounded-restore curve (0 = full rate)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     return ap.parse_args()
 
@@ -96,6 +100,25 @@ class Timer:
 
     def mean_ms(self):
         return float(np.mean([a.elapsed_time(b) for a, b in self.pairs]))
+
+    def stats(self, scale=1.0, unit="ms"):
+        """Median, p10, p90 and mean of the recorded pairs (times scale), after a sync."""
+        self.torch.cuda.synchronize()
+        t = np.array([a.elapsed_time(b) for a, b in self.pairs]) * scale
+        return {"unit": unit, "reps": int(t.size), "median": round(float(np.median(t)), 4),
+                "p10": round(float(np.percentile(t, 10)), 4), "p90": round(float(np.percentile(t, 90)), 4),
+                "mean": round(float(t.mean()), 4)}
+
+
+def sample(torch, stream, fn, reps, scale=1.0, unit="ms"):
+    """Time fn() reps times, each in its own event pair on `stream`."""
+    timer = Timer(torch, stream)
+    torch.cuda.synchronize()
+    for i in range(reps):
+        e = timer.start()
+        fn(i)
+        timer.stop(e)
+    return timer.stats(scale, unit)
 
 
 def dev16(torch, a):
@@ -145,15 +168,32 @@ def decode_leg(torch, kv, W, args):
     wall = time.perf_counter() - t0
     assert kv.ls_device_errors() == 0
     kernel_ms = timer.mean_ms() / args.steps
+    # Distribution of single calls (each in its own event pair, pools rotating).
+    per_call = sample(torch, stream, lambda i: kv.paged_attn_decode(pools[i % 3], 0, q, tables, lens_d,
+                                                                   case.scale, out, ws),
+                      args.reps, 1e3, "us")
     res = dict(case=case, pools=pools, copies=copies, q=q, tables=tables, lens=lens_d, out=out,
                ws=ws, alg_bytes=alg_bytes, kv_bytes=kv_bytes, wall_s=wall, kernel_ms=kernel_ms,
-               ms_per_step=wall * 1e3 / args.steps)
-    log("decode: %.1f us/step wall, %.1f us/launch (events), %.0f GB/s" % (
-        res["ms_per_step"] * 1e3, kernel_ms * 1e3, alg_bytes / (kernel_ms * 1e-3) / 1e9))
+               ms_per_step=wall * 1e3 / args.steps, per_call=per_call)
+    log("decode: %.1f us/step wall, %.1f us/launch (events), %.0f GB/s; single calls median %.1f us "
+        "(p10 %.1f, p90 %.1f)" % (res["ms_per_step"] * 1e3, kernel_ms * 1e3,
+                                  alg_bytes / (kernel_ms * 1e-3) / 1e9, per_call["median"],
+                                  per_call["p10"], per_call["p90"]))
     return res
 
 
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(dec, W):
+    import subprocess
     import oracle
     case = dec["case"]
     threads = oracle.num_threads()
@@ -165,11 +205,28 @@ def cpu_baseline(dec, W):
         total += t
         reps += 1
     per = total / reps
-    log("cpu oracle: %.2f s per decode step on %d threads (%d reps)" % (per, threads, reps))
+    # The same full step on one thread, in a child process (OpenMP reads its
+    # thread count at start-up).
+    code = ("import sys, time; sys.path.insert(0, %r); import oracle; "
+            "from paper_2606_22983_amd import workloads as W; c = W.thinker_decode(); "
+            "t0 = time.perf_counter(); oracle.decode(c.pool.data, 16, c.pool.head_dim, 0, c.q[0], "
+            "c.block_tables, c.context_lens, c.scale); print(time.perf_counter() - t0)" % ROOT)
+    env = dict(os.environ, OMP_NUM_THREADS="1")
+    one = None
+    try:
+        r = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True, timeout=120)
+        one = float(r.stdout.strip().splitlines()[-1])
+    except Exception as e:  # reported, not fatal
+        log("cpu oracle, 1 thread: not measured (%s)" % e)
+    model = _cpu_model()
+    log("cpu oracle: %.2f s per decode step on %d threads (%d reps), %s s on 1 thread; %s" % (
+        per, threads, reps, "%.2f" % one if one else "-", model))
     return {"value": round(dec["alg_bytes"] / per / 1e9, 4), "unit": "GB/s", "cores": threads,
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": model,
+            "one_thread": None if one is None else {"seconds_per_step": round(one, 3),
+                                                     "value": round(dec["alg_bytes"] / one / 1e9, 4)},
             "sample": "full thinker-shaped decode step (64 sessions, %d tokens), fp64, %d rep(s), "
-                      "%.2f s each" % (int(case.context_lens.sum()), reps, per)}
+                      "%.2f s each on %d threads" % (int(case.context_lens.sum()), reps, per, threads)}
 
 
 def prefill_leg(torch, kv, W, args):
@@ -189,25 +246,30 @@ def prefill_leg(torch, kv, W, args):
     tables = dev32(torch, case.block_tables)
     out = torch.empty(q.shape, dtype=torch.bfloat16, device="cuda")
     maxn = int(n.max())
-    # The first call appends the turn's K/V; timed calls run attention only.
-    kv.paged_attn_prefill(pool, 0, q, cu, ctx, maxn, tables, case.scale, out, kn, vn)
-    kv.paged_attn_prefill(pool, 0, q, cu, ctx, maxn, tables, case.scale, out)
-    timer = Timer(torch, torch.cuda.current_stream())
+    lens_host = np.stack([n, c], 1)
+    stream = torch.cuda.current_stream()
+    # The timed call is the whole call: the turn's K/V is appended, then
+    # attention runs (the appends rewrite the same slots with the same values).
+    call = lambda i: kv.paged_attn_prefill(pool, 0, q, cu, ctx, maxn, tables, case.scale, out, kn, vn,
+                                           lens_host=lens_host)
+    call(0)
+    call(0)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.prefill_reps):
-        e = timer.start()
-        kv.paged_attn_prefill(pool, 0, q, cu, ctx, maxn, tables, case.scale, out)
-        timer.stop(e)
-    torch.cuda.synchronize()
+    st = sample(torch, stream, call, args.prefill_reps)
     wall = time.perf_counter() - t0
+    attn = sample(torch, stream, lambda i: kv.paged_attn_prefill(pool, 0, q, cu, ctx, maxn, tables,
+                                                                 case.scale, out), 10)
     assert kv.ls_device_errors() == 0
-    ms = timer.mean_ms()
+    ms = st["median"]
     tflops = flops / (ms * 1e-3) / 1e12
-    log("prefill: %.2f ms/launch, %.1f TFLOP/s" % (ms, tflops))
+    log("prefill (append + attention): median %.3f ms (p10 %.3f, p90 %.3f) over %d calls, %.1f TFLOP/s; "
+        "attention alone %.3f ms" % (ms, st["p10"], st["p90"], st["reps"], tflops, attn["median"]))
     return {"workload": "next-turn prefill: 32 sessions, n~U[256,2048] new tokens over "
-                        "c~U[2048,32768] reused context, 32/4 heads, D=128, bf16, fp32 accumulate",
-            "tflop": round(flops / 1e12, 4), "ms_per_launch": round(ms, 4),
+                        "c~U[2048,32768] reused context, 32/4 heads, D=128, bf16, fp32 accumulate; "
+                        "the timed call appends the turn's K/V and attends",
+            "tflop": round(flops / 1e12, 4), "ms_per_launch": round(ms, 4), "call_ms": st,
+            "attention_only_ms": attn,
             "wall_ms_per_launch": round(wall * 1e3 / args.prefill_reps, 4),
             "value": round(tflops, 2), "unit": "TFLOP/s",
             "roofline": {"bound": "mfma", "achieved": round(tflops, 2),
@@ -222,58 +284,51 @@ def talker_leg(torch, kv, W, args):
     step_bytes = [int((case.context_lens.astype(np.int64) + t + 1).sum()) * hkv * d * 4 +
                   2 * S * hkv * d * 2 + 2 * S * hq * d * 2 for t in range(case.steps)]
     total_bytes = float(sum(step_bytes))
-    pool_t = dev16(torch, case.pool.data)
-    pool = kv.kv_pool_create(pool_t, 1, case.pool.num_blocks, hkv, d)
+    # Three pool copies (0.76 GB each); step t runs on copy t % 3, so consecutive
+    # steps cannot be served from the 256 MB Infinity Cache.  Every copy first
+    # receives all 32 appends, so whichever copy a step runs on holds the same
+    # keys (the step's own append rewrites its slot with the same values).
+    base = dev16(torch, case.pool.data)
+    copies = [base] + [base.clone() for _ in range(2)]
+    pools = [kv.kv_pool_create(t, 1, case.pool.num_blocks, hkv, d) for t in copies]
     tables = dev32(torch, case.block_tables)
     qs = [dev16(torch, case.q[t]) for t in range(case.steps)]
     kns = [dev16(torch, case.k_new[t]) for t in range(case.steps)]
     vns = [dev16(torch, case.v_new[t]) for t in range(case.steps)]
     lens = [dev32(torch, case.lens_at(t)) for t in range(case.steps)]
     out = torch.empty((S, hq, d), dtype=torch.bfloat16, device="cuda")
-    ws = torch.zeros(kv.decode_workspace_bytes(pool, S, hq, case.block_tables.shape[1]),
+    ws = torch.zeros(kv.decode_workspace_bytes(pools[0], S, hq, case.block_tables.shape[1]),
                      dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
 
-    def run32():
+    def run32(rot=True, pool_of=None):
         for t in range(case.steps):
-            kv.paged_attn_decode(pool, 0, qs[t], tables, lens[t], case.scale, out, ws, kns[t],
-                                 vns[t])
+            p = pools[t % 3] if rot else pool_of
+            kv.paged_attn_decode(p, 0, qs[t], tables, lens[t], case.scale, out, ws, kns[t], vns[t])
 
-    run32()
-    timer = Timer(torch, torch.cuda.current_stream())
+    for p in pools:
+        run32(False, p)
     torch.cuda.synchronize()
-    reps = 3
     t0 = time.perf_counter()
-    for _ in range(reps):
-        e = timer.start()
-        run32()
-        timer.stop(e)
-    torch.cuda.synchronize()
+    st = sample(torch, stream, lambda i: run32(), args.reps, 1e3 / case.steps, "us per step")
     wall = time.perf_counter() - t0
     assert kv.ls_device_errors() == 0
-    ms32 = timer.mean_ms()
-    gbs = total_bytes / (ms32 * 1e-3) / 1e9
-    # The same 32 steps captured once as a HIP graph and replayed (the appends
-    # rewrite the same slots, so replays are idempotent).
+    us = st["median"]
+    gbs = total_bytes / case.steps / (us * 1e-6) / 1e9
+    # The same 32 steps captured once as a HIP graph and replayed.
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph):
         run32()
     graph.replay()
-    gtimer = Timer(torch, torch.cuda.current_stream())
-    torch.cuda.synchronize()
-    for _ in range(reps):
-        e = gtimer.start()
-        graph.replay()
-        gtimer.stop(e)
-    torch.cuda.synchronize()
+    gst = sample(torch, stream, lambda i: graph.replay(), args.reps, 1e3 / case.steps, "us per step")
     assert kv.ls_device_errors() == 0
-    gms32 = gtimer.mean_ms()
-    log("talker: %.1f us/step eager, %.1f us/step as one graph, %.0f GB/s" % (
-        ms32 * 1e3 / case.steps, gms32 * 1e3 / case.steps, gbs))
+    log("talker: median %.1f us/step eager (p10 %.1f, p90 %.1f), %.1f us/step as one graph, %.0f GB/s" % (
+        us, st["p10"], st["p90"], gst["median"], gbs))
     return {"workload": "talker-shaped decode: 256 sessions, L0~U[512,4096], 16/2 heads, D=128, "
-                        "32 consecutive steps appending one token per session",
-            "us_per_step": round(ms32 * 1e3 / case.steps, 2),
-            "wall_us_per_step": round(wall * 1e6 / (reps * case.steps), 2),
-            "graph_us_per_step": round(gms32 * 1e3 / case.steps, 2),
+                        "32 consecutive steps appending one token per session; 3 pool copies rotate per step",
+            "us_per_step": round(us, 2), "step_us": st,
+            "wall_us_per_step": round(wall * 1e6 / (args.reps * case.steps), 2),
+            "graph_us_per_step": round(gst["median"], 2), "graph_step_us": gst,
             "mb_per_step": round(total_bytes / case.steps / 1e6, 1),
             "value": round(gbs, 1), "unit": "GB/s", "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)}
 
@@ -338,10 +393,10 @@ def restore_leg(torch, kv, W, args, dec):
     kv.kv_blocks_stash(pool, a, staging)
     torch.cuda.synchronize()
     rng = np.random.default_rng(rc.seed)
-    sample = rng.choice(n, size=16, replace=False)
+    sample_ids = rng.choice(n, size=16, replace=False)
     pview = pool_t.view(nl, nb, -1)
     sview = staging.view(n, nl, -1)
-    for i in sample:
+    for i in sample_ids:
         assert torch.equal(sview[i], pview[:, int(rc.stash_ids[i])]), "stash sample %d" % i
 
     def timed(fn, reps):
@@ -353,19 +408,19 @@ def restore_leg(torch, kv, W, args, dec):
         torch.cuda.synchronize()
         return timer.mean_ms()
 
-    stash_ms = timed(lambda: kv.kv_blocks_stash(pool, a, staging), args.restore_reps)
-    restore_ms = timed(lambda: kv.kv_blocks_restore(pool, b, staging), args.restore_reps)
-    for i in sample:
+    stash_st = sample(torch, stream, lambda i: kv.kv_blocks_stash(pool, a, staging), args.restore_reps)
+    restore_st = sample(torch, stream, lambda i: kv.kv_blocks_restore(pool, b, staging), args.restore_reps)
+    stash_ms, restore_ms = stash_st["median"], restore_st["median"]
+    for i in sample_ids:
         assert torch.equal(pview[:, int(rc.restore_ids[i])], sview[i]), "restore sample %d" % i
     assert kv.ls_device_errors() == 0
     scatter_gbs = 2.0 * payload / (restore_ms * 1e-3) / 1e9
     gather_gbs = 2.0 * payload / (stash_ms * 1e-3) / 1e9
-    log("restore scatter: %.2f ms, %.0f GB/s (2N); stash gather: %.2f ms, %.0f GB/s" % (
-        restore_ms, scatter_gbs, stash_ms, gather_gbs))
+    log("restore scatter: median %.2f ms (p10 %.2f, p90 %.2f), %.0f GB/s (2N); stash gather: %.2f ms, "
+        "%.0f GB/s" % (restore_ms, restore_st["p10"], restore_st["p90"], scatter_gbs, stash_ms, gather_gbs))
 
     # restore on a side stream while the thinker decode repeats on the main stream
     side = torch.cuda.Stream()
-    dec_alone_ms = dec["kernel_ms"]
 
     def overlap_decode(start_side, dec_stream=stream, side_stream=side, alone=False):
         n_dec = 0
@@ -379,7 +434,7 @@ def restore_leg(torch, kv, W, args, dec):
             with torch.cuda.stream(side_stream):
                 start_side(side_stream)
         ev_side_end.record(side_stream)
-        while (n_dec < 64 if alone else not ev_side_end.query()) and n_dec < 4000:
+        while (n_dec < 256 if alone else not ev_side_end.query()) and n_dec < 4000:
             e = dtimer.start()
             kv.paged_attn_decode(dec["pools"][n_dec % 3], 0, dec["q"], dec["tables"], dec["lens"],
                                  dec["case"].scale, dec["out"], dec["ws"], stream=dec_stream)
@@ -392,11 +447,34 @@ def restore_leg(torch, kv, W, args, dec):
                 "side_ms": round(ev_side_start.elapsed_time(ev_side_end), 3),
                 "us": round(dtimer.mean_ms() * 1e3, 2) if n_dec else float("nan")}
 
+    # Decode alone, timed the same way (one event pair per call, a sync every
+    # 16 calls): the reference for every slowdown below.
+    dec_alone_ms = overlap_decode(None, alone=True)["us"] * 1e-3
+    log("decode alone, single calls: %.1f us" % (dec_alone_ms * 1e3))
     ov = overlap_decode(lambda st: kv.kv_blocks_restore(pool, b, staging, stream=st))
     n_dec, side_ms, dec_conc_ms = ov["steps"], ov["side_ms"], ov["us"] * 1e-3
     agg = (2.0 * payload + n_dec * dec["alg_bytes"]) / ov["makespan"] / 1e9
     log("overlap: restore %.2f ms on the side stream, %d decode steps at %.1f us (alone %.1f us)" % (
         side_ms, n_dec, dec_conc_ms * 1e3, dec_alone_ms * 1e3))
+
+    # Bounded interference (§5.2: background preloads must not hurt live
+    # requests): the same device-staged restore on a side stream, paced to a
+    # payload rate, beside the thinker decode.  Each point restores a block
+    # count sized to run ~40 ms at its rate.
+    curve = []
+    for gbps in args.rates:
+        nb_b = n if gbps == 0 else int(min(n, max(256, gbps * 1e9 * 0.04 // per_block)))
+        ids_b = b[:nb_b]
+        pt = overlap_decode(lambda st: kv.kv_blocks_restore(pool, ids_b, staging, max_gbps=gbps, stream=st))
+        gbs_b = 2.0 * nb_b * per_block / (pt["side_ms"] * 1e-3) / 1e9
+        curve.append({"max_gbps_payload": gbps, "blocks": nb_b, "restore_ms": pt["side_ms"],
+                      "restore_gbs_2n": round(gbs_b, 1), "decode_steps": pt["steps"],
+                      "decode_us_concurrent": pt["us"],
+                      "decode_slowdown_pct": round(100 * (pt["us"] * 1e-3 / dec_alone_ms - 1), 1)})
+        log("paced restore: cap %s GB/s payload, %.0f GB/s (2N) over %.1f ms, decode %.1f us (+%.1f%%)" % (
+            gbps or "none", gbs_b, pt["side_ms"], pt["us"], curve[-1]["decode_slowdown_pct"]))
+    within = [p for p in curve if p["decode_slowdown_pct"] <= 10.0]
+    best = max(within, key=lambda p: p["restore_gbs_2n"]) if within else None
 
     # The same restore confined to a few CUs (a CU-masked side stream, the
     # knob the paper's preloader would use to bound interference), decode on a
@@ -446,6 +524,19 @@ def restore_leg(torch, kv, W, args, dec):
                         "decode_slowdown_pct": round(100 * (hdec["us"] * 1e-3 / dec_alone_ms - 1), 1)}
         log("host-staged preload overlap: %.2f ms on the side stream, %d decode steps at %.1f us" % (
             hdec["side_ms"], hdec["steps"], hdec["us"]))
+        # The same preload with its ring scatters rate-bounded (to four times the
+        # PCIe rate, so that a chunk's scatter takes a fraction of its transfer):
+        # they share the CUs with decode instead of taking them over.
+        hb_rate = 4 * PCIE_PEAK_GBS
+        hdec_b = overlap_decode(lambda st: kv.kv_blocks_restore(pool, ids_h, hbuf, ring=ring,
+                                                                max_gbps=hb_rate, stream=st))
+        host_overlap["paced_scatter"] = {
+            "max_gbps_payload": hb_rate, "restore_side_stream_ms": hdec_b["side_ms"],
+            "restore_gbs": round(hb * per_block / (hdec_b["side_ms"] * 1e-3) / 1e9, 2),
+            "decode_steps": hdec_b["steps"], "decode_us_concurrent": hdec_b["us"],
+            "decode_slowdown_pct": round(100 * (hdec_b["us"] * 1e-3 / dec_alone_ms - 1), 1)}
+        log("host-staged preload, scatters paced to %.0f GB/s: %.2f ms, decode %.1f us" % (
+            hb_rate, hdec_b["side_ms"], hdec_b["us"]))
         del hbuf
     assert kv.ls_device_errors() == 0
     del pool_t, staging, ring
@@ -456,7 +547,10 @@ def restore_leg(torch, kv, W, args, dec):
             "payload_gib": round(payload / 2 ** 30, 2),
             "restore_ms": round(restore_ms, 3), "value": round(scatter_gbs, 1), "unit": "GB/s",
             "frac_hbm_peak": round(scatter_gbs / HBM_PEAK_GBS, 4),
+            "restore_call_ms": restore_st, "stash_call_ms": stash_st,
             "stash_ms": round(stash_ms, 3), "stash_gbs": round(gather_gbs, 1),
+            "bounded_interference_curve": curve,
+            "fastest_within_10pct_slowdown": best,
             "roofline": {"bound": "hbm", "achieved": round(scatter_gbs, 1), "peak": HBM_PEAK_GBS,
                          "unit": "GB/s", "frac": round(scatter_gbs / HBM_PEAK_GBS, 4),
                          "traffic": measured_traffic("block_copy", source_digest("blockcopy.hip"))},

@@ -226,16 +226,22 @@ ls_status paged_attn_prefill(ls_kv_pool *pool, int32_t layer, int32_t num_sessio
  *                   of staging_bytes >= n x (one block's all-layer slab) bytes
  *                   (LS_ENOMEM otherwise), layout above
  *   ring            with host staging: caller-owned device memory (16-byte aligned)
- *                   that the copy moves through in whole-block chunks: a DMA and a
- *                   copy kernel per chunk, on the caller's stream.  It must hold the
- *                   copied layer range of at least one block (LS_ENOMEM otherwise).
- *                   Two copies that may run at the same time (different streams)
- *                   need different rings.  Ignored (may be NULL) with device staging.
- *   max_workgroups  0: full rate (a persistent grid of four workgroups per CU the
- *                   stream may use).  k > 0: at most k workgroups, which bounds the
- *                   copy's share of the GPU — its HBM traffic and CU slots — when it
- *                   runs beside live decode as background work (§5.2: preloads must
- *                   not interfere with live requests); the copy is then slower.
+ *                   that the copy moves through in whole-block chunks: a DMA engine
+ *                   transfer and a copy kernel per chunk, on the caller's stream.  It
+ *                   must hold the copied layer range of at least one block (LS_ENOMEM
+ *                   otherwise).  Two copies that may run at the same time (different
+ *                   streams) need different rings.  Ignored (may be NULL) with device
+ *                   staging.
+ *   max_gbps        0: full rate (a persistent grid of four 256-thread workgroups per
+ *                   CU the stream may use).  r > 0: a rate-bounded copy of at most r GB/s
+ *                   (10^9 bytes per second) of payload, for background work beside live
+ *                   decode (§5.2: preloads must not interfere with live requests; the
+ *                   KV manager's admission divides bytes by such a rate).  It runs one
+ *                   workgroup per CU, small enough to share the CU with a decode
+ *                   workgroup, each copying a burst of four slabs per window of the
+ *                   GPU's constant-frequency clock (at the window's start, then it
+ *                   sleeps).  A rate above what that grid moves gives its maximum.
+ *                   LS_EINVAL for a negative or NaN rate.
  * Bit-exact byte copies.  n == 0 is a no-op.
  */
 
@@ -244,13 +250,13 @@ ls_status paged_attn_prefill(ls_kv_pool *pool, int32_t layer, int32_t num_sessio
  * into staging (layout above), the HBM-to-DRAM eviction of idle multi-turn KV
  * (§5, §5.1; eviction stays block-level, suffix blocks first — the order is
  * the caller's).  The pool is left unchanged; freeing the ids is the caller's
- * decision once the stream has passed this call.  With host staging each
- * chunk is a gather kernel into the ring, then a device-to-host DMA.
+ * decision once the stream has passed this call.  With host staging and a
+ * ring, each chunk is a gather kernel into the ring, then a device-to-host DMA.
  */
 ls_status kv_blocks_stash(ls_kv_pool *pool, int32_t n, const int32_t *block_ids,
                           const int32_t *block_ids_host, void *staging, size_t staging_bytes,
                           int32_t staging_on_host, void *ring, size_t ring_bytes,
-                          int32_t max_workgroups, hipStream_t stream);
+                          double max_gbps, hipStream_t stream);
 
 /*
  * kv_blocks_restore — reload / speech-triggered preload: copy staging (layout
@@ -259,13 +265,13 @@ ls_status kv_blocks_stash(ls_kv_pool *pool, int32_t n, const int32_t *block_ids,
  * restore cut short by the caller (a cancelled preload) leaves a complete
  * prefix, and restoring the remaining ids afterwards (the synchronous
  * fallback of §5.2) gives the same pool as one full restore.  With host
- * staging each chunk is a host-to-device DMA into the ring, then the scatter
- * kernel.
+ * staging and a ring, each chunk is a host-to-device DMA into the ring, then
+ * the scatter kernel.
  */
 ls_status kv_blocks_restore(ls_kv_pool *pool, int32_t n, const int32_t *block_ids,
                             const int32_t *block_ids_host, const void *staging,
                             size_t staging_bytes, int32_t staging_on_host, void *ring,
-                            size_t ring_bytes, int32_t max_workgroups, hipStream_t stream);
+                            size_t ring_bytes, double max_gbps, hipStream_t stream);
 
 /*
  * kv_blocks_restore_layers — kv_blocks_restore of the layers
@@ -274,16 +280,16 @@ ls_status kv_blocks_restore(ls_kv_pool *pool, int32_t n, const int32_t *block_id
  * layer l is back, while later layers are still being restored (the reload
  * leaves the critical path, §5.2 and §7): the caller restores layer by layer
  * on a copy stream and makes the compute stream wait on an event per layer.
- * With host staging, each chunk is one strided host-to-device copy (the
- * range of every block) into the ring, then the scatter kernel; the ring must
- * hold the range of one block.  LS_EINVAL for a range outside [0, num_layers);
+ * With host staging and a ring, each chunk is one strided host-to-device
+ * copy (the range of every block) into the ring, then the scatter kernel; the
+ * ring must hold the range of one block.  LS_EINVAL for a range outside [0, num_layers);
  * otherwise as kv_blocks_restore.  Restoring every layer range of a set of
  * blocks gives the same pool as one kv_blocks_restore.
  */
 ls_status kv_blocks_restore_layers(ls_kv_pool *pool, int32_t layer_begin, int32_t layer_count, int32_t n,
                                    const int32_t *block_ids, const int32_t *block_ids_host,
                                    const void *staging, size_t staging_bytes, int32_t staging_on_host,
-                                   void *ring, size_t ring_bytes, int32_t max_workgroups,
+                                   void *ring, size_t ring_bytes, double max_gbps,
                                    hipStream_t stream);
 
 /* ------------------------------------------------------------------------

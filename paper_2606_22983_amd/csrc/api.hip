@@ -149,13 +149,14 @@ ls_status check_ids_host(const PoolGeom &p, int32_t n, const int32_t *ids) {
 ls_status copy_blocks(ls_kv_pool *pool, int32_t lb, int32_t lc, int32_t n, const int32_t *block_ids,
                       const int32_t *block_ids_host, void *staging, size_t staging_bytes,
                       int32_t staging_on_host, void *ring_ptr, size_t ring_bytes,
-                      int32_t max_workgroups, bool to_pool, hipStream_t stream) {
+                      double max_gbps, bool to_pool, hipStream_t stream) {
     if (ls_status st = check_pool(pool)) return st;
     const PoolGeom &p = pool->geom;
     if (lb < 0 || lc < 1 || lb > p.num_layers - lc)
         return fail(LS_EINVAL, "layer range [%d, %d + %d) outside [0, %d)", lb, lb, lc, p.num_layers);
     if (n < 0) return fail(LS_EINVAL, "n must be >= 0");
-    if (max_workgroups < 0) return fail(LS_EINVAL, "max_workgroups must be >= 0");
+    if (!(max_gbps >= 0.0) || max_gbps > 1e9)
+        return fail(LS_EINVAL, "max_gbps must be a number >= 0 (got %g)", max_gbps);
     if (n == 0) return LS_OK;
     if (!block_ids || !staging) return fail(LS_EINVAL, "block_ids and staging must not be NULL");
     if (n > p.num_blocks) return fail(LS_EINVAL, "n (%d) exceeds num_blocks", n);
@@ -176,7 +177,7 @@ ls_status copy_blocks(ls_kv_pool *pool, int32_t lb, int32_t lc, int32_t n, const
     if (!err) return fail(LS_EHIP, "cannot resolve the device error word");
     if (!staging_on_host) {
         hipError_t e = launch_block_copy(p, n, block_ids, static_cast<uint8_t *>(staging), lb, lc,
-                                         p.num_layers, lb, to_pool, max_workgroups, err, stream);
+                                         p.num_layers, lb, to_pool, max_gbps, err, stream);
         return e == hipSuccess ? LS_OK : hip_fail(e, "block copy launch");
     }
     // Whole blocks per chunk, in id order, all on the caller's stream.  The
@@ -193,11 +194,11 @@ ls_status copy_blocks(ls_kv_pool *pool, int32_t lb, int32_t lc, int32_t n, const
                     ? hipMemcpyAsync(ring, h, range * (size_t)cnt, hipMemcpyHostToDevice, stream)
                     : hipMemcpy2DAsync(ring, range, h, per_block, range, cnt, hipMemcpyHostToDevice, stream);
             if (e != hipSuccess) return hip_fail(e, "restore host-to-device copy");
-            e = launch_block_copy(p, cnt, block_ids + i0, ring, lb, lc, lc, 0, true, max_workgroups, err,
+            e = launch_block_copy(p, cnt, block_ids + i0, ring, lb, lc, lc, 0, true, max_gbps, err,
                                   stream);
             if (e != hipSuccess) return hip_fail(e, "restore scatter launch");
         } else {
-            e = launch_block_copy(p, cnt, block_ids + i0, ring, lb, lc, lc, 0, false, max_workgroups, err,
+            e = launch_block_copy(p, cnt, block_ids + i0, ring, lb, lc, lc, 0, false, max_gbps, err,
                                   stream);
             if (e != hipSuccess) return hip_fail(e, "stash gather launch");
             e = range == per_block
@@ -292,10 +293,13 @@ ls_status kv_pool_create(const ls_kv_pool_desc *desc, ls_kv_pool **out) {
     if (desc->kv_bytes < need)
         return fail(LS_ENOMEM, "kv_bytes (%zu) is smaller than the layout needs (%zu)",
                     desc->kv_bytes, need);
-    int dev = 0, cus = 0;
+    int dev = 0, cus = 0, wall_khz = 0;
     if (hipGetDevice(&dev) != hipSuccess) dev = -1;
     if (dev >= 0 && hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         cus = 0;
+    if (dev >= 0 && hipDeviceGetAttribute(&wall_khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess)
+        wall_khz = 0;
+    (void)hipGetLastError();
     ls_kv_pool *pool = new (std::nothrow) ls_kv_pool;
     if (!pool) return fail(LS_ENOMEM, "out of host memory");
     pool->geom.num_layers = desc->num_layers;
@@ -305,6 +309,7 @@ ls_status kv_pool_create(const ls_kv_pool_desc *desc, ls_kv_pool **out) {
     pool->geom.base = static_cast<uint16_t *>(desc->kv_base);
     pool->geom.device = dev;
     pool->geom.num_cus = cus;
+    pool->geom.wall_khz = wall_khz;
     *out = pool;
     return LS_OK;
 }
@@ -426,28 +431,28 @@ ls_status paged_attn_prefill(ls_kv_pool *pool, int32_t layer, int32_t num_sessio
 ls_status kv_blocks_stash(ls_kv_pool *pool, int32_t n, const int32_t *block_ids,
                           const int32_t *block_ids_host, void *staging, size_t staging_bytes,
                           int32_t staging_on_host, void *ring, size_t ring_bytes,
-                          int32_t max_workgroups, hipStream_t stream) {
+                          double max_gbps, hipStream_t stream) {
     return copy_blocks(pool, 0, pool ? pool->geom.num_layers : 1, n, block_ids, block_ids_host, staging,
-                       staging_bytes, staging_on_host, ring, ring_bytes, max_workgroups, false, stream);
+                       staging_bytes, staging_on_host, ring, ring_bytes, max_gbps, false, stream);
 }
 
 ls_status kv_blocks_restore(ls_kv_pool *pool, int32_t n, const int32_t *block_ids,
                             const int32_t *block_ids_host, const void *staging,
                             size_t staging_bytes, int32_t staging_on_host, void *ring,
-                            size_t ring_bytes, int32_t max_workgroups, hipStream_t stream) {
+                            size_t ring_bytes, double max_gbps, hipStream_t stream) {
     return copy_blocks(pool, 0, pool ? pool->geom.num_layers : 1, n, block_ids, block_ids_host,
                        const_cast<void *>(staging), staging_bytes, staging_on_host, ring, ring_bytes,
-                       max_workgroups, true, stream);
+                       max_gbps, true, stream);
 }
 
 ls_status kv_blocks_restore_layers(ls_kv_pool *pool, int32_t layer_begin, int32_t layer_count, int32_t n,
                                    const int32_t *block_ids, const int32_t *block_ids_host,
                                    const void *staging, size_t staging_bytes, int32_t staging_on_host,
-                                   void *ring, size_t ring_bytes, int32_t max_workgroups,
+                                   void *ring, size_t ring_bytes, double max_gbps,
                                    hipStream_t stream) {
     return copy_blocks(pool, layer_begin, layer_count, n, block_ids, block_ids_host,
                        const_cast<void *>(staging), staging_bytes, staging_on_host, ring, ring_bytes,
-                       max_workgroups, true, stream);
+                       max_gbps, true, stream);
 }
 
 ls_status ls_device_errors(uint32_t *bits) {

@@ -16,6 +16,17 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kCopyThreads = 256;
 constexpr int kCopyUnroll = 8;      // 16-byte chunks in flight per thread
 constexpr int kCopyWorkgroupsPerCu = 4;   // persistent grid: resident workgroups per CU
+// A rate-bounded copy (a background preload beside live decode) runs one
+// workgroup per CU: with four waves (one per SIMD, 80 registers each) it fits
+// beside a decode workgroup (two waves per SIMD of 208 registers), whereas the
+// full-rate grid holds four workgroups per CU and keeps decode off the CU
+// until it ends.  Each workgroup copies a burst of slabs at the start of each
+// window of the GPU's constant-frequency wall clock (the same boundaries for
+// all), then sleeps until the next window.  Measured beside the thinker decode
+// at 0.5 TB/s (read + write): a steady trickle from single waves slowed the
+// decode by ~28%, one slab per window by 10.4%, four by 7.3%.
+constexpr int kPacedWorkgroupsPerCu = 1;
+constexpr int kPacedSlabsPerWindow = 4;
 
 // Persistent copy: workgroup w copies the (block i, layer) slabs
 // unit = w, w + grid, ... (unit = i * layer_count + (layer - layer_begin)) of
@@ -28,12 +39,41 @@ constexpr int kCopyWorkgroupsPerCu = 4;   // persistent grid: resident workgroup
 // (a full all-layer staging: num_layers and layer_begin; a compact copy of the
 // layer range: layer_count and 0).
 // to_pool: staging -> pool (restore); otherwise pool -> staging (stash).
-__global__ __launch_bounds__(kCopyThreads) void block_copy_kernel(
+// ticks_per_unit > 0 (paced copies): a workgroup starts its slabs at the
+// boundaries of the global clock windows of ticks_per_unit ticks, at most
+// kPacedSlabsPerWindow per window (a workgroup that falls behind waits for the
+// next boundary instead of catching up).  The first burst waits at least one whole window,
+// so that a copy of any size stays within its rate.  Every wait ends: the
+// clock only moves forward.
+template <int kThreads>
+__global__ __launch_bounds__(kThreads) void block_copy_kernel(
     uint8_t *__restrict__ pool, const int32_t *__restrict__ ids, uint8_t *__restrict__ staging,
     int64_t num_blocks, int32_t layer_begin, int32_t layer_count, int32_t stage_block_slabs,
-    int32_t stage_layer0, int64_t slab_bytes, int64_t units, int32_t to_pool, unsigned int *err) {
+    int32_t stage_layer0, int64_t slab_bytes, int64_t units, int32_t to_pool, unsigned int *err,
+    uint64_t ticks_per_unit) {
     const int64_t chunks = slab_bytes / 16;
+    uint64_t next = 0;
+    int burst = 0;
+    if (ticks_per_unit) {
+        const uint64_t now = __builtin_amdgcn_s_memrealtime();
+        next = (now / ticks_per_unit + 2) * ticks_per_unit;
+    }
     for (int64_t unit = blockIdx.x; unit < units; unit += gridDim.x) {
+        if (ticks_per_unit) {
+            // Long sleeps while the boundary is far (s_sleep 127 is ~8k cycles,
+            // a few microseconds; the clock ticks every ~10 ns), short ones near it.
+            uint64_t now = __builtin_amdgcn_s_memrealtime();
+            while ((int64_t)(now - next) < 0) {
+                if (next - now > 512) __builtin_amdgcn_s_sleep(127);
+                else __builtin_amdgcn_s_sleep(2);
+                now = __builtin_amdgcn_s_memrealtime();
+            }
+            if (++burst == kPacedSlabsPerWindow) {
+                burst = 0;
+                next += ticks_per_unit;
+                if ((int64_t)(now - next) >= 0) next = (now / ticks_per_unit + 1) * ticks_per_unit;
+            }
+        }
         const int64_t i = unit / layer_count;
         const int32_t lr = (int32_t)(unit - i * layer_count);
         const int32_t layer = layer_begin + lr;
@@ -47,16 +87,16 @@ __global__ __launch_bounds__(kCopyThreads) void block_copy_kernel(
             staging + (i * stage_block_slabs + stage_layer0 + lr) * slab_bytes);
         const u32x4 *src = to_pool ? stage_slab : pool_slab;
         u32x4 *dst = to_pool ? pool_slab : stage_slab;
-        for (int64_t base = threadIdx.x; base < chunks; base += (int64_t)kCopyThreads * kCopyUnroll) {
+        for (int64_t base = threadIdx.x; base < chunks; base += (int64_t)kThreads * kCopyUnroll) {
             u32x4 v[kCopyUnroll];
 #pragma unroll
             for (int u = 0; u < kCopyUnroll; ++u) {
-                const int64_t c = base + (int64_t)u * kCopyThreads;
+                const int64_t c = base + (int64_t)u * kThreads;
                 if (c < chunks) v[u] = __builtin_nontemporal_load(src + c);
             }
 #pragma unroll
             for (int u = 0; u < kCopyUnroll; ++u) {
-                const int64_t c = base + (int64_t)u * kCopyThreads;
+                const int64_t c = base + (int64_t)u * kThreads;
                 if (c < chunks) __builtin_nontemporal_store(v[u], dst + c);
             }
         }
@@ -67,16 +107,24 @@ __global__ __launch_bounds__(kCopyThreads) void block_copy_kernel(
 
 hipError_t launch_block_copy(const PoolGeom &p, int32_t n, const int32_t *ids, uint8_t *staging,
                              int32_t layer_begin, int32_t layer_count, int32_t stage_block_slabs,
-                             int32_t stage_layer0, bool to_pool, int32_t max_workgroups,
+                             int32_t stage_layer0, bool to_pool, double max_gbps,
                              unsigned int *err, hipStream_t stream) {
     if (n <= 0 || layer_count <= 0) return hipSuccess;
     const int64_t units = (int64_t)n * layer_count;
-    int64_t grid = std::min<int64_t>(units, (int64_t)kCopyWorkgroupsPerCu * stream_cus(p, stream));
-    if (max_workgroups > 0) grid = std::min<int64_t>(grid, max_workgroups);
-    hipLaunchKernelGGL(block_copy_kernel, dim3((unsigned)grid), dim3(kCopyThreads), 0, stream,
+    const int64_t slab = (int64_t)p.slab_bytes();
+    const int64_t per_cu = max_gbps > 0.0 ? kPacedWorkgroupsPerCu : kCopyWorkgroupsPerCu;
+    const int64_t grid = std::min<int64_t>(units, per_cu * stream_cus(p, stream));
+    uint64_t ticks = 0;
+    if (max_gbps > 0.0) {
+        // grid slabs per window: the window lasts slab * grid / rate (the wall
+        // clock ticks wall_khz thousand times a second).
+        const double khz = p.wall_khz > 0 ? (double)p.wall_khz : 100000.0;
+        const double secs = (double)slab * kPacedSlabsPerWindow * (double)grid / (max_gbps * 1e9);
+        ticks = std::max<uint64_t>(1, (uint64_t)(secs * khz * 1e3));
+    }
+    hipLaunchKernelGGL(block_copy_kernel<kCopyThreads>, dim3((unsigned)grid), dim3(kCopyThreads), 0, stream,
                        reinterpret_cast<uint8_t *>(p.base), ids, staging, p.num_blocks, layer_begin,
-                       layer_count, stage_block_slabs, stage_layer0, (int64_t)p.slab_bytes(), units,
-                       to_pool ? 1 : 0, err);
+                       layer_count, stage_block_slabs, stage_layer0, slab, units, to_pool ? 1 : 0, err, ticks);
     return hipGetLastError();
 }
 

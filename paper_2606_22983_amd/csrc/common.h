@@ -22,6 +22,7 @@ struct PoolGeom {
     uint16_t *base;                 // bf16 bit patterns
     int device;
     int num_cus;                    // compute units of that device (0 if unknown)
+    int wall_khz;                   // frequency of its constant wall clock (0 if unknown)
 
     // Elements of one (kv, head) tile and of one (layer, block) slab.
     int64_t tile_elems() const { return (int64_t)kBlock * head_dim; }
@@ -59,10 +60,10 @@ DecodePlan plan_decode(const PoolGeom &p, int32_t num_sessions, int32_t num_q_he
 // Copies the slabs of layers [layer_begin, layer_begin + layer_count) of blocks
 // ids[0..n): staging block i holds stage_block_slabs slabs, layer_begin's is
 // its stage_layer0-th.
-// max_workgroups > 0 caps the persistent grid (a bounded-interference copy).
+// max_gbps > 0: a paced copy of at most that many GB/s of payload.
 hipError_t launch_block_copy(const PoolGeom &p, int32_t n, const int32_t *ids, uint8_t *staging,
                              int32_t layer_begin, int32_t layer_count, int32_t stage_block_slabs,
-                             int32_t stage_layer0, bool to_pool, int32_t max_workgroups,
+                             int32_t stage_layer0, bool to_pool, double max_gbps,
                              unsigned int *err, hipStream_t stream);
 hipError_t launch_append_prefill(const PoolGeom &p, int layer, int32_t num_sessions,
                                  int32_t total_tokens, const uint16_t *k_new,

@@ -45,10 +45,11 @@ _lib.paged_attn_decode_static.argtypes = [_p, _i32, _i32, _i32, _p, _p, _p, _p, 
                                           _p, _p]
 _lib.paged_attn_prefill.argtypes = [_p, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _i32, _i32, _p,
                                     _i32, _f32, _p, _p]
-_lib.kv_blocks_stash.argtypes = [_p, _i32, _p, _p, _p, _sz, _i32, _p, _sz, _i32, _p]
-_lib.kv_blocks_restore.argtypes = [_p, _i32, _p, _p, _p, _sz, _i32, _p, _sz, _i32, _p]
+_f64 = ctypes.c_double
+_lib.kv_blocks_stash.argtypes = [_p, _i32, _p, _p, _p, _sz, _i32, _p, _sz, _f64, _p]
+_lib.kv_blocks_restore.argtypes = [_p, _i32, _p, _p, _p, _sz, _i32, _p, _sz, _f64, _p]
 _lib.kv_blocks_restore_layers.argtypes = [_p, _i32, _i32, _i32, _p, _p, _p, _sz, _i32, _p, _sz,
-                                          _i32, _p]
+                                          _f64, _p]
 _lib.ls_device_errors.argtypes = [ctypes.POINTER(ctypes.c_uint32)]
 _lib.ls_last_error.restype = ctypes.c_char_p
 _lib.ls_version.restype = ctypes.c_char_p
@@ -286,7 +287,7 @@ def _host_ids(ids):
     return arr, ctypes.c_void_p(arr.ctypes.data)
 
 
-def _copy_args(pool: KVPool, block_ids: torch.Tensor, staging: torch.Tensor, ring, max_workgroups):
+def _copy_args(pool: KVPool, block_ids: torch.Tensor, staging: torch.Tensor, ring, max_gbps):
     """Checks shared by the block copies; returns (on_host, ring pointer, ring bytes)."""
     _shape(block_ids, "block_ids", (None,), torch.int32)
     if not staging.is_contiguous():
@@ -294,8 +295,8 @@ def _copy_args(pool: KVPool, block_ids: torch.Tensor, staging: torch.Tensor, rin
     if _nbytes(staging) < block_ids.numel() * pool.block_bytes:
         raise ValueError("staging holds %d bytes; %d blocks need %d" % (
             _nbytes(staging), block_ids.numel(), block_ids.numel() * pool.block_bytes))
-    if max_workgroups < 0:
-        raise ValueError("max_workgroups must be >= 0")
+    if not max_gbps >= 0:
+        raise ValueError("max_gbps must be >= 0")
     _dev(block_ids, "block_ids")
     on_host = not staging.is_cuda
     if on_host and not staging.is_pinned():
@@ -307,13 +308,13 @@ def _copy_args(pool: KVPool, block_ids: torch.Tensor, staging: torch.Tensor, rin
 
 def kv_blocks_stash(pool: KVPool, block_ids: torch.Tensor, staging: torch.Tensor,
                     block_ids_host=None, ring: Optional[torch.Tensor] = None,
-                    max_workgroups: int = 0, stream=None) -> torch.Tensor:
+                    max_gbps: float = 0.0, stream=None) -> torch.Tensor:
     """Copy every layer's slab of ``block_ids`` into ``staging`` (device, or pinned host
-    through the device ``ring``)."""
-    on_host, rp, rb = _copy_args(pool, block_ids, staging, ring, max_workgroups)
+    through the device ``ring``); ``max_gbps`` > 0 paces it to that payload rate."""
+    on_host, rp, rb = _copy_args(pool, block_ids, staging, ring, max_gbps)
     keep, hp = _host_ids(block_ids_host)
     _check(_lib.kv_blocks_stash(pool.handle, block_ids.numel(), _ptr(block_ids), hp, _ptr(staging),
-                                _nbytes(staging), 1 if on_host else 0, rp, rb, max_workgroups,
+                                _nbytes(staging), 1 if on_host else 0, rp, rb, max_gbps,
                                 _stream(stream)),
            "kv_blocks_stash")
     del keep
@@ -322,29 +323,29 @@ def kv_blocks_stash(pool: KVPool, block_ids: torch.Tensor, staging: torch.Tensor
 
 def kv_blocks_restore(pool: KVPool, block_ids: torch.Tensor, staging: torch.Tensor,
                       block_ids_host=None, ring: Optional[torch.Tensor] = None,
-                      max_workgroups: int = 0, stream=None):
+                      max_gbps: float = 0.0, stream=None):
     """Copy ``staging`` (device, or pinned host through the device ``ring``) back into
     pool blocks ``block_ids``."""
-    on_host, rp, rb = _copy_args(pool, block_ids, staging, ring, max_workgroups)
+    on_host, rp, rb = _copy_args(pool, block_ids, staging, ring, max_gbps)
     keep, hp = _host_ids(block_ids_host)
     _check(_lib.kv_blocks_restore(pool.handle, block_ids.numel(), _ptr(block_ids), hp,
                                   _ptr(staging), _nbytes(staging), 1 if on_host else 0, rp, rb,
-                                  max_workgroups, _stream(stream)),
+                                  max_gbps, _stream(stream)),
            "kv_blocks_restore")
     del keep
 
 
 def kv_blocks_restore_layers(pool: KVPool, layer_begin: int, layer_count: int, block_ids: torch.Tensor,
                              staging: torch.Tensor, block_ids_host=None,
-                             ring: Optional[torch.Tensor] = None, max_workgroups: int = 0,
+                             ring: Optional[torch.Tensor] = None, max_gbps: float = 0.0,
                              stream=None):
     """Restore layers [layer_begin, layer_begin + layer_count) of ``block_ids`` from an
     all-layer ``staging`` (device, or pinned host through the device ``ring``)."""
-    on_host, rp, rb = _copy_args(pool, block_ids, staging, ring, max_workgroups)
+    on_host, rp, rb = _copy_args(pool, block_ids, staging, ring, max_gbps)
     keep, hp = _host_ids(block_ids_host)
     _check(_lib.kv_blocks_restore_layers(pool.handle, layer_begin, layer_count, block_ids.numel(),
                                          _ptr(block_ids), hp, _ptr(staging), _nbytes(staging),
-                                         1 if on_host else 0, rp, rb, max_workgroups,
+                                         1 if on_host else 0, rp, rb, max_gbps,
                                          _stream(stream)), "kv_blocks_restore_layers")
     del keep
 

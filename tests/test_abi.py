@@ -184,12 +184,12 @@ BLOCK = 2 * 2 * 4 * 16 * 128 * 2        # all-layer bytes of one block of the te
 
 
 def _copy(lib, fn, pool, n, ids=F, ids_host=None, staging=F, staging_bytes=None, on_host=0,
-          ring=None, ring_bytes=0, budget=0):
+          ring=None, ring_bytes=0, rate=0.0):
     if staging_bytes is None:
         staging_bytes = max(n, 0) * BLOCK
     return getattr(lib, fn)(pool, n, ctypes.c_void_p(ids), ids_host, ctypes.c_void_p(staging),
                             ctypes.c_size_t(staging_bytes), on_host, ctypes.c_void_p(ring),
-                            ctypes.c_size_t(ring_bytes), budget, None)
+                            ctypes.c_size_t(ring_bytes), ctypes.c_double(rate), None)
 
 
 @pytest.mark.parametrize("fn", ["kv_blocks_restore", "kv_blocks_stash"])
@@ -208,9 +208,10 @@ def test_copy_rejects_bad_host_ids(lib, pool, fn, ids, status):
     (dict(on_host=1, ring=F, ring_bytes=BLOCK - 16), LS_ENOMEM, b"ring"),    # ring below one block
     (dict(on_host=1, ring=F + 8, ring_bytes=BLOCK), LS_EINVAL, b"aligned"),
     (dict(staging_bytes=2 * BLOCK - 1), LS_ENOMEM, b"staging_bytes"),       # staging short of 2 blocks
-    (dict(budget=-1), LS_EINVAL, b"max_workgroups"),
+    (dict(rate=-1.0), LS_EINVAL, b"max_gbps"),
+    (dict(rate=float("nan")), LS_EINVAL, b"max_gbps"),
 ])
-def test_copy_rejects_staging_ring_and_budget(lib, pool, fn, kw, status, word):
+def test_copy_rejects_staging_ring_and_rate(lib, pool, fn, kw, status, word):
     arr = (ctypes.c_int32 * 2)(1, 2)
     assert _copy(lib, fn, pool, 2, ids_host=arr, **kw) == status
     assert word in lib.ls_last_error()
@@ -223,7 +224,7 @@ def test_restore_layers_checks_range_and_staging(lib, pool):
     def call(lb, lc, staging_bytes=2 * BLOCK, on_host=0, ring_bytes=0):
         return L(pool, lb, lc, 2, ctypes.c_void_p(F), arr, ctypes.c_void_p(F),
                  ctypes.c_size_t(staging_bytes), on_host, ctypes.c_void_p(F),
-                 ctypes.c_size_t(ring_bytes), 0, None)
+                 ctypes.c_size_t(ring_bytes), ctypes.c_double(0.0), None)
     assert call(1, 2) == LS_EINVAL                   # layers [1, 3) of 2
     assert call(-1, 1) == LS_EINVAL
     assert call(1, 1, staging_bytes=2 * BLOCK - 2) == LS_ENOMEM   # all-layer stride even for one layer
@@ -296,6 +297,5 @@ def test_binding_copy_checks_staging_size(built_lib, binding):
     pool = _fake_pool(kv, nl=2)
     with pytest.raises(ValueError, match="staging"):
         kv.kv_blocks_restore(pool, _i32(3), _bf(3 * pool.block_bytes // 2 - 1))
-    with pytest.raises(ValueError, match="max_workgroups"):
-        kv.kv_blocks_stash(pool, _i32(3), _bf(3 * pool.block_bytes // 2),
-                           max_workgroups=-2)
+    with pytest.raises(ValueError, match="max_gbps"):
+        kv.kv_blocks_stash(pool, _i32(3), _bf(3 * pool.block_bytes // 2), max_gbps=-2.0)

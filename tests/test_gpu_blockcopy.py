@@ -207,22 +207,33 @@ def test_host_staged_stash_and_restore_on_two_streams(kv, oracle_lib):
     assert kv.ls_device_errors() == 0
 
 
-@pytest.mark.parametrize("budget", [1, 3, 64])
-def test_budgeted_copies_are_bit_exact(kv, oracle_lib, budget):
-    """A bounded-interference copy (at most `budget` workgroups) moves the same bytes."""
-    rng = np.random.default_rng(60 + budget)
+@pytest.mark.parametrize("gbps", [0.5, 40.0, 1e6])
+def test_rate_bounded_copies_are_bit_exact(kv, oracle_lib, gbps):
+    """A rate-bounded copy (full-rate bursts at clock-window boundaries) moves the
+    same bytes; at 0.5 GB/s the 11 MB stash takes at least ~20 ms, at 40 GB/s at
+    least ~0.3 ms."""
+    rng = np.random.default_rng(60 + int(gbps) % 97)
     nl, hkv, d, nb, n = 5, 4, 128, 90, 70
     pool = _random_pool(rng, nl, nb, hkv, d)
     ids = rng.permutation(nb)[:n].astype(np.int32)
     dp = DevicePool(kv, pool, d, ring_blocks=4)
     st = torch.empty((n, nl, 2, hkv, 16 * d), dtype=torch.int16, device="cuda")
-    kv.kv_blocks_stash(dp.pool, i32_dev(ids), st, max_workgroups=budget)
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    kv.kv_blocks_stash(dp.pool, i32_dev(ids), st, max_gbps=gbps)
+    t1.record()
     assert np.array_equal(host_bits(st), oracle_lib.stash(pool, 16, d, ids))
+    ms = t0.elapsed_time(t1)
+    payload = n * nl * 2 * hkv * 16 * d * 2
+    log("stash of %.1f MB at a %.1f GB/s cap: %.3f ms (%.1f GB/s)" % (payload / 1e6, gbps, ms,
+                                                                       payload / ms / 1e6))
+    if gbps < 100:
+        assert payload / (ms * 1e-3) <= 1.15 * gbps * 1e9, "the copy ran faster than its cap"
     fresh = _random_pool(rng, n, nl, hkv, d).reshape(n, nl, 2, hkv, 16 * d)
     host = torch.from_numpy(fresh.view(np.int16)).pin_memory()
     ids2 = rng.permutation(nb)[:n].astype(np.int32)
-    kv.kv_blocks_restore(dp.pool, i32_dev(ids2), host, block_ids_host=ids2, ring=dp.ring,
-                         max_workgroups=budget)
+    kv.kv_blocks_restore(dp.pool, i32_dev(ids2), host, block_ids_host=ids2, ring=dp.ring, max_gbps=gbps)
     assert np.array_equal(dp.host(), oracle_lib.restore(pool.copy(), 16, d, ids2, fresh))
     assert kv.ls_device_errors() == 0
 
@@ -260,3 +271,4 @@ def test_restore_at_preload_geometry_10k_blocks(kv, oracle_lib):
     got = data.cpu().numpy().view(np.uint16).reshape(expect.shape)
     assert np.array_equal(got, expect)
     assert kv.ls_device_errors() == 0
+
