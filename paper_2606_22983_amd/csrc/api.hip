@@ -415,7 +415,7 @@ ls_status paged_attn_prefill(ls_kv_pool *pool, int32_t layer, int32_t num_sessio
     unsigned int *err = device_error_word();
     if (!err) return fail(LS_EHIP, "cannot resolve the device error word");
     if (k_new) {
-        hipError_t e = launch_append_prefill(p, layer, num_sessions, total_new_tokens,
+        hipError_t e = launch_append_prefill(p, layer, num_sessions, total_new_tokens, max_new_len,
                                              static_cast<const uint16_t *>(k_new),
                                              static_cast<const uint16_t *>(v_new), cu_new_lens,
                                              reused_lens, block_tables, max_blocks_per_session, err,
@@ -423,7 +423,7 @@ ls_status paged_attn_prefill(ls_kv_pool *pool, int32_t layer, int32_t num_sessio
         if (e != hipSuccess) return hip_fail(e, "append launch");
     }
     hipError_t e = launch_prefill(p, layer, num_sessions, num_q_heads, static_cast<const uint16_t *>(q),
-                                  cu_new_lens, reused_lens, max_new_len, block_tables,
+                                  cu_new_lens, reused_lens, total_new_tokens, max_new_len, block_tables,
                                   max_blocks_per_session, scale, static_cast<uint16_t *>(out), err, stream);
     return e == hipSuccess ? LS_OK : hip_fail(e, "prefill launch");
 }

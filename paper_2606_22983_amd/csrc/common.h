@@ -65,11 +65,11 @@ hipError_t launch_block_copy(const PoolGeom &p, int32_t n, const int32_t *ids, u
                              int32_t layer_begin, int32_t layer_count, int32_t stage_block_slabs,
                              int32_t stage_layer0, bool to_pool, double max_gbps,
                              unsigned int *err, hipStream_t stream);
-hipError_t launch_append_prefill(const PoolGeom &p, int layer, int32_t num_sessions,
-                                 int32_t total_tokens, const uint16_t *k_new,
-                                 const uint16_t *v_new, const int32_t *cu_new_lens,
-                                 const int32_t *reused_lens, const int32_t *block_tables,
-                                 int32_t max_blocks, unsigned int *err, hipStream_t stream);
+hipError_t launch_append_prefill(const PoolGeom &p, int layer, int32_t num_sessions, int32_t total_tokens,
+                                 int32_t max_new_len, const uint16_t *k_new, const uint16_t *v_new,
+                                 const int32_t *cu_new_lens, const int32_t *reused_lens,
+                                 const int32_t *block_tables, int32_t max_blocks, unsigned int *err,
+                                 hipStream_t stream);
 // With k_new / v_new (both non-null) the step's own token is attended from
 // them and written to its pool slot by the decode kernel itself.
 hipError_t launch_decode(const PoolGeom &p, int layer, int32_t num_sessions, int32_t num_q_heads,
@@ -80,7 +80,7 @@ hipError_t launch_decode(const PoolGeom &p, int layer, int32_t num_sessions, int
                          unsigned int *err, hipStream_t stream);
 hipError_t launch_prefill(const PoolGeom &p, int layer, int32_t num_sessions, int32_t num_q_heads,
                           const uint16_t *q, const int32_t *cu_new_lens,
-                          const int32_t *reused_lens, int32_t max_new_len,
+                          const int32_t *reused_lens, int32_t total_tokens, int32_t max_new_len,
                           const int32_t *block_tables, int32_t max_blocks, float scale,
                           uint16_t *out, unsigned int *err, hipStream_t stream);
 

@@ -72,6 +72,7 @@ struct PrefillArgs {
     int32_t group;
     int32_t num_sessions;
     int32_t qtiles;                // query tiles of the longest turn
+    int32_t total;                 // new tokens of the call (rows of q and out)
     const uint16_t *q;             // [T][Hq][D]
     uint16_t *out;                 // [T][Hq][D]
     const int32_t *cu;             // [S+1]
@@ -229,7 +230,8 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     if (blockIdx.x == 0)
         for (int sp = tid; sp < S; sp += kPreThreads) {
             const int nt = a.cu[sp + 1] - a.cu[sp];
-            if (nt < 0 || nt > QT * qtok || a.ctx[sp] < 0) flag_error(a.err, LS_DEVERR_LENGTH);
+            if (nt < 0 || nt > QT * qtok || a.ctx[sp] < 0 || a.cu[sp] < 0 || a.cu[sp + 1] > a.total)
+                flag_error(a.err, LS_DEVERR_LENGTH);
         }
     int s, g, qt;
     if (P <= kMaxPairs) {
@@ -282,7 +284,7 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
 
     const int n = a.cu[s + 1] - a.cu[s];
     const int j0 = qt * qtok;
-    if (j0 >= n) return;
+    if (j0 >= n || a.cu[s] < 0 || a.cu[s + 1] > a.total) return;   // (lengths outside q: flagged above)
     const int c = a.ctx[s];
     const int j_last = min(j0 + qtok, n) - 1;
     const int kv_len = c + n;
@@ -655,7 +657,7 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
 
 hipError_t launch_prefill(const PoolGeom &p, int layer, int32_t num_sessions, int32_t num_q_heads,
                           const uint16_t *q, const int32_t *cu_new_lens,
-                          const int32_t *reused_lens, int32_t max_new_len,
+                          const int32_t *reused_lens, int32_t total_tokens, int32_t max_new_len,
                           const int32_t *block_tables, int32_t max_blocks, float scale,
                           uint16_t *out, unsigned int *err, hipStream_t stream) {
     if (num_sessions <= 0 || max_new_len <= 0) return hipSuccess;
@@ -665,6 +667,7 @@ hipError_t launch_prefill(const PoolGeom &p, int layer, int32_t num_sessions, in
     a.num_kv_heads = p.num_kv_heads;
     a.group = num_q_heads / p.num_kv_heads;
     a.num_sessions = num_sessions;
+    a.total = total_tokens;
     a.q = q;
     a.out = out;
     a.cu = cu_new_lens;
