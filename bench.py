@@ -172,9 +172,27 @@ def decode_leg(torch, kv, W, args):
     per_call = sample(torch, stream, lambda i: kv.paged_attn_decode(pools[i % 3], 0, q, tables, lens_d,
                                                                    case.scale, out, ws),
                       args.reps, 1e3, "us")
+    # The same calls with the lengths also given on the host (the schedule is
+    # then planned on the host when that is estimated to be faster).
+    lens_h = case.context_lens.astype(np.int32)
+    hcall = lambda i: kv.paged_attn_decode(pools[i % 3], 0, q, tables, lens_d, case.scale, out, ws,
+                                           context_lens_host=lens_h)
+    for i in range(args.warmup):
+        hcall(i)
+    htimer = Timer(torch, stream)
+    torch.cuda.synchronize()
+    e = htimer.start()
+    for i in range(args.steps):
+        hcall(i)
+    htimer.stop(e)
+    torch.cuda.synchronize()
+    assert kv.ls_device_errors() == 0
+    host_ms = htimer.mean_ms() / args.steps
     res = dict(case=case, pools=pools, copies=copies, q=q, tables=tables, lens=lens_d, out=out,
                ws=ws, alg_bytes=alg_bytes, kv_bytes=kv_bytes, wall_s=wall, kernel_ms=kernel_ms,
-               ms_per_step=wall * 1e3 / args.steps, per_call=per_call)
+               ms_per_step=wall * 1e3 / args.steps, per_call=per_call, host_lens_ms=host_ms)
+    log("decode with host lengths: %.1f us/launch (events), %.0f GB/s" % (
+        host_ms * 1e3, alg_bytes / (host_ms * 1e-3) / 1e9))
     log("decode: %.1f us/step wall, %.1f us/launch (events), %.0f GB/s; single calls median %.1f us "
         "(p10 %.1f, p90 %.1f)" % (res["ms_per_step"] * 1e3, kernel_ms * 1e3,
                                   alg_bytes / (kernel_ms * 1e-3) / 1e9, per_call["median"],
@@ -301,10 +319,13 @@ def talker_leg(torch, kv, W, args):
                      dtype=torch.uint8, device="cuda")
     stream = torch.cuda.current_stream()
 
-    def run32(rot=True, pool_of=None):
+    lens_h = [case.lens_at(t).astype(np.int32) for t in range(case.steps)]
+
+    def run32(rot=True, pool_of=None, host=False):
         for t in range(case.steps):
             p = pools[t % 3] if rot else pool_of
-            kv.paged_attn_decode(p, 0, qs[t], tables, lens[t], case.scale, out, ws, kns[t], vns[t])
+            kv.paged_attn_decode(p, 0, qs[t], tables, lens[t], case.scale, out, ws, kns[t], vns[t],
+                                 context_lens_host=lens_h[t] if host else None)
 
     for p in pools:
         run32(False, p)
@@ -322,13 +343,26 @@ def talker_leg(torch, kv, W, args):
     graph.replay()
     gst = sample(torch, stream, lambda i: graph.replay(), args.reps, 1e3 / case.steps, "us per step")
     assert kv.ls_device_errors() == 0
-    log("talker: median %.1f us/step eager (p10 %.1f, p90 %.1f), %.1f us/step as one graph, %.0f GB/s" % (
-        us, st["p10"], st["p90"], gst["median"], gbs))
+    # With the lengths also on the host: the schedule is planned there.
+    hst = sample(torch, stream, lambda i: run32(host=True), args.reps, 1e3 / case.steps, "us per step")
+    hgraph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(hgraph):
+        run32(host=True)
+    hgraph.replay()
+    hgst = sample(torch, stream, lambda i: hgraph.replay(), args.reps, 1e3 / case.steps, "us per step")
+    assert kv.ls_device_errors() == 0
+    hgbs = total_bytes / case.steps / (hst["median"] * 1e-6) / 1e9
+    log("talker: median %.1f us/step eager (p10 %.1f, p90 %.1f), %.1f us/step as one graph, %.0f GB/s; "
+        "host lengths %.1f us/step eager, %.1f as one graph, %.0f GB/s" % (
+            us, st["p10"], st["p90"], gst["median"], gbs, hst["median"], hgst["median"], hgbs))
     return {"workload": "talker-shaped decode: 256 sessions, L0~U[512,4096], 16/2 heads, D=128, "
                         "32 consecutive steps appending one token per session; 3 pool copies rotate per step",
             "us_per_step": round(us, 2), "step_us": st,
             "wall_us_per_step": round(wall * 1e6 / (args.reps * case.steps), 2),
             "graph_us_per_step": round(gst["median"], 2), "graph_step_us": gst,
+            "host_lengths": {"us_per_step": round(hst["median"], 2), "step_us": hst,
+                             "graph_us_per_step": round(hgst["median"], 2), "graph_step_us": hgst,
+                             "value": round(hgbs, 1), "frac_hbm_peak": round(hgbs / HBM_PEAK_GBS, 4)},
             "mb_per_step": round(total_bytes / case.steps / 1e6, 1),
             "value": round(gbs, 1), "unit": "GB/s", "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)}
 

@@ -158,6 +158,20 @@ ls_status paged_attn_decode(ls_kv_pool *pool, int32_t layer, int32_t num_session
                             const int32_t *context_lens_host, float scale, void *out,
                             void *workspace, size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * ls_decode_schedule — how paged_attn_decode will run a batch of this shape
+ * on `stream`: *split_tokens tokens per split, *host_planned 1 when the
+ * schedule is planned on the host from context_lens_host (0: in the kernel,
+ * also when the host plan is estimated to be no faster or does not fit the
+ * argument block), *merge 1 when the split merge kernel runs.  appended: 1
+ * when k_new / v_new will be given.  Pure host computation; LS_EINVAL as for
+ * paged_attn_decode.
+ */
+ls_status ls_decode_schedule(const ls_kv_pool *pool, int32_t num_sessions, int32_t num_q_heads,
+                             int32_t max_blocks_per_session, const int32_t *context_lens_host,
+                             int32_t appended, hipStream_t stream, int32_t *split_tokens,
+                             int32_t *host_planned, int32_t *merge);
+
 /* Bytes of the static split scratch behind paged_attn_decode_static. */
 #define LS_DECODE_STATIC_SCRATCH_BYTES ((size_t)32 << 20)
 

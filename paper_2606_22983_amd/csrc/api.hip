@@ -359,9 +359,30 @@ ls_status paged_attn_decode(ls_kv_pool *pool, int32_t layer, int32_t num_session
     // The step's own K/V row is written by the decode kernel (no separate append launch).
     hipError_t e = launch_decode(p, layer, num_sessions, num_q_heads, static_cast<const uint16_t *>(q),
                                  static_cast<const uint16_t *>(k_new), static_cast<const uint16_t *>(v_new),
-                                 block_tables, max_blocks_per_session, context_lens,
+                                 block_tables, max_blocks_per_session, context_lens, context_lens_host,
                                  scale, static_cast<uint16_t *>(out), workspace, plan, err, stream);
     return e == hipSuccess ? LS_OK : hip_fail(e, "decode launch");
+}
+
+ls_status ls_decode_schedule(const ls_kv_pool *pool, int32_t num_sessions, int32_t num_q_heads,
+                             int32_t max_blocks_per_session, const int32_t *context_lens_host, int32_t appended,
+                             hipStream_t stream, int32_t *split_tokens, int32_t *host_planned, int32_t *merge) {
+    if (ls_status st = check_pool(pool)) return st;
+    const PoolGeom &p = pool->geom;
+    if (num_sessions <= 0 || max_blocks_per_session <= 0 || (appended != 0 && appended != 1))
+        return fail(LS_EINVAL, "num_sessions and max_blocks_per_session must be > 0, appended 0 or 1");
+    if (!split_tokens || !host_planned || !merge) return fail(LS_EINVAL, "output pointers must not be NULL");
+    if (ls_status st = check_heads(p, num_q_heads)) return st;
+    const DecodePlan plan = plan_decode(p, num_sessions, num_q_heads, max_blocks_per_session);
+    if (!plan.supported) return fail(LS_EUNSUPPORTED, "batch exceeds the decode limits");
+    if (context_lens_host)
+        if (ls_status st = check_decode_lens_host(num_sessions, context_lens_host, appended, max_blocks_per_session))
+            return st;
+    const DecodeSchedule sc = decode_schedule(p, num_sessions, context_lens_host, appended, plan, stream);
+    *split_tokens = sc.split_tokens;
+    *host_planned = sc.host_planned ? 1 : 0;
+    *merge = sc.merge ? 1 : 0;
+    return LS_OK;
 }
 
 ls_status paged_attn_decode_static(ls_kv_pool *pool, int32_t layer, int32_t num_sessions,

@@ -72,11 +72,24 @@ hipError_t launch_append_prefill(const PoolGeom &p, int layer, int32_t num_sessi
                                  hipStream_t stream);
 // With k_new / v_new (both non-null) the step's own token is attended from
 // them and written to its pool slot by the decode kernel itself.
+// The schedule paged_attn_decode runs for a batch: tokens per split, planned
+// on the host (from context_lens_host) or in the kernel, merge kernel or not.
+struct DecodeSchedule {
+    int split_tokens;
+    bool host_planned;
+    bool merge;
+};
+DecodeSchedule decode_schedule(const PoolGeom &p, int32_t num_sessions, const int32_t *context_lens_host,
+                               int32_t appended, const DecodePlan &plan, hipStream_t stream);
+
+// With context_lens_host (the same lengths on the host) the split-K schedule
+// is planned on the host; the split merge is launched only if some session is
+// split.
 hipError_t launch_decode(const PoolGeom &p, int layer, int32_t num_sessions, int32_t num_q_heads,
                          const uint16_t *q, const uint16_t *k_new, const uint16_t *v_new,
                          const int32_t *block_tables,
-                         int32_t max_blocks, const int32_t *context_lens, float scale,
-                         uint16_t *out, void *workspace, const DecodePlan &plan,
+                         int32_t max_blocks, const int32_t *context_lens, const int32_t *context_lens_host,
+                         float scale, uint16_t *out, void *workspace, const DecodePlan &plan,
                          unsigned int *err, hipStream_t stream);
 hipError_t launch_prefill(const PoolGeom &p, int layer, int32_t num_sessions, int32_t num_q_heads,
                           const uint16_t *q, const int32_t *cu_new_lens,

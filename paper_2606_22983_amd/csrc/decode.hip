@@ -37,6 +37,9 @@
 // tile built from k_new / v_new, and then writes it to the slot for the next
 // steps.
 #include <algorithm>
+#include <queue>
+#include <type_traits>
+#include <vector>
 
 #include "common.h"
 
@@ -89,6 +92,25 @@ struct DecodeArgs {
     unsigned int *err;             // device error word
     int32_t num_sessions;
 };
+
+// A schedule planned on the host (paged_attn_decode with host lengths),
+// passed by value in the kernel arguments: workgroup w runs items
+// item[start[w] .. start[w + 1]), each packed as session (bits 0..11), KV head
+// (12..19), split (20..30) and "last split the plan gives the session" (31).
+constexpr int kPlanMaxWg = 256;
+constexpr int kPlanMaxItems = 640;
+struct DecodeHostPlan {
+    uint16_t start[kPlanMaxWg + 2];            // (+1 keeps the items 4-byte aligned)
+    uint32_t item[kPlanMaxItems];
+};
+struct NoPlan {
+    int32_t unused;
+};
+template <bool kHost>
+using PlanArg = typename std::conditional<kHost, DecodeHostPlan, NoPlan>::type;
+__device__ __forceinline__ uint32_t plan_start(const DecodeHostPlan &p, int w) { return p.start[w]; }
+__device__ __forceinline__ uint32_t plan_start(const NoPlan &, int) { return 0; }
+__device__ __forceinline__ uint32_t plan_item(const DecodeHostPlan &p, int i) { return p.item[i]; }
 
 template <int D>
 struct BlockRegs {
@@ -216,7 +238,9 @@ __device__ __forceinline__ unsigned block_exclusive_scan(unsigned v, unsigned *s
 }
 
 // Persistent decode: a fixed grid (one workgroup per CU) walks the work
-// items (session s, split k, KV head g).  Each workgroup first orders, in LDS,
+// items (session s, split k, KV head g).
+//
+// Device-planned schedule (kHost false): each workgroup first orders, in LDS,
 // the work rows (session, split) longest first: every full split (T tokens),
 // then each session's last, shorter split by block count, largest first (an
 // empty session's one row is among them).  Items are dealt in snake order:
@@ -224,10 +248,20 @@ __device__ __forceinline__ unsigned block_exclusive_scan(unsigned v, unsigned *s
 // k (W workgroups), so every workgroup receives about the same number of
 // tokens; with plain round-robin the workgroups holding one item more than the
 // rest decide the call's duration.  Every workgroup derives the same order
-// from the lengths, no workgroup is launched for a split that does not exist,
-// and each fetches the next item's block ids while it works on the current one.
-template <int D, int kDepth, int kMaxPerWave>
-__global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
+// from the lengths, and no workgroup is launched for a split that does not
+// exist.
+//
+// Host-planned schedule (kHost): the host, which knows the lengths, chose the
+// split size and gave each workgroup its list of items in the kernel
+// arguments; the workgroup only loads the lengths.  An item may then span
+// several chunks of kChunk tokens (8 blocks per wave); the online-softmax
+// state is carried from chunk to chunk and the waves merge once per item.
+//
+// Either way each workgroup fetches the next chunk's block ids while it works
+// on the current one, and requests its first blocks before merging.
+template <int D, int kDepth, int kMaxPerWave, bool kHost>
+__global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a, PlanArg<kHost> plan) {
+    constexpr int kChunk = kMaxPerWave * kDecWaves * kBlock;   // tokens per chunk
     __shared__ int sm_cum[kMaxBatch + 1];       // first full-split row of each session
     __shared__ int sm_len[kMaxBatch];           // attended length of each session
     __shared__ int sm_porder[kMaxBatch];        // sessions of the short-split rows, in row order
@@ -254,83 +288,92 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
         sm_arrived[tid] = 0;
         sm_merged[tid] = 0;
     }
-    constexpr int kMaskWords = kDecThreads / 64;
-    for (int i = tid; i < kKeyBins * kMaskWords; i += kDecThreads) sm_kmask[i / kMaskWords][i % kMaskWords] = 0ull;
-    // ---- work rows: full splits per session (prefix sum) and short splits.
-    // Both counts share one unsigned scan: full rows in bits 0..19 (at most
-    // kMaxBatch * kMaxSplits = 2^19 in total), short rows (at most kMaxBatch)
-    // in bits 20..31.
-    const int per_thread = (S + kDecThreads - 1) / kDecThreads;
-    const int s_begin = min(S, tid * per_thread);
-    const int s_end = min(S, s_begin + per_thread);
-    auto has_short = [&](int L) { return L == 0 || L % T != 0; };   // an empty session still owns one row
-    unsigned mine = 0;
-    for (int s = s_begin; s < s_end; ++s) {
-        const int L = attended_len(a, s, blockIdx.x == 0);
-        sm_len[s] = L;
-        sm_own[s] = a.appended && a.lens[s] >= 0 && a.lens[s] + 1 <= a.max_blocks * kBlock;
-        mine += (unsigned)(L / T) + (has_short(L) ? 1u << 20 : 0u);
-    }
-    unsigned packed_total = 0;
-    const unsigned packed_run = block_exclusive_scan(mine, sm_wave_tot, packed_total);
-    const int full_rows = (int)(packed_total & 0xFFFFFu);
-    const int total_rows = full_rows + (int)(packed_total >> 20);
-    {
-        int frun = (int)(packed_run & 0xFFFFFu), prun = (int)(packed_run >> 20);
+    int full_rows = 0, total_rows = 0;
+    if constexpr (kHost) {
+        // The schedule came with the arguments: only the lengths are needed.
+        for (int s = tid; s < S; s += kDecThreads) {
+            sm_len[s] = attended_len(a, s, blockIdx.x == 0);
+            sm_own[s] = a.appended && a.lens[s] >= 0 && a.lens[s] + 1 <= a.max_blocks * kBlock;
+        }
+    } else {
+        constexpr int kMaskWords = kDecThreads / 64;
+        for (int i = tid; i < kKeyBins * kMaskWords; i += kDecThreads) sm_kmask[i / kMaskWords][i % kMaskWords] = 0ull;
+        // ---- work rows: full splits per session (prefix sum) and short splits.
+        // Both counts share one unsigned scan: full rows in bits 0..19 (at most
+        // kMaxBatch * kMaxSplits = 2^19 in total), short rows (at most kMaxBatch)
+        // in bits 20..31.
+        const int per_thread = (S + kDecThreads - 1) / kDecThreads;
+        const int s_begin = min(S, tid * per_thread);
+        const int s_end = min(S, s_begin + per_thread);
+        auto has_short = [&](int L) { return L == 0 || L % T != 0; };   // an empty session still owns one row
+        unsigned mine = 0;
         for (int s = s_begin; s < s_end; ++s) {
-            const int L = sm_len[s];
-            sm_cum[s] = frun;
-            frun += L / T;
-            if (has_short(L)) {
-                if (S > kDecThreads) sm_porder[prun] = s;         // large batch: session order
-                ++prun;
+            const int L = attended_len(a, s, blockIdx.x == 0);
+            sm_len[s] = L;
+            sm_own[s] = a.appended && a.lens[s] >= 0 && a.lens[s] + 1 <= a.max_blocks * kBlock;
+            mine += (unsigned)(L / T) + (has_short(L) ? 1u << 20 : 0u);
+        }
+        unsigned packed_total = 0;
+        const unsigned packed_run = block_exclusive_scan(mine, sm_wave_tot, packed_total);
+        full_rows = (int)(packed_total & 0xFFFFFu);
+        total_rows = full_rows + (int)(packed_total >> 20);
+        {
+            int frun = (int)(packed_run & 0xFFFFFu), prun = (int)(packed_run >> 20);
+            for (int s = s_begin; s < s_end; ++s) {
+                const int L = sm_len[s];
+                sm_cum[s] = frun;
+                frun += L / T;
+                if (has_short(L)) {
+                    if (S > kDecThreads) sm_porder[prun] = s;         // large batch: session order
+                    ++prun;
+                }
+            }
+            if (S <= kDecThreads && tid < S) {
+                const int L = sm_len[tid];
+                sm_key[tid] = has_short(L) ? (L % T + kBlock - 1) / kBlock : -1;
             }
         }
-        if (S <= kDecThreads && tid < S) {
-            const int L = sm_len[tid];
-            sm_key[tid] = has_short(L) ? (L % T + kBlock - 1) / kBlock : -1;
-        }
-    }
-    if (tid == 0) sm_cum[S] = full_rows;
-    __syncthreads();
-    // Rank of each short row: rows with a larger block count first, then
-    // session order.  Keys are block counts 0..T/16, so the rank is the number
-    // of sessions with a larger key (suffix sums of per-key counts) plus the
-    // sessions before this one with the same key (a popcount of that key's
-    // session bitmask); both are built with order-independent LDS atomics, so
-    // every workgroup derives the same order.
-    const bool ranked = S <= kDecThreads && tid < S && sm_key[tid] >= 0;
-    if (ranked) __hip_atomic_fetch_or(&sm_kmask[sm_key[tid]][tid / 64], 1ull << (tid % 64), __ATOMIC_RELAXED,
-                                      __HIP_MEMORY_SCOPE_WORKGROUP);
-    __syncthreads();
-    if (S <= kDecThreads && tid < kWave) {
-        // Suffix sums over the key bins, one wave: bins 64*c + lane in chunk c.
-        int carry = 0;
-        for (int c = (kKeyBins + kWave - 1) / kWave - 1; c >= 0; --c) {
-            const int bin = c * kWave + tid;
-            int cnt = 0;
-            if (bin < kKeyBins)
-                for (int w = 0; w < kDecThreads / 64; ++w) cnt += __popcll(sm_kmask[bin][w]);
-            // inclusive suffix scan of cnt over the lanes (higher lanes first)
-            int x = cnt;
+        if (tid == 0) sm_cum[S] = full_rows;
+        __syncthreads();
+        // Rank of each short row: rows with a larger block count first, then
+        // session order.  Keys are block counts 0..T/16, so the rank is the number
+        // of sessions with a larger key (suffix sums of per-key counts) plus the
+        // sessions before this one with the same key (a popcount of that key's
+        // session bitmask); both are built with order-independent LDS atomics, so
+        // every workgroup derives the same order.
+        const bool ranked = S <= kDecThreads && tid < S && sm_key[tid] >= 0;
+        if (ranked) __hip_atomic_fetch_or(&sm_kmask[sm_key[tid]][tid / 64], 1ull << (tid % 64), __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_WORKGROUP);
+        __syncthreads();
+        if (S <= kDecThreads && tid < kWave) {
+            // Suffix sums over the key bins, one wave: bins 64*c + lane in chunk c.
+            int carry = 0;
+            for (int c = (kKeyBins + kWave - 1) / kWave - 1; c >= 0; --c) {
+                const int bin = c * kWave + tid;
+                int cnt = 0;
+                if (bin < kKeyBins)
+                    for (int w = 0; w < kDecThreads / 64; ++w) cnt += __popcll(sm_kmask[bin][w]);
+                // inclusive suffix scan of cnt over the lanes (higher lanes first)
+                int x = cnt;
 #pragma unroll
-            for (int off = 1; off < kWave; off <<= 1) {
-                const int y = __shfl_down(x, off);
-                if (tid + off < kWave) x += y;
+                for (int off = 1; off < kWave; off <<= 1) {
+                    const int y = __shfl_down(x, off);
+                    if (tid + off < kWave) x += y;
+                }
+                if (bin < kKeyBins) sm_kabove[bin] = carry + x - cnt;
+                carry += __shfl(x, 0);
             }
-            if (bin < kKeyBins) sm_kabove[bin] = carry + x - cnt;
-            carry += __shfl(x, 0);
         }
+        __syncthreads();
+        if (ranked) {
+            const int key = sm_key[tid];
+            int rank = sm_kabove[key];
+            for (int w = 0; w < tid / 64; ++w) rank += __popcll(sm_kmask[key][w]);
+            rank += __popcll(sm_kmask[key][tid / 64] & ((1ull << (tid % 64)) - 1ull));
+            sm_porder[rank] = tid;
+        }
+        __syncthreads();
     }
-    __syncthreads();
-    if (ranked) {
-        const int key = sm_key[tid];
-        int rank = sm_kabove[key];
-        for (int w = 0; w < tid / 64; ++w) rank += __popcll(sm_kmask[key][w]);
-        rank += __popcll(sm_kmask[key][tid / 64] & ((1ull << (tid % 64)) - 1ull));
-        sm_porder[rank] = tid;
-    }
-    __syncthreads();
     const int total_items = total_rows * a.num_kv_heads;
     const int W = (int)gridDim.x;
     auto item_of = [&](int round) { return round * W + ((round & 1) ? W - 1 - (int)blockIdx.x : (int)blockIdx.x); };
@@ -345,10 +388,10 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
 #pragma unroll
     for (int dt = 0; dt < D / 16; ++dt) voff[dt] = ((dt * 16 + c16) * kBlock + g4 * 4) * 2;
 
-    // (session, split) of work row r.  A full row: the largest s with
-    // sm_cum[s] <= r (a session without full splits shares its sm_cum with the
-    // next session, so it is never the largest).  A short row: its session's
-    // last split.
+    // (session, split) of work row r of the device schedule.  A full row: the
+    // largest s with sm_cum[s] <= r (a session without full splits shares its
+    // sm_cum with the next session, so it is never the largest).  A short row:
+    // its session's last split.
     auto locate = [&](int row, int &s_out, int &split_out) {
         if (row >= full_rows) {
             s_out = sm_porder[row - full_rows];
@@ -363,11 +406,34 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
         s_out = lo;
         split_out = row - sm_cum[lo];
     };
-    // Raw block ids of a split, one per lane.  The load is unconditional (its
-    // index clamped into the table row) and the id is validated only when it is
-    // used, so nothing waits for this load until the item is processed.
-    auto fetch_ids = [&](int s_, int split_) -> int {
-        const int j = min(split_ * (T / kBlock) + lane, a.max_blocks - 1);
+    // This workgroup's k-th item: (session, KV head, split, last split the
+    // plan gives the session), or false past its last item.
+    const int host_base = kHost ? (int)plan_start(plan, blockIdx.x) : 0;
+    const int host_count = kHost ? (int)plan_start(plan, blockIdx.x + 1) - host_base : 0;
+    auto item_at = [&](int k, int &s_out, int &g_out, int &split_out, bool &last_out) -> bool {
+        if constexpr (kHost) {
+            if (k >= host_count) return false;
+            const uint32_t e = plan_item(plan, host_base + k);
+            s_out = (int)(e & 0xFFFu);
+            g_out = (int)((e >> 12) & 0xFFu);
+            split_out = (int)((e >> 20) & 0x7FFu);
+            last_out = (e >> 31) != 0;
+            return true;
+        } else {
+            const int item = item_of(k);
+            if (item >= total_items) return false;
+            locate(item / a.num_kv_heads, s_out, split_out);
+            g_out = item % a.num_kv_heads;
+            last_out = false;
+            return true;
+        }
+    };
+    // Raw block ids of chunk c of a split, one per lane.  The load is
+    // unconditional (its index clamped into the table row) and the id is
+    // validated only when it is used, so nothing waits for this load until the
+    // chunk is processed.
+    auto fetch_ids = [&](int s_, int split_, int c_) -> int {
+        const int j = min(split_ * (T / kBlock) + c_ * (kChunk / kBlock) + lane, a.max_blocks - 1);
         return a.block_tables[(int64_t)s_ * a.max_blocks + j];
     };
     // Validated id (or -1) of entry idx of a fetched id register.
@@ -391,64 +457,76 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
             qo[ks] = __builtin_bit_cast(bf16x8, v);
         }
     };
-    // Block count of a split and this wave's it-th block id within it.
-    auto split_blocks = [&](int s_, int split_) -> int {
-        const int L = sm_len[s_];
-        const int t0 = split_ * T;
-        return L > t0 ? (min(L, t0 + T) + kBlock - 1) / kBlock - t0 / kBlock : 0;
+    // Block count of chunk c of a split: tokens [t0, min(L, split end, t0 + kChunk)).
+    auto chunk_blocks = [&](int L, int split_, int c_) -> int {
+        const int t0 = split_ * T + c_ * kChunk;
+        const int t1 = min(min(L, split_ * T + T), t0 + kChunk);
+        return t1 > t0 ? (t1 + kBlock - 1) / kBlock - t0 / kBlock : 0;
     };
 
-    // kDepth blocks in flight per wave, carried across items: the next item's
-    // first blocks (and its q) are requested before the current item's merge.
+    // kDepth blocks in flight per wave, carried across chunks and items: the
+    // next chunk's first blocks (and, for a new item, its q) are requested
+    // before the current item is merged.
     BlockRegs<D> r[kDepth];
     int bb[kDepth];
     bf16x8 qop[D / 32];
-    // Each wave keeps the fetched block ids of the current and the next item in
+    // Each wave keeps the fetched block ids of the current and the next chunk in
     // its own LDS slots (double-buffered; read back with readlane), so no value
-    // loaded from memory is carried around the item loop.
+    // loaded from memory is carried around the loop.
     __shared__ int sm_ids[kDecWaves][2][kMaxSplitTokens / kBlock];
-    int item = item_of(0);
-    int s = 0, split = 0;
-    if (item < total_items) {
-        locate(item / a.num_kv_heads, s, split);
-        const int ids0 = fetch_ids(s, split);
-        if (lane < kMaxSplitTokens / kBlock) sm_ids[wave][0][lane] = ids0;
-        load_q(s, item % a.num_kv_heads, qop);
-        const int nb = split_blocks(s, split);
+    int k = 0, c = 0;                  // current item (index in this workgroup's list) and chunk
+    int s = 0, g = 0, split = 0;
+    bool last_planned = false;
+    bool have = item_at(0, s, g, split, last_planned);
+    int ids_pre = have ? fetch_ids(s, split, 0) : -1;
+    if (have) load_q(s, g, qop);
+    if constexpr (kHost) __syncthreads();      // the lengths are in LDS
+    if (have) {
+        if (lane < kMaxSplitTokens / kBlock) sm_ids[wave][0][lane] = ids_pre;
+        const int nb = chunk_blocks(sm_len[s], split, 0);
 #pragma unroll
         for (int j = 0; j < kDepth; ++j) {
-            bb[j] = checked_id(ids0, wave + j * kDecWaves, nb);
-            load_block<D>(r[j], a.pool, a.num_kv_heads, item % a.num_kv_heads, bb[j], koff, voff);
+            bb[j] = checked_id(ids_pre, wave + j * kDecWaves, nb);
+            load_block<D>(r[j], a.pool, a.num_kv_heads, g, bb[j], koff, voff);
         }
     }
-    for (int k = 0; item < total_items; ++k, item = item_of(k)) {
-        const int g = item % a.num_kv_heads;
+    float m = kMaxFloor, lsum = 0.f;
+    f32x4 o[D / 16];
+    int merges = 0;
+    for (int u = 0; have; ++u) {
         const int L = sm_len[s];
         const int own = sm_own[s];
         const int Lp = L - own;            // keys read from the pool; the own token comes from k_new
-        const int cur_s = s, cur_split = split;
-        const int cur_ids = lane < kMaxSplitTokens / kBlock ? sm_ids[wave][k & 1][lane] : -1;
-        // Next item: its (session, split) and block ids, fetched now.
-        const int next = item_of(k + 1);
-        const bool has_next = next < total_items;
+        const int cur_s = s, cur_g = g, cur_split = split, cur_c = c;
+        const bool cur_last_planned = last_planned;
+        const int cur_ids = lane < kMaxSplitTokens / kBlock ? sm_ids[wave][u & 1][lane] : -1;
+        const int t_split_end = min(L, cur_split * T + T);
+        const int t0 = cur_split * T + cur_c * kChunk;
+        const bool last_chunk = t0 + kChunk >= t_split_end;
+        // Next chunk: the same item's, or the next item's first; its ids fetched now.
         int next_ids = -1;
-        if (has_next) {
-            locate(next / a.num_kv_heads, s, split);
-            next_ids = fetch_ids(s, split);
+        if (last_chunk) {
+            ++k;
+            c = 0;
+            have = item_at(k, s, g, split, last_planned);
+        } else {
+            ++c;
         }
-        const int t0 = cur_split * T;
+        if (have) next_ids = fetch_ids(s, split, c);
         const int nsplit = L > 0 ? (L + T - 1) / T : 1;
         const int blk0 = t0 / kBlock;
-        const int nblk = split_blocks(cur_s, cur_split);
+        const int nblk = chunk_blocks(L, cur_split, cur_c);
         const int my_n = wave < nblk ? (nblk - wave + kDecWaves - 1) / kDecWaves : 0;
         auto bid = [&](int it) -> int { return checked_id(cur_ids, wave + it * kDecWaves, nblk); };
 
-        // The running max starts at a finite floor: a block whose keys are all
-        // masked then leaves (m, l, O) unchanged instead of producing NaN.
-        float m = kMaxFloor, lsum = 0.f;
-        f32x4 o[D / 16];
+        // A new item's running max starts at a finite floor: a block whose keys
+        // are all masked then leaves (m, l, O) unchanged instead of producing NaN.
+        if (cur_c == 0) {
+            m = kMaxFloor;
+            lsum = 0.f;
 #pragma unroll
-        for (int dt = 0; dt < D / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int dt = 0; dt < D / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
 
         // The per-wave block sequence is fully unrolled (at most kMaxPerWave
         // blocks) with forward-only exits, so the compiler sees straight-line
@@ -462,7 +540,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
             process_block<D>(r[j], qop, tb, bb[j] >= 0 ? Lp : 0, a.scale_log2, g4, m, lsum, o);
             if (i + kDepth < kMaxPerWave) {
                 bb[j] = bid(i + kDepth);
-                load_block<D>(r[j], a.pool, a.num_kv_heads, g, bb[j], koff, voff);
+                load_block<D>(r[j], a.pool, a.num_kv_heads, cur_g, bb[j], koff, voff);
             }
         }
         // The step's own token (position Lp): the wave that held its block attends
@@ -470,10 +548,10 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
         // masked above) and writes it to that slot for later steps.  No other
         // workgroup reads the slot in this launch, and the same wave already
         // loaded the block, so the write races with no read that matters.
-        if (own && cur_split == nsplit - 1) {
-            const int bl = Lp / kBlock - blk0;             // the token's block within the split
+        if (own && cur_split == nsplit - 1 && last_chunk) {
+            const int bl = Lp / kBlock - blk0;             // the token's block within the chunk
             if (wave == bl % kDecWaves) {
-                const int64_t row = ((int64_t)cur_s * a.num_kv_heads + g) * D;
+                const int64_t row = ((int64_t)cur_s * a.num_kv_heads + cur_g) * D;
                 BlockRegs<D> nr;
 #pragma unroll
                 for (int ks = 0; ks < D / 32; ++ks) {
@@ -491,7 +569,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
                     const int t = Lp % kBlock;
                     uint16_t *pool = const_cast<uint16_t *>(a.pool);
                     const int64_t tile = (int64_t)kBlock * D;
-                    uint16_t *kt = pool + ((int64_t)blk * 2 * a.num_kv_heads + g) * tile;
+                    uint16_t *kt = pool + ((int64_t)blk * 2 * a.num_kv_heads + cur_g) * tile;
                     uint16_t *vt = kt + (int64_t)a.num_kv_heads * tile;
                     for (int d = lane; d < D; d += kWave) {
                         kt[((d >> 3) * kBlock + t) * 8 + (d & 7)] = a.k_new[row + d];
@@ -500,39 +578,45 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
                 }
             }
         }
-        // Request the next item's first blocks and q before merging this one.
-        if (has_next) {
-            if (lane < kMaxSplitTokens / kBlock) sm_ids[wave][(k + 1) & 1][lane] = next_ids;
-            const int g_next = next % a.num_kv_heads;
-            const int nb = split_blocks(s, split);
-            load_q(s, g_next, qop);
+        // Request the next chunk's first blocks (and a new item's q) before
+        // merging this item.
+        if (have) {
+            if (lane < kMaxSplitTokens / kBlock) sm_ids[wave][(u + 1) & 1][lane] = next_ids;
+            const int nb = chunk_blocks(sm_len[s], split, c);
+            if (c == 0) load_q(s, g, qop);
 #pragma unroll
             for (int j = 0; j < kDepth; ++j) {
                 bb[j] = checked_id(next_ids, wave + j * kDecWaves, nb);
-                load_block<D>(r[j], a.pool, a.num_kv_heads, g_next, bb[j], koff, voff);
+                load_block<D>(r[j], a.pool, a.num_kv_heads, g, bb[j], koff, voff);
             }
         }
-        lsum = wave_sum_xor_16_32(lsum);
+        if (!last_chunk) continue;         // the item goes on: (m, l, O) carry over
+        // A host plan that stops short of the session's keys leaves them
+        // unattended: flagged (the device lengths differ from the host's).
+        if (kHost && cur_last_planned && cur_split * T + T < L && lane == 0 && wave == 0)
+            flag_error(a.err, LS_DEVERR_LENGTH);
+        const float lsum_w = wave_sum_xor_16_32(lsum);
 
         // ---- asynchronous merge of the item's waves: no workgroup barrier.
-        const int slot = k & 1;
-        // The slot is free once the merge of the item two steps back is done.
+        const int slot = merges & 1;
+        // The slot is free once the merge of the item two merges back is done.
         // (Bounded: a wait that never ends would be a bug; it is flagged, not hung on.)
         for (int spin = 0; __hip_atomic_load(&sm_merged[slot], __ATOMIC_ACQUIRE,
-                                             __HIP_MEMORY_SCOPE_WORKGROUP) != (k >> 1); ++spin) {
+                                             __HIP_MEMORY_SCOPE_WORKGROUP) != (merges >> 1); ++spin) {
             if (spin == kSpinLimit) {
                 if (lane == 0) flag_error(a.err, LS_DEVERR_INTERNAL);
                 break;
             }
             __builtin_amdgcn_s_sleep(1);
         }
+        ++merges;
         if (c16 < G) {
 #pragma unroll
             for (int dt = 0; dt < D / 16; ++dt)
                 *reinterpret_cast<f32x4 *>(&sm_o[slot][wave][c16][dt * 16 + g4 * 4]) = o[dt];
             if (g4 == 0) {
                 sm_m[slot][wave][c16] = m;
-                sm_l[slot][wave][c16] = lsum;
+                sm_l[slot][wave][c16] = lsum_w;
             }
         }
         // One arrival per wave (lane 0), broadcast to the whole wave.
@@ -543,12 +627,15 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
         before = __builtin_amdgcn_readfirstlane(before);
         if (before == kDecWaves - 1) {
             // Last wave in: merge the item (4 consecutive outputs per lane per step).
-            const int64_t part = ((int64_t)cur_s * a.num_kv_heads + g) * a.max_splits + cur_split;
+            // A split past the session's last (device lengths shorter than the
+            // host plan assumed) writes nothing.
+            const int64_t part = ((int64_t)cur_s * a.num_kv_heads + cur_g) * a.max_splits + cur_split;
+            const bool writes = cur_split < nsplit;
             for (int base = lane * 4; base < G * D && L <= 0; base += kWave * 4)
                 // Softmax over no key is undefined: the output is zero (flagged in attended_len).
-                *reinterpret_cast<uint2 *>(a.out + ((int64_t)cur_s * hq_total + g * G) * D + base) =
+                *reinterpret_cast<uint2 *>(a.out + ((int64_t)cur_s * hq_total + cur_g * G) * D + base) =
                     make_uint2(0u, 0u);
-            for (int base = lane * 4; base < G * D && L > 0; base += kWave * 4) {
+            for (int base = lane * 4; base < G * D && L > 0 && writes; base += kWave * 4) {
                 const int h = base / D, d = base % D;
                 float M = sm_m[slot][0][h];
 #pragma unroll
@@ -563,7 +650,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a) {
                 }
                 if (nsplit == 1) {
                     const float inv = 1.f / wsum;
-                    *reinterpret_cast<uint2 *>(a.out + ((int64_t)cur_s * hq_total + g * G + h) * D + d) =
+                    *reinterpret_cast<uint2 *>(a.out + ((int64_t)cur_s * hq_total + cur_g * G + h) * D + d) =
                         make_uint2(pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv));
                 } else {
                     *reinterpret_cast<f32x4 *>(a.part_acc + (part * G + h) * D + d) = acc;
@@ -695,11 +782,142 @@ DecodePlan plan_decode(const PoolGeom &p, int32_t num_sessions, int32_t num_q_he
     return plan;
 }
 
+namespace {
+
+// Host-side schedule (see DecodeHostPlan).  Chooses the split size T (a
+// multiple of 1024 tokens, at least t_min) among: no split at all (T covers
+// the longest session), 2048 and 4096, by the cost of a longest-first
+// assignment of the items to the workgroups: the most loaded workgroup's
+// tokens plus a fixed cost per item, plus the merge kernel's cost when some
+// session is split.  Items then go, longest first, to the least loaded
+// workgroup; each workgroup runs its items in that order.  Returns false when
+// the batch does not fit the argument block (more workgroups or items), or
+// when the device's own schedule (split size t_dev, snake-dealt rows; its merge
+// launched whenever dev_merges) is estimated to finish no later.
+constexpr int64_t kItemCostTokens = 64;      // per-item start-up, in tokens of streaming
+constexpr int64_t kMergeCostTokens = 256;    // the split merge launch, in tokens
+constexpr int64_t kScheduleCostTokens = 128; // the device schedule in the kernel prologue, in tokens
+bool plan_decode_host(int S, int num_kv_heads, const int32_t *lens_host, int appended, int W, int t_min,
+                      int t_dev, bool dev_merges, DecodeHostPlan &plan, int &t_out, bool &any_split) {
+    if (W < 1 || W > kPlanMaxWg || S > 4096 || num_kv_heads > 255) return false;
+    int64_t max_len = 1;
+    for (int s = 0; s < S; ++s) max_len = std::max<int64_t>(max_len, (int64_t)lens_host[s] + appended);
+    // The device schedule's estimated makespan: rows of full splits in session
+    // order, then the short rows by block count (largest first), each row's
+    // heads consecutive, dealt in snake order.
+    int64_t dev_cost;
+    {
+        std::vector<int64_t> rows;
+        std::vector<std::pair<int, int>> shorts;   // (-blocks, session)
+        for (int s = 0; s < S; ++s) {
+            const int64_t L = std::max<int64_t>((int64_t)lens_host[s] + appended, 0);
+            for (int64_t k = 0; k < L / t_dev; ++k) rows.push_back(t_dev);
+            if (L == 0 || L % t_dev) shorts.push_back({-(int)((L % t_dev + kBlock - 1) / kBlock), s});
+        }
+        std::stable_sort(shorts.begin(), shorts.end());
+        for (const auto &r : shorts) rows.push_back((int64_t)(-r.first) * kBlock);
+        std::vector<int64_t> load(W, 0);
+        int64_t item = 0;
+        for (int64_t t : rows)
+            for (int g = 0; g < num_kv_heads; ++g, ++item) {
+                const int64_t round = item / W, w = item % W;
+                load[(round & 1) ? W - 1 - w : w] += t + kItemCostTokens;
+            }
+        dev_cost = *std::max_element(load.begin(), load.end()) + kScheduleCostTokens +
+                   (dev_merges ? kMergeCostTokens : 0);
+    }
+    struct Item {
+        int64_t tokens;
+        int s, split, g;
+    };
+    std::vector<Item> items;
+    auto build = [&](int T) -> bool {
+        items.clear();
+        for (int s = 0; s < S; ++s) {
+            const int64_t L = std::max<int64_t>((int64_t)lens_host[s] + appended, 1);
+            const int ns = (int)((L + T - 1) / T);
+            if (ns > 2047) return false;
+            for (int k = 0; k < ns; ++k)
+                for (int g = 0; g < num_kv_heads; ++g)
+                    items.push_back({std::min<int64_t>(L, (int64_t)(k + 1) * T) - (int64_t)k * T, s, k, g});
+            if ((int)items.size() > kPlanMaxItems) return false;
+        }
+        std::stable_sort(items.begin(), items.end(),
+                         [](const Item &x, const Item &y) { return x.tokens > y.tokens; });
+        return true;
+    };
+    typedef std::pair<int64_t, int> Load;      // (tokens, workgroup), least loaded on top
+    auto makespan = [&](std::vector<int> *owner) -> int64_t {
+        std::priority_queue<Load, std::vector<Load>, std::greater<Load>> heap;
+        for (int w = 0; w < W; ++w) heap.push(Load(0, w));
+        int64_t worst = 0;
+        for (size_t i = 0; i < items.size(); ++i) {
+            Load l = heap.top();
+            heap.pop();
+            l.first += items[i].tokens + kItemCostTokens;
+            worst = std::max(worst, l.first);
+            if (owner) (*owner)[i] = l.second;
+            heap.push(l);
+        }
+        return worst;
+    };
+    const int unit = 1024;
+    int cands[3] = {(int)((max_len + unit - 1) / unit * unit), 2048, 4096};
+    int best_t = 0;
+    int64_t best_cost = INT64_MAX;
+    for (int T : cands) {
+        T = std::max(T, t_min);
+        if (T % unit || T > (int)((max_len + unit - 1) / unit * unit) + unit) continue;
+        if (!build(T)) continue;
+        const bool split = T < max_len;
+        const int64_t cost = makespan(nullptr) + (split ? kMergeCostTokens : 0);
+        if (cost < best_cost) {
+            best_cost = cost;
+            best_t = T;
+        }
+    }
+    if (!best_t || best_cost >= dev_cost || !build(best_t)) return false;
+    std::vector<int> owner(items.size());
+    makespan(&owner);
+    std::vector<int> count(W + 1, 0);
+    for (int w : owner) ++count[w + 1];
+    for (int w = 0; w < W; ++w) count[w + 1] += count[w];
+    for (int w = 0; w <= W; ++w) plan.start[w] = (uint16_t)count[w];
+    std::vector<int> fill(count.begin(), count.end() - 1);
+    for (size_t i = 0; i < items.size(); ++i) {
+        const Item &it = items[i];
+        const int64_t L = std::max<int64_t>((int64_t)lens_host[it.s] + appended, 1);
+        const bool last = (int64_t)(it.split + 1) * best_t >= L;
+        plan.item[fill[owner[i]]++] = (uint32_t)it.s | ((uint32_t)it.g << 12) | ((uint32_t)it.split << 20) |
+                                      (last ? 0x80000000u : 0u);
+    }
+    t_out = best_t;
+    any_split = best_t < max_len;
+    return true;
+}
+
+}  // namespace
+
+DecodeSchedule decode_schedule(const PoolGeom &p, int32_t num_sessions, const int32_t *context_lens_host,
+                               int32_t appended, const DecodePlan &plan, hipStream_t stream) {
+    DecodeSchedule sc{plan.split_tokens, false, plan.max_splits > 1};
+    if (context_lens_host) {
+        static thread_local DecodeHostPlan hp;
+        int T = 0;
+        bool split = false;
+        if (plan_decode_host(num_sessions, p.num_kv_heads, context_lens_host, appended, stream_cus(p, stream),
+                             std::max(plan.split_tokens, 1024), plan.split_tokens, plan.max_splits > 1, hp, T,
+                             split))
+            sc = DecodeSchedule{T, true, split};
+    }
+    return sc;
+}
+
 hipError_t launch_decode(const PoolGeom &p, int layer, int32_t num_sessions, int32_t num_q_heads,
                          const uint16_t *q, const uint16_t *k_new, const uint16_t *v_new,
                          const int32_t *block_tables,
-                         int32_t max_blocks, const int32_t *context_lens, float scale,
-                         uint16_t *out, void *workspace, const DecodePlan &plan,
+                         int32_t max_blocks, const int32_t *context_lens, const int32_t *context_lens_host,
+                         float scale, uint16_t *out, void *workspace, const DecodePlan &plan,
                          unsigned int *err, hipStream_t stream) {
     DecodeArgs a;
     a.pool = p.layer_base(layer);
@@ -722,13 +940,38 @@ hipError_t launch_decode(const PoolGeom &p, int layer, int32_t num_sessions, int
     a.part_ml = reinterpret_cast<float *>(ws);
     a.part_acc = reinterpret_cast<float *>(ws + plan.ml_bytes);
     a.num_sessions = num_sessions;
+    const int64_t resident = (int64_t)stream_cus(p, stream);
+    dim3 cgrid(p.num_kv_heads, num_sessions);
+    // Host lengths: the schedule is planned here and passed with the arguments.
+    if (context_lens_host) {
+        static thread_local DecodeHostPlan hp;
+        int T = 0;
+        bool split = false;
+        if (plan_decode_host(num_sessions, p.num_kv_heads, context_lens_host, a.appended, (int)resident,
+                             std::max(plan.split_tokens, 1024), plan.split_tokens, plan.max_splits > 1, hp, T,
+                             split)) {
+            a.split_tokens = T;
+            const dim3 grid((unsigned)resident);
+            if (p.head_dim == 128)
+                hipLaunchKernelGGL((decode_kernel<128, 2, 8, true>), grid, dim3(kDecThreads), 0, stream, a, hp);
+            else
+                hipLaunchKernelGGL((decode_kernel<64, 2, 8, true>), grid, dim3(kDecThreads), 0, stream, a, hp);
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess || !split) return e;
+            if (p.head_dim == 128)
+                hipLaunchKernelGGL(decode_combine_kernel<128>, cgrid, dim3(kCombThreads), 0, stream, a);
+            else
+                hipLaunchKernelGGL(decode_combine_kernel<64>, cgrid, dim3(kCombThreads), 0, stream, a);
+            return hipGetLastError();
+        }
+    }
     const int64_t upper = (int64_t)num_sessions * p.num_kv_heads * plan.max_splits;
     // Persistent grid: one 512-thread workgroup (8 waves, this kernel's
     // occupancy) on every CU the stream may use.
-    const int64_t resident = (int64_t)stream_cus(p, stream);
     dim3 grid((unsigned)std::min<int64_t>(upper, resident));
+    const NoPlan none{0};
 #define LS_DECODE(DD, PW) \
-    hipLaunchKernelGGL((decode_kernel<DD, 2, PW>), grid, dim3(kDecThreads), 0, stream, a)
+    hipLaunchKernelGGL((decode_kernel<DD, 2, PW, false>), grid, dim3(kDecThreads), 0, stream, a, none)
     const int per_wave = plan.split_tokens / (kDecWaves * kBlock);
     if (p.head_dim == 128) {
         if (per_wave == 4) LS_DECODE(128, 4);
@@ -740,7 +983,6 @@ hipError_t launch_decode(const PoolGeom &p, int layer, int32_t num_sessions, int
 #undef LS_DECODE
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || plan.max_splits == 1) return e;
-    dim3 cgrid(p.num_kv_heads, num_sessions);
     if (p.head_dim == 128)
         hipLaunchKernelGGL(decode_combine_kernel<128>, cgrid, dim3(kCombThreads), 0, stream, a);
     else

@@ -41,6 +41,9 @@ _lib.ls_decode_workspace_bytes.argtypes = [_p, _i32, _i32, _i32]
 _lib.ls_decode_workspace_bytes.restype = _sz
 _lib.paged_attn_decode.argtypes = [_p, _i32, _i32, _i32, _p, _p, _p, _p, _i32, _p, _p, _f32, _p,
                                    _p, _sz, _p]
+_lib.ls_decode_schedule.argtypes = [_p, _i32, _i32, _i32, _p, _i32, _p, ctypes.POINTER(_i32),
+                                    ctypes.POINTER(_i32), ctypes.POINTER(_i32)]
+_lib.ls_decode_schedule.restype = ctypes.c_int
 _lib.paged_attn_decode_static.argtypes = [_p, _i32, _i32, _i32, _p, _p, _p, _p, _i32, _p, _p, _f32,
                                           _p, _p]
 _lib.paged_attn_prefill.argtypes = [_p, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _i32, _i32, _p,
@@ -213,6 +216,18 @@ def paged_attn_decode(pool: KVPool, layer: int, q: torch.Tensor, block_tables: t
            "paged_attn_decode")
     del keep
     return out
+
+
+def ls_decode_schedule(pool: KVPool, num_sessions: int, num_q_heads: int, max_blocks_per_session: int,
+                       context_lens_host=None, appended: bool = False, stream=None) -> dict:
+    """How paged_attn_decode will run this batch: split size, host-planned, merge."""
+    keep, hl = _host_i32(context_lens_host, "context_lens_host", num_sessions)
+    t, h, m = _i32(), _i32(), _i32()
+    _check(_lib.ls_decode_schedule(pool.handle, num_sessions, num_q_heads, max_blocks_per_session, hl,
+                                   1 if appended else 0, _stream(stream), ctypes.byref(t), ctypes.byref(h),
+                                   ctypes.byref(m)), "ls_decode_schedule")
+    del keep
+    return {"split_tokens": t.value, "host_planned": bool(h.value), "merge": bool(m.value)}
 
 
 def paged_attn_decode_static(pool: KVPool, layer: int, q: torch.Tensor, block_tables: torch.Tensor,

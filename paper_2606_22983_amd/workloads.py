@@ -221,13 +221,31 @@ def tiny_decode(seed: int = SEEDS["tiny"], append: bool = False) -> DecodeCase:
     return _decode_case("tiny_decode", seed, rng, lens, 8, 2, 64, 256, 1, append)
 
 
+def _thinker_lengths(rng: np.random.Generator, num_sessions: int, sigma: float) -> np.ndarray:
+    z = rng.standard_normal(num_sessions)
+    return np.clip(np.round(np.exp(np.log(4096.0) + sigma * z)), 512, 16384).astype(np.int64)
+
+
+def _talker_lengths(rng: np.random.Generator, num_sessions: int) -> np.ndarray:
+    return rng.integers(512, 4096, size=num_sessions, endpoint=True).astype(np.int64)
+
+
+def thinker_lengths(seed: int = SEEDS["thinker"], num_sessions: int = 64, sigma: float = 1.0) -> np.ndarray:
+    """The context lengths of :func:`thinker_decode` alone (its first draws)."""
+    return _thinker_lengths(np.random.Generator(np.random.PCG64(seed)), num_sessions, sigma)
+
+
+def talker_lengths(seed: int = SEEDS["talker"], num_sessions: int = 256) -> np.ndarray:
+    """The starting context lengths of :func:`talker_decode` alone (its first draws)."""
+    return _talker_lengths(np.random.Generator(np.random.PCG64(seed)), num_sessions)
+
+
 def thinker_decode(seed: int = SEEDS["thinker"], num_sessions: int = 64, sigma: float = 1.0,
                    append: bool = False) -> DecodeCase:
     """64 sessions, L = clip(round(exp(ln 4096 + sigma * N(0,1))), 512, 16384),
     32/4 heads, D = 128, pool 1.25x the blocks in use, one query token each."""
     rng = np.random.Generator(np.random.PCG64(seed))
-    z = rng.standard_normal(num_sessions)
-    lens = np.clip(np.round(np.exp(np.log(4096.0) + sigma * z)), 512, 16384).astype(np.int64)
+    lens = _thinker_lengths(rng, num_sessions, sigma)
     case = _decode_case("thinker_decode", seed, rng, lens, 32, 4, 128, None, 1, append,
                         pool_factor=1.25)
     case.notes["sigma"] = sigma
@@ -239,7 +257,7 @@ def talker_decode(seed: int = SEEDS["talker"], num_sessions: int = 256, steps: i
     """256 sessions, L0 ~ U[512, 4096], 16/2 heads, D = 128, ``steps`` consecutive
     decode steps each appending one fresh token per session."""
     rng = np.random.Generator(np.random.PCG64(seed))
-    lens = rng.integers(512, 4096, size=num_sessions, endpoint=True).astype(np.int64)
+    lens = _talker_lengths(rng, num_sessions)
     return _decode_case("talker_decode", seed, rng, lens, 16, 2, 128, None, steps, True,
                         pool_factor=1.25)
 

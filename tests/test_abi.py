@@ -299,3 +299,54 @@ def test_binding_copy_checks_staging_size(built_lib, binding):
         kv.kv_blocks_restore(pool, _i32(3), _bf(3 * pool.block_bytes // 2 - 1))
     with pytest.raises(ValueError, match="max_gbps"):
         kv.kv_blocks_stash(pool, _i32(3), _bf(3 * pool.block_bytes // 2), max_gbps=-2.0)
+
+
+# ---- the decode schedule planned on the host (pure host code: no GPU needed)
+def _sched(lib, hkv, hq, lens, maxb, appended=0, host=True):
+    import numpy as np
+    h = ctypes.c_void_p()
+    d = _desc(num_layers=1, num_kv_heads=hkv, num_blocks=1 << 20, kv_bytes=1 << 40)
+    assert lib.kv_pool_create(ctypes.byref(d), ctypes.byref(h)) == LS_OK
+    arr = np.ascontiguousarray(lens, dtype=np.int32)
+    t, hp, m = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    r = lib.ls_decode_schedule(h, len(arr), hq, maxb, arr.ctypes.data_as(ctypes.c_void_p) if host else None,
+                               appended, None, ctypes.byref(t), ctypes.byref(hp), ctypes.byref(m))
+    lib.kv_pool_destroy(h)
+    return r, t.value, bool(hp.value), bool(m.value)
+
+
+def test_schedule_talker_batch_is_planned_on_host_without_merge(lib):
+    """256 talker sessions (512-4128 keys, 2 KV heads): whole sessions balance the
+    GPU, so the host plans one split per session and no merge kernel runs."""
+    from paper_2606_22983_amd import workloads as W
+    l0 = W.talker_lengths()
+    maxb = int(((l0 + 32 + 15) // 16).max())
+    for t in (0, 31):
+        r, split, host, merge = _sched(lib, 2, 16, l0 + t, maxb, appended=1)
+        assert r == LS_OK and host and not merge
+        assert split >= int(l0.max()) + t + 1 and split % 1024 == 0
+
+
+def test_schedule_thinker_batch_keeps_the_device_schedule(lib):
+    """The lognormal thinker batch (64 sessions up to 16k keys): the plans that fit
+    the argument block are no better than the device's 1024-token splits."""
+    from paper_2606_22983_amd import workloads as W
+    lens = W.thinker_lengths()
+    maxb = int(((lens + 15) // 16).max())
+    assert _sched(lib, 4, 32, lens, maxb) == (LS_OK, 1024, False, True)
+    assert _sched(lib, 4, 32, lens, maxb, host=False) == (LS_OK, 1024, False, True)
+
+
+def test_schedule_mixed_batch_splits_long_sessions(lib):
+    """Mostly ~2k-key sessions and ten of 8000 keys: the host splits at 2048 tokens
+    and the merge runs."""
+    import numpy as np
+    rng = np.random.default_rng(1)
+    lens = np.concatenate([rng.integers(1500, 2040, 200), np.full(10, 8000)])
+    assert _sched(lib, 2, 16, lens, 600) == (LS_OK, 2048, True, True)
+
+
+def test_schedule_rejects_bad_host_lengths(lib):
+    assert _sched(lib, 2, 16, [5, 0, 7], 10)[0] == LS_EINVAL          # an empty context
+    assert _sched(lib, 2, 16, [5, 0, 7], 10, appended=1)[0] == LS_OK
+    assert _sched(lib, 2, 16, [5, 161, 7], 10)[0] == LS_EINVAL        # past a 10-block table

@@ -241,3 +241,96 @@ def test_decode_with_host_lengths_matches_oracle(kv, oracle_lib, append):
     if append:
         assert np.array_equal(dp.host(), ref_pool)
     assert kv.ls_device_errors() == 0
+
+
+def _host_planned(kv, dp, S, hq, maxb, lens, appended):
+    return kv.ls_decode_schedule(dp.pool, S, hq, maxb, context_lens_host=lens, appended=appended)
+
+
+def test_talker_32_steps_host_planned(kv, oracle_lib):
+    """The talker loop with host lengths: the host plans one item per (session, KV
+    head) and no merge runs; steps checked against the oracle, pool bit-exact."""
+    case = W.talker_decode()
+    dp = DevicePool(kv, case.pool.data, 128)
+    tables = i32_dev(case.block_tables)
+    ws = None
+    ref_pool = case.pool.data.copy()
+    checked = {0, 7, 16, 31}
+    for t in range(case.steps):
+        lens = case.lens_at(t)
+        sc = _host_planned(kv, dp, case.num_sessions, case.num_q_heads, case.block_tables.shape[1], lens, True)
+        assert sc["host_planned"] and not sc["merge"], sc
+        if ws is None:
+            ws = torch.zeros(kv.decode_workspace_bytes(dp.pool, case.num_sessions, case.num_q_heads,
+                                                       case.block_tables.shape[1]), dtype=torch.uint8, device="cuda")
+        out = torch.empty((case.num_sessions, case.num_q_heads, 128), dtype=torch.bfloat16, device="cuda")
+        kv.paged_attn_decode(dp.pool, 0, bf16_dev(case.q[t]), tables, i32_dev(lens), case.scale, out, ws,
+                             bf16_dev(case.k_new[t]), bf16_dev(case.v_new[t]), context_lens_host=lens)
+        if t in checked:
+            ref, ref_pool = oracle_lib.decode(ref_pool, 16, 128, 0, case.q[t], case.block_tables, lens, case.scale,
+                                              k_new=case.k_new[t], v_new=case.v_new[t], pool_out=True)
+            assert_attn_close(out, ref, "host-planned talker step %d (split %d)" % (t, sc["split_tokens"]))
+        else:
+            oracle_lib.append(ref_pool, 16, 128, 0, case.block_tables, np.arange(case.num_sessions), lens,
+                              case.k_new[t], case.v_new[t])
+    assert np.array_equal(dp.host(), ref_pool), "pool after 32 host-planned appends differs"
+    assert kv.ls_device_errors() == 0
+
+
+@pytest.mark.parametrize("append", [False, True])
+def test_host_planned_with_splits_and_merge(kv, oracle_lib, append):
+    """Mostly ~2k-key sessions and a few of 8000: the host splits at 2048 tokens
+    (several chunks of 1024 per item) and the merge runs."""
+    rng = np.random.default_rng(90 + append)
+    lens = np.concatenate([rng.integers(1500, 2040, 200), np.full(10, 8000), [1, 2047, 2048, 4097]])
+    pool, tables, q, kn, vn = _synthetic(rng, lens, 16, 2, 128, append)
+    dp = DevicePool(kv, pool, 128)
+    sc = _host_planned(kv, dp, len(lens), 16, tables.shape[1], lens, append)
+    log("schedule: %s" % sc)
+    assert sc["host_planned"] and sc["merge"] and sc["split_tokens"] == 2048
+    ws = torch.zeros(kv.decode_workspace_bytes(dp.pool, len(lens), 16, tables.shape[1]), dtype=torch.uint8,
+                     device="cuda")
+    out = torch.empty((len(lens), 16, 128), dtype=torch.bfloat16, device="cuda")
+    kv.paged_attn_decode(dp.pool, 0, bf16_dev(q), i32_dev(tables), i32_dev(lens), 0.0884, out, ws,
+                         None if kn is None else bf16_dev(kn), None if vn is None else bf16_dev(vn),
+                         context_lens_host=lens)
+    ref, ref_pool = oracle_lib.decode(pool, 16, 128, 0, q, tables, lens, 0.0884, k_new=kn, v_new=vn, pool_out=True)
+    assert_attn_close(out, ref, "host-planned with splits, append=%s" % append)
+    if append:
+        assert np.array_equal(dp.host(), ref_pool)
+    assert kv.ls_device_errors() == 0
+
+
+def test_host_plan_device_lengths_disagree(kv, oracle_lib):
+    """Device lengths shorter than the host's: the plan covers them and the result
+    is that of the device lengths.  Longer: the keys past the plan are flagged
+    (LS_DEVERR_LENGTH), and nothing faults."""
+    rng = np.random.default_rng(95)
+    lens = rng.integers(600, 3000, size=256)
+    pool, tables, q, _, _ = _synthetic(rng, lens, 16, 2, 128, False)
+    dp = DevicePool(kv, pool, 128)
+    host = lens.copy()
+    assert _host_planned(kv, dp, 256, 16, tables.shape[1], host, False)["host_planned"]
+    shorter = lens - rng.integers(0, 500, size=256)
+    kv.ls_device_errors()
+    out, ws = run_decode(kv, dp, bf16_dev(q), i32_dev(tables), i32_dev(shorter), 0.0884)
+    out2 = torch.empty_like(out)
+    kv.paged_attn_decode(dp.pool, 0, bf16_dev(q), i32_dev(tables), i32_dev(shorter), 0.0884, out2, ws,
+                         context_lens_host=host)
+    ref = oracle_lib.decode(pool, 16, 128, 0, q, tables, shorter, 0.0884)
+    assert_attn_close(out2, ref, "host plan over shorter device lengths")
+    assert kv.ls_device_errors() == 0
+    # Device lengths of 2500-3000 keys (in the tables) against host lengths of at
+    # most 2000: the plan's one 2048-token split per session stops short.
+    real = rng.integers(2500, 3001, size=256)
+    pool2, tables2, q2, _, _ = _synthetic(rng, real, 16, 2, 128, False)
+    dp2 = DevicePool(kv, pool2, 128)
+    claimed = rng.integers(600, 2001, size=256)
+    sc = _host_planned(kv, dp2, 256, 16, tables2.shape[1], claimed, False)
+    assert sc["host_planned"] and sc["split_tokens"] == 2048 and not sc["merge"], sc
+    ws2 = torch.zeros(kv.decode_workspace_bytes(dp2.pool, 256, 16, tables2.shape[1]), dtype=torch.uint8,
+                      device="cuda")
+    out3 = torch.empty((256, 16, 128), dtype=torch.bfloat16, device="cuda")
+    kv.paged_attn_decode(dp2.pool, 0, bf16_dev(q2), i32_dev(tables2), i32_dev(real), 0.0884, out3, ws2,
+                         context_lens_host=claimed)
+    assert kv.ls_device_errors() & kv.LS_DEVERR_LENGTH

@@ -19,7 +19,8 @@ def kv():
     return kv_mod
 
 
-def test_captured_talker_steps_replay_exactly(kv, oracle_lib):
+@pytest.mark.parametrize("host_lengths", [False, True])
+def test_captured_talker_steps_replay_exactly(kv, oracle_lib, host_lengths):
     case = W.talker_decode(num_sessions=64, steps=8)
     dp = DevicePool(kv, case.pool.data, 128)
     tables = i32_dev(case.block_tables)
@@ -32,9 +33,12 @@ def test_captured_talker_steps_replay_exactly(kv, oracle_lib):
     ws = torch.zeros(kv.decode_workspace_bytes(dp.pool, S, hq, case.block_tables.shape[1]),
                      dtype=torch.uint8, device="cuda")
 
+    lens_h = [case.lens_at(t) if host_lengths else None for t in range(case.steps)]
+
     def steps():
         for t in range(case.steps):
-            kv.paged_attn_decode(dp.pool, 0, qs[t], tables, lens[t], case.scale, outs[t], ws, kns[t], vns[t])
+            kv.paged_attn_decode(dp.pool, 0, qs[t], tables, lens[t], case.scale, outs[t], ws, kns[t], vns[t],
+                                 context_lens_host=lens_h[t])
 
     steps()
     torch.cuda.synchronize()
