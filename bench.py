@@ -152,8 +152,15 @@ def decode_leg(torch, kv, W, args):
                                                case.block_tables.shape[1]),
                      dtype=torch.uint8, device="cuda")
     stream = torch.cuda.current_stream()
+    # The call as a serving loop makes it: lengths on the device for the kernel
+    # and on the host for the schedule (planned there when that is faster).
+    lens_h = case.context_lens.astype(np.int32)
+    call = lambda i: kv.paged_attn_decode(pools[i % 3], 0, q, tables, lens_d, case.scale, out, ws,
+                                          context_lens_host=lens_h)
+    sched = kv.ls_decode_schedule(pools[0], case.num_sessions, hq, case.block_tables.shape[1],
+                                  context_lens_host=lens_h)
     for i in range(args.warmup):
-        kv.paged_attn_decode(pools[i % 3], 0, q, tables, lens_d, case.scale, out, ws)
+        call(i)
     # One event pair over the back-to-back launches of the timed region: the
     # average launch duration includes the gap between the partial and merge
     # kernels but no event records between steps.
@@ -162,37 +169,34 @@ def decode_leg(torch, kv, W, args):
     t0 = time.perf_counter()
     e = timer.start()
     for i in range(args.steps):
-        kv.paged_attn_decode(pools[i % 3], 0, q, tables, lens_d, case.scale, out, ws)
+        call(i)
     timer.stop(e)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     assert kv.ls_device_errors() == 0
     kernel_ms = timer.mean_ms() / args.steps
     # Distribution of single calls (each in its own event pair, pools rotating).
-    per_call = sample(torch, stream, lambda i: kv.paged_attn_decode(pools[i % 3], 0, q, tables, lens_d,
-                                                                   case.scale, out, ws),
-                      args.reps, 1e3, "us")
-    # The same calls with the lengths also given on the host (the schedule is
-    # then planned on the host when that is estimated to be faster).
-    lens_h = case.context_lens.astype(np.int32)
-    hcall = lambda i: kv.paged_attn_decode(pools[i % 3], 0, q, tables, lens_d, case.scale, out, ws,
-                                           context_lens_host=lens_h)
+    per_call = sample(torch, stream, call, args.reps, 1e3, "us")
+    # The same calls without host lengths: the schedule is planned in the kernel.
+    dcall = lambda i: kv.paged_attn_decode(pools[i % 3], 0, q, tables, lens_d, case.scale, out, ws)
     for i in range(args.warmup):
-        hcall(i)
-    htimer = Timer(torch, stream)
+        dcall(i)
+    dtimer = Timer(torch, stream)
     torch.cuda.synchronize()
-    e = htimer.start()
+    e = dtimer.start()
     for i in range(args.steps):
-        hcall(i)
-    htimer.stop(e)
+        dcall(i)
+    dtimer.stop(e)
     torch.cuda.synchronize()
     assert kv.ls_device_errors() == 0
-    host_ms = htimer.mean_ms() / args.steps
-    res = dict(case=case, pools=pools, copies=copies, q=q, tables=tables, lens=lens_d, out=out,
+    device_ms = dtimer.mean_ms() / args.steps
+    res = dict(case=case, pools=pools, copies=copies, q=q, tables=tables, lens=lens_d, lens_h=lens_h, out=out,
                ws=ws, alg_bytes=alg_bytes, kv_bytes=kv_bytes, wall_s=wall, kernel_ms=kernel_ms,
-               ms_per_step=wall * 1e3 / args.steps, per_call=per_call, host_lens_ms=host_ms)
-    log("decode with host lengths: %.1f us/launch (events), %.0f GB/s" % (
-        host_ms * 1e3, alg_bytes / (host_ms * 1e-3) / 1e9))
+               ms_per_step=wall * 1e3 / args.steps, per_call=per_call, device_ms=device_ms, schedule=sched)
+    log("decode (host lengths, %s): %.1f us/step wall, %.1f us/launch (events), %.0f GB/s; single calls median "
+        "%.1f us (p10 %.1f, p90 %.1f); schedule planned in the kernel: %.1f us/launch" % (
+            sched, res["ms_per_step"] * 1e3, kernel_ms * 1e3, alg_bytes / (kernel_ms * 1e-3) / 1e9,
+            per_call["median"], per_call["p10"], per_call["p90"], device_ms * 1e3))
     log("decode: %.1f us/step wall, %.1f us/launch (events), %.0f GB/s; single calls median %.1f us "
         "(p10 %.1f, p90 %.1f)" % (res["ms_per_step"] * 1e3, kernel_ms * 1e3,
                                   alg_bytes / (kernel_ms * 1e-3) / 1e9, per_call["median"],
@@ -471,7 +475,8 @@ def restore_leg(torch, kv, W, args, dec):
         while (n_dec < 256 if alone else not ev_side_end.query()) and n_dec < 4000:
             e = dtimer.start()
             kv.paged_attn_decode(dec["pools"][n_dec % 3], 0, dec["q"], dec["tables"], dec["lens"],
-                                 dec["case"].scale, dec["out"], dec["ws"], stream=dec_stream)
+                                 dec["case"].scale, dec["out"], dec["ws"], context_lens_host=dec["lens_h"],
+                                 stream=dec_stream)
             dtimer.stop(e)
             n_dec += 1
             if n_dec % 16 == 0:
@@ -915,9 +920,15 @@ def main():
         "data": "synthetic (seeded multi-turn speech sessions; see workloads.py)",
         "config": {"workload": "thinker-shaped batched decode: 64 sessions, lognormal context "
                                "(median 4096, sigma 1, clipped [512,16384]), 32/4 heads GQA, "
-                               "head_dim 128, 16-token blocks, shuffled pool 1.25x",
+                               "head_dim 128, 16-token blocks, shuffled pool 1.25x; lengths given "
+                               "on the device and the host",
                    "sessions": 64, "tokens": int(dec["case"].context_lens.sum()),
-                   "algorithmic_mb_per_step": round(dec["alg_bytes"] / 1e6, 2)},
+                   "algorithmic_mb_per_step": round(dec["alg_bytes"] / 1e6, 2),
+                   "schedule": dec["schedule"]},
+        "decode_call_us": dec["per_call"],
+        "decode_schedule_in_kernel": {"us_per_launch": round(dec["device_ms"] * 1e3, 2),
+                                      "frac_hbm_peak": round(dec["alg_bytes"] / (dec["device_ms"] * 1e-3) / 1e9 /
+                                                             HBM_PEAK_GBS, 4)},
         "roofline": {"bound": "hbm", "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic("decode", source_digest("decode.hip"))},

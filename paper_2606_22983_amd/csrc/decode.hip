@@ -95,12 +95,16 @@ struct DecodeArgs {
 
 // A schedule planned on the host (paged_attn_decode with host lengths),
 // passed by value in the kernel arguments: workgroup w runs items
-// item[start[w] .. start[w + 1]), each packed as session (bits 0..11), KV head
-// (12..19), split (20..30) and "last split the plan gives the session" (31).
+// start[w] .. start[w + 1] - 1.  Items are 32-bit words (session in bits
+// 0..11, KV head 12..19, split 20..30, "last split the plan gives the
+// session" 31), or, when start[kPlanMaxWg + 1] is 1, 16-bit halves of them
+// (session 0..9, KV head 10..11, split 12..14, last split 15), which holds
+// twice as many items for batches of at most 1024 sessions, 4 KV heads and 8
+// splits per session.
 constexpr int kPlanMaxWg = 256;
-constexpr int kPlanMaxItems = 640;
+constexpr int kPlanMaxItems = 640;                     // 32-bit items (1280 16-bit ones)
 struct DecodeHostPlan {
-    uint16_t start[kPlanMaxWg + 2];            // (+1 keeps the items 4-byte aligned)
+    uint16_t start[kPlanMaxWg + 2];            // [kPlanMaxWg + 1]: 1 = 16-bit items
     uint32_t item[kPlanMaxItems];
 };
 struct NoPlan {
@@ -110,7 +114,12 @@ template <bool kHost>
 using PlanArg = typename std::conditional<kHost, DecodeHostPlan, NoPlan>::type;
 __device__ __forceinline__ uint32_t plan_start(const DecodeHostPlan &p, int w) { return p.start[w]; }
 __device__ __forceinline__ uint32_t plan_start(const NoPlan &, int) { return 0; }
-__device__ __forceinline__ uint32_t plan_item(const DecodeHostPlan &p, int i) { return p.item[i]; }
+// Item i in the 32-bit layout.
+__device__ __forceinline__ uint32_t plan_item(const DecodeHostPlan &p, int i) {
+    if (p.start[kPlanMaxWg + 1] == 0) return p.item[i];
+    const uint32_t h = (p.item[i >> 1] >> ((i & 1) * 16)) & 0xFFFFu;
+    return (h & 0x3FFu) | (((h >> 10) & 3u) << 12) | (((h >> 12) & 7u) << 20) | ((h >> 15) << 31);
+}
 
 template <int D>
 struct BlockRegs {
@@ -831,16 +840,20 @@ bool plan_decode_host(int S, int num_kv_heads, const int32_t *lens_host, int app
         int s, split, g;
     };
     std::vector<Item> items;
+    bool compact = false;                      // 16-bit items
     auto build = [&](int T) -> bool {
         items.clear();
+        const int64_t ns_max = (max_len + T - 1) / T;
+        compact = S <= 1024 && num_kv_heads <= 4 && ns_max <= 8;
+        const int cap = compact ? 2 * kPlanMaxItems : kPlanMaxItems;
+        if (ns_max > 2047) return false;
         for (int s = 0; s < S; ++s) {
             const int64_t L = std::max<int64_t>((int64_t)lens_host[s] + appended, 1);
             const int ns = (int)((L + T - 1) / T);
-            if (ns > 2047) return false;
             for (int k = 0; k < ns; ++k)
                 for (int g = 0; g < num_kv_heads; ++g)
                     items.push_back({std::min<int64_t>(L, (int64_t)(k + 1) * T) - (int64_t)k * T, s, k, g});
-            if ((int)items.size() > kPlanMaxItems) return false;
+            if ((int)items.size() > cap) return false;
         }
         std::stable_sort(items.begin(), items.end(),
                          [](const Item &x, const Item &y) { return x.tokens > y.tokens; });
@@ -862,7 +875,7 @@ bool plan_decode_host(int S, int num_kv_heads, const int32_t *lens_host, int app
         return worst;
     };
     const int unit = 1024;
-    int cands[3] = {(int)((max_len + unit - 1) / unit * unit), 2048, 4096};
+    int cands[4] = {(int)((max_len + unit - 1) / unit * unit), 2048, 3072, 4096};
     int best_t = 0;
     int64_t best_cost = INT64_MAX;
     for (int T : cands) {
@@ -883,13 +896,23 @@ bool plan_decode_host(int S, int num_kv_heads, const int32_t *lens_host, int app
     for (int w : owner) ++count[w + 1];
     for (int w = 0; w < W; ++w) count[w + 1] += count[w];
     for (int w = 0; w <= W; ++w) plan.start[w] = (uint16_t)count[w];
+    plan.start[kPlanMaxWg + 1] = compact ? 1 : 0;
     std::vector<int> fill(count.begin(), count.end() - 1);
     for (size_t i = 0; i < items.size(); ++i) {
         const Item &it = items[i];
         const int64_t L = std::max<int64_t>((int64_t)lens_host[it.s] + appended, 1);
         const bool last = (int64_t)(it.split + 1) * best_t >= L;
-        plan.item[fill[owner[i]]++] = (uint32_t)it.s | ((uint32_t)it.g << 12) | ((uint32_t)it.split << 20) |
-                                      (last ? 0x80000000u : 0u);
+        const int slot = fill[owner[i]]++;
+        if (compact) {
+            const uint32_t h = (uint32_t)it.s | ((uint32_t)it.g << 10) | ((uint32_t)it.split << 12) |
+                               (last ? 0x8000u : 0u);
+            uint32_t &word = plan.item[slot >> 1];
+            const int sh = (slot & 1) * 16;
+            word = (word & ~(0xFFFFu << sh)) | (h << sh);
+        } else {
+            plan.item[slot] = (uint32_t)it.s | ((uint32_t)it.g << 12) | ((uint32_t)it.split << 20) |
+                              (last ? 0x80000000u : 0u);
+        }
     }
     t_out = best_t;
     any_split = best_t < max_len;

@@ -327,23 +327,25 @@ def test_schedule_talker_batch_is_planned_on_host_without_merge(lib):
         assert split >= int(l0.max()) + t + 1 and split % 1024 == 0
 
 
-def test_schedule_thinker_batch_keeps_the_device_schedule(lib):
-    """The lognormal thinker batch (64 sessions up to 16k keys): the plans that fit
-    the argument block are no better than the device's 1024-token splits."""
+def test_schedule_thinker_batch_splits_long_sessions(lib):
+    """The lognormal thinker batch (64 sessions up to 16k keys): 2048-token splits
+    (856 items, in the 16-bit item form) balance better than the device's
+    1024-token snake; the merge runs.  Without host lengths: the device schedule."""
     from paper_2606_22983_amd import workloads as W
     lens = W.thinker_lengths()
     maxb = int(((lens + 15) // 16).max())
-    assert _sched(lib, 4, 32, lens, maxb) == (LS_OK, 1024, False, True)
+    assert _sched(lib, 4, 32, lens, maxb) == (LS_OK, 2048, True, True)
     assert _sched(lib, 4, 32, lens, maxb, host=False) == (LS_OK, 1024, False, True)
 
 
 def test_schedule_mixed_batch_splits_long_sessions(lib):
-    """Mostly ~2k-key sessions and ten of 8000 keys: the host splits at 2048 tokens
-    and the merge runs."""
+    """Mostly ~2k-key sessions and ten of 8000 keys: the host splits the long ones
+    (a multiple of 1024 below 8000) and the merge runs."""
     import numpy as np
     rng = np.random.default_rng(1)
     lens = np.concatenate([rng.integers(1500, 2040, 200), np.full(10, 8000)])
-    assert _sched(lib, 2, 16, lens, 600) == (LS_OK, 2048, True, True)
+    r, split, host, merge = _sched(lib, 2, 16, lens, 600)
+    assert r == LS_OK and host and merge and split % 1024 == 0 and 2048 <= split < 8000
 
 
 def test_schedule_rejects_bad_host_lengths(lib):

@@ -279,15 +279,15 @@ def test_talker_32_steps_host_planned(kv, oracle_lib):
 
 @pytest.mark.parametrize("append", [False, True])
 def test_host_planned_with_splits_and_merge(kv, oracle_lib, append):
-    """Mostly ~2k-key sessions and a few of 8000: the host splits at 2048 tokens
-    (several chunks of 1024 per item) and the merge runs."""
+    """Mostly ~2k-key sessions and a few of 8000: the host splits the long sessions
+    (items of several 1024-token chunks) and the merge runs."""
     rng = np.random.default_rng(90 + append)
     lens = np.concatenate([rng.integers(1500, 2040, 200), np.full(10, 8000), [1, 2047, 2048, 4097]])
     pool, tables, q, kn, vn = _synthetic(rng, lens, 16, 2, 128, append)
     dp = DevicePool(kv, pool, 128)
     sc = _host_planned(kv, dp, len(lens), 16, tables.shape[1], lens, append)
     log("schedule: %s" % sc)
-    assert sc["host_planned"] and sc["merge"] and sc["split_tokens"] == 2048
+    assert sc["host_planned"] and sc["merge"] and sc["split_tokens"] >= 2048
     ws = torch.zeros(kv.decode_workspace_bytes(dp.pool, len(lens), 16, tables.shape[1]), dtype=torch.uint8,
                      device="cuda")
     out = torch.empty((len(lens), 16, 128), dtype=torch.bfloat16, device="cuda")
@@ -334,3 +334,21 @@ def test_host_plan_device_lengths_disagree(kv, oracle_lib):
     kv.paged_attn_decode(dp2.pool, 0, bf16_dev(q2), i32_dev(tables2), i32_dev(real), 0.0884, out3, ws2,
                          context_lens_host=claimed)
     assert kv.ls_device_errors() & kv.LS_DEVERR_LENGTH
+
+
+def test_thinker_decode_full_host_planned(kv, oracle_lib):
+    """The full thinker batch with host lengths: 2048-token splits in the 16-bit
+    item form, two chunks per full split, merge."""
+    case = W.thinker_decode()
+    dp = DevicePool(kv, case.pool.data, 128)
+    sc = kv.ls_decode_schedule(dp.pool, case.num_sessions, case.num_q_heads, case.block_tables.shape[1],
+                               context_lens_host=case.context_lens)
+    assert sc["host_planned"] and sc["merge"], sc
+    ws = torch.zeros(kv.decode_workspace_bytes(dp.pool, case.num_sessions, case.num_q_heads,
+                                               case.block_tables.shape[1]), dtype=torch.uint8, device="cuda")
+    out = torch.empty((case.num_sessions, case.num_q_heads, 128), dtype=torch.bfloat16, device="cuda")
+    kv.paged_attn_decode(dp.pool, 0, bf16_dev(case.q[0]), i32_dev(case.block_tables), i32_dev(case.context_lens),
+                         case.scale, out, ws, context_lens_host=case.context_lens)
+    ref = oracle_lib.decode(case.pool.data, 16, 128, 0, case.q[0], case.block_tables, case.context_lens, case.scale)
+    assert_attn_close(out, ref, "thinker decode, host-planned (split %d)" % sc["split_tokens"])
+    assert kv.ls_device_errors() == 0
