@@ -13,9 +13,9 @@ and the KV-block restore/stash scatter legs (48 layers x 4 KV heads x 128 dims,
 side stream.  Inputs are seeded synthetic sessions, resident in HBM before the
 timed region starts.  ``cpu_baseline`` is the CPU oracle timed on this host.
 
-Usage: python bench.py [--steps K] [--warmup W] [--legs decode,prefill,talker,restore,pipeline,kvm,sched,calib]
-(decode always runs; "calib" adds a 1 GiB plain device copy used to scale the
-rocprofv3 HBM-traffic counters.)
+Usage: python bench.py [--steps K] [--warmup W] [--legs decode,prefill,talker,restore,overlap,pipeline,kvm,sched,calib]
+(the JSON line's headline needs "decode", which "overlap" also runs; "calib" adds
+a 1 GiB plain device copy used to scale the rocprofv3 HBM-traffic counters.)
 """
 import argparse
 import hashlib
@@ -44,7 +44,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--legs", default="decode,prefill,talker,restore,pipeline,kvm,sched")
+    ap.add_argument("--legs", default="decode,prefill,talker,restore,overlap,pipeline,kvm,sched",
+                    help="decode (the headline), prefill, talker, restore (scatter, gather, host leg), "
+                         "overlap (restores beside decode), pipeline, kvm, sched, calib")
     ap.add_argument("--reps", type=int, default=60, help="repetitions of the timed unit per leg")
     ap.add_argument("--prefill-reps", type=int, default=60)
     ap.add_argument("--restore-reps", type=int, default=50)
@@ -459,6 +461,7 @@ def restore_leg(torch, kv, W, args, dec):
 
     # restore on a side stream while the thinker decode repeats on the main stream
     side = torch.cuda.Stream()
+    overlaps = dec is not None
 
     def overlap_decode(start_side, dec_stream=stream, side_stream=side, alone=False):
         n_dec = 0
@@ -486,56 +489,61 @@ def restore_leg(torch, kv, W, args, dec):
                 "side_ms": round(ev_side_start.elapsed_time(ev_side_end), 3),
                 "us": round(dtimer.mean_ms() * 1e3, 2) if n_dec else float("nan")}
 
-    # Decode alone, timed the same way (one event pair per call, a sync every
-    # 16 calls): the reference for every slowdown below.
-    dec_alone_ms = overlap_decode(None, alone=True)["us"] * 1e-3
-    log("decode alone, single calls: %.1f us" % (dec_alone_ms * 1e3))
-    ov = overlap_decode(lambda st: kv.kv_blocks_restore(pool, b, staging, stream=st))
-    n_dec, side_ms, dec_conc_ms = ov["steps"], ov["side_ms"], ov["us"] * 1e-3
-    agg = (2.0 * payload + n_dec * dec["alg_bytes"]) / ov["makespan"] / 1e9
-    log("overlap: restore %.2f ms on the side stream, %d decode steps at %.1f us (alone %.1f us)" % (
-        side_ms, n_dec, dec_conc_ms * 1e3, dec_alone_ms * 1e3))
+    curve, best, part, dev_overlap = [], None, {}, {}
+    if overlaps:
+        # Decode alone, timed the same way (one event pair per call, a sync every
+        # 16 calls): the reference for every slowdown below.
+        dec_alone_ms = overlap_decode(None, alone=True)["us"] * 1e-3
+        log("decode alone, single calls: %.1f us" % (dec_alone_ms * 1e3))
+        ov = overlap_decode(lambda st: kv.kv_blocks_restore(pool, b, staging, stream=st))
+        n_dec, side_ms, dec_conc_ms = ov["steps"], ov["side_ms"], ov["us"] * 1e-3
+        agg = (2.0 * payload + n_dec * dec["alg_bytes"]) / ov["makespan"] / 1e9
+        log("overlap: restore %.2f ms on the side stream, %d decode steps at %.1f us (alone %.1f us)" % (
+            side_ms, n_dec, dec_conc_ms * 1e3, dec_alone_ms * 1e3))
+        dev_overlap = {"restore_side_stream_ms": round(side_ms, 3), "decode_steps": n_dec,
+                       "decode_us_alone": round(dec_alone_ms * 1e3, 2),
+                       "decode_us_concurrent": round(dec_conc_ms * 1e3, 2),
+                       "decode_slowdown_pct": round(100 * (dec_conc_ms / dec_alone_ms - 1), 1),
+                       "aggregate_gbs": round(agg, 1)}
 
-    # Bounded interference (§5.2: background preloads must not hurt live
-    # requests): the same device-staged restore on a side stream, paced to a
-    # payload rate, beside the thinker decode.  Each point restores a block
-    # count sized to run ~40 ms at its rate.
-    curve = []
-    for gbps in args.rates:
-        nb_b = n if gbps == 0 else int(min(n, max(256, gbps * 1e9 * 0.04 // per_block)))
-        ids_b = b[:nb_b]
-        pt = overlap_decode(lambda st: kv.kv_blocks_restore(pool, ids_b, staging, max_gbps=gbps, stream=st))
-        gbs_b = 2.0 * nb_b * per_block / (pt["side_ms"] * 1e-3) / 1e9
-        curve.append({"max_gbps_payload": gbps, "blocks": nb_b, "restore_ms": pt["side_ms"],
-                      "restore_gbs_2n": round(gbs_b, 1), "decode_steps": pt["steps"],
-                      "decode_us_concurrent": pt["us"],
-                      "decode_slowdown_pct": round(100 * (pt["us"] * 1e-3 / dec_alone_ms - 1), 1)})
-        log("paced restore: cap %s GB/s payload, %.0f GB/s (2N) over %.1f ms, decode %.1f us (+%.1f%%)" % (
-            gbps or "none", gbs_b, pt["side_ms"], pt["us"], curve[-1]["decode_slowdown_pct"]))
-    within = [p for p in curve if p["decode_slowdown_pct"] <= 10.0]
-    best = max(within, key=lambda p: p["restore_gbs_2n"]) if within else None
+        # Bounded interference (§5.2: background preloads must not hurt live
+        # requests): the same device-staged restore on a side stream, paced to a
+        # payload rate, beside the thinker decode.  Each point restores a block
+        # count sized to run ~40 ms at its rate.
+        for gbps in args.rates:
+            nb_b = n if gbps == 0 else int(min(n, max(256, gbps * 1e9 * 0.04 // per_block)))
+            ids_b = b[:nb_b]
+            pt = overlap_decode(lambda st: kv.kv_blocks_restore(pool, ids_b, staging, max_gbps=gbps, stream=st))
+            gbs_b = 2.0 * nb_b * per_block / (pt["side_ms"] * 1e-3) / 1e9
+            curve.append({"max_gbps_payload": gbps, "blocks": nb_b, "restore_ms": pt["side_ms"],
+                          "restore_gbs_2n": round(gbs_b, 1), "decode_steps": pt["steps"],
+                          "decode_us_concurrent": pt["us"],
+                          "decode_slowdown_pct": round(100 * (pt["us"] * 1e-3 / dec_alone_ms - 1), 1)})
+            log("paced restore: cap %s GB/s payload, %.0f GB/s (2N) over %.1f ms, decode %.1f us (+%.1f%%)" % (
+                gbps or "none", gbs_b, pt["side_ms"], pt["us"], curve[-1]["decode_slowdown_pct"]))
+        within = [p for p in curve if p["decode_slowdown_pct"] <= 10.0]
+        best = max(within, key=lambda p: p["restore_gbs_2n"]) if within else None
 
-    # The same restore confined to a few CUs (a CU-masked side stream, the
-    # knob the paper's preloader would use to bound interference), decode on a
-    # stream masked to the other CUs; the library sizes both persistent grids
-    # to their stream's CUs.
-    part = {}
-    masked = cu_masked_streams(torch, args.restore_cus)
-    if masked:
-        dec_st, res_st, n_cus, _ = masked
-        solo = overlap_decode(None, dec_stream=dec_st, side_stream=res_st, alone=True)
-        conc = overlap_decode(lambda st: kv.kv_blocks_restore(pool, b, staging, stream=st),
-                              dec_stream=dec_st, side_stream=res_st)
-        part = {"restore_cus": args.restore_cus, "decode_cus": n_cus - args.restore_cus,
-                "restore_side_stream_ms": conc["side_ms"],
-                "restore_gbs": round(2.0 * payload / (conc["side_ms"] * 1e-3) / 1e9, 1),
-                "decode_steps": conc["steps"], "decode_us_alone_all_cus": round(dec_alone_ms * 1e3, 2),
-                "decode_us_alone_own_cus": solo["us"], "decode_us_concurrent": conc["us"],
-                "decode_slowdown_pct": round(100 * (conc["us"] * 1e-3 / dec_alone_ms - 1), 1)}
-        log("partitioned overlap: restore on %d CUs %.2f ms (%.0f GB/s), decode on %d CUs %.1f us alone, %.1f us "
-            "concurrent" % (args.restore_cus, conc["side_ms"], part["restore_gbs"], n_cus - args.restore_cus,
-                            solo["us"], conc["us"]))
-        destroy_streams(masked)
+        # The same restore confined to a few CUs (a CU-masked side stream, the
+        # knob the paper's preloader would use to bound interference), decode on a
+        # stream masked to the other CUs; the library sizes both persistent grids
+        # to their stream's CUs.
+        masked = cu_masked_streams(torch, args.restore_cus)
+        if masked:
+            dec_st, res_st, n_cus, _ = masked
+            solo = overlap_decode(None, dec_stream=dec_st, side_stream=res_st, alone=True)
+            conc = overlap_decode(lambda st: kv.kv_blocks_restore(pool, b, staging, stream=st),
+                                  dec_stream=dec_st, side_stream=res_st)
+            part = {"restore_cus": args.restore_cus, "decode_cus": n_cus - args.restore_cus,
+                    "restore_side_stream_ms": conc["side_ms"],
+                    "restore_gbs": round(2.0 * payload / (conc["side_ms"] * 1e-3) / 1e9, 1),
+                    "decode_steps": conc["steps"], "decode_us_alone_all_cus": round(dec_alone_ms * 1e3, 2),
+                    "decode_us_alone_own_cus": solo["us"], "decode_us_concurrent": conc["us"],
+                    "decode_slowdown_pct": round(100 * (conc["us"] * 1e-3 / dec_alone_ms - 1), 1)}
+            log("partitioned overlap: restore on %d CUs %.2f ms (%.0f GB/s), decode on %d CUs %.1f us alone, %.1f us "
+                "concurrent" % (args.restore_cus, conc["side_ms"], part["restore_gbs"], n_cus - args.restore_cus,
+                                solo["us"], conc["us"]))
+            destroy_streams(masked)
 
     # host leg: pinned host staging -> device ring -> scatter, through the same call
     host = {}
@@ -554,6 +562,7 @@ def restore_leg(torch, kv, W, args, dec):
                 "pcie_peak_gbs": PCIE_PEAK_GBS}
         log("host leg: restore %.1f GB/s, stash %.1f GB/s over %.1f GiB" % (
             host["restore_gbs"], host["stash_gbs"], host["gib"]))
+    if hb > 0 and overlaps:
         # The preload of the paper's path (host DRAM -> HBM, PCIe-bound) on a
         # side stream while the thinker decode runs on the main stream.
         hdec = overlap_decode(lambda st: kv.kv_blocks_restore(pool, ids_h, hbuf, ring=ring, stream=st))
@@ -595,11 +604,7 @@ def restore_leg(torch, kv, W, args, dec):
                          "traffic": measured_traffic("block_copy", source_digest("blockcopy.hip"))},
             "overlap_host_preload": host_overlap,
             "overlap_device_staging_partitioned": part,
-            "overlap_device_staging": {"restore_side_stream_ms": round(side_ms, 3), "decode_steps": n_dec,
-                                       "decode_us_alone": round(dec_alone_ms * 1e3, 2),
-                                       "decode_us_concurrent": round(dec_conc_ms * 1e3, 2),
-                                       "decode_slowdown_pct": round(100 * (dec_conc_ms / dec_alone_ms - 1), 1),
-                                       "aggregate_gbs": round(agg, 1)},
+            "overlap_device_staging": dev_overlap,
             "host_leg": host}
 
 
@@ -882,9 +887,7 @@ def main():
     log("device:", torch.cuda.get_device_name(0), "| library:", kv.version())
 
     calib = calib_leg(torch, args) if "calib" in legs else None
-    dec = decode_leg(torch, kv, W, args)
-    dec_gbs = dec["alg_bytes"] / (dec["kernel_ms"] * 1e-3) / 1e9
-    wall_gbs = dec["alg_bytes"] * args.steps / dec["wall_s"] / 1e9
+    dec = decode_leg(torch, kv, W, args) if legs & {"decode", "overlap"} else None
     extra = {}
     if "prefill" in legs:
         extra["prefill"] = prefill_leg(torch, kv, W, args)
@@ -893,7 +896,7 @@ def main():
         extra["talker"] = talker_leg(torch, kv, W, args)
         torch.cuda.empty_cache()
     if "restore" in legs:
-        extra["restore"] = restore_leg(torch, kv, W, args, dec)
+        extra["restore"] = restore_leg(torch, kv, W, args, dec if "overlap" in legs else None)
     if "pipeline" in legs:
         extra["restore_prefill_pipeline"] = pipeline_leg(torch, kv, W, args)
         torch.cuda.empty_cache()
@@ -903,6 +906,11 @@ def main():
         extra["scheduler"] = sched_leg()
     if calib:
         extra["calibration_copy"] = calib
+    if dec is None:                # a partial run (profiling one leg): no headline
+        print(json.dumps({"metric": None, "value": None, "legs": extra}), flush=True)
+        return
+    dec_gbs = dec["alg_bytes"] / (dec["kernel_ms"] * 1e-3) / 1e9
+    wall_gbs = dec["alg_bytes"] * args.steps / dec["wall_s"] / 1e9
     cpu = None if args.no_cpu_baseline else cpu_baseline(dec, W)
 
     line = {

@@ -37,7 +37,7 @@
 // tile built from k_new / v_new, and then writes it to the slot for the next
 // steps.
 #include <algorithm>
-#include <queue>
+#include <cstdlib>
 #include <type_traits>
 #include <vector>
 
@@ -795,128 +795,240 @@ namespace {
 
 // Host-side schedule (see DecodeHostPlan).  Chooses the split size T (a
 // multiple of 1024 tokens, at least t_min) among: no split at all (T covers
-// the longest session), 2048 and 4096, by the cost of a longest-first
+// the longest session), 2048, 3072 and 4096, by the cost of a longest-first
 // assignment of the items to the workgroups: the most loaded workgroup's
 // tokens plus a fixed cost per item, plus the merge kernel's cost when some
 // session is split.  Items then go, longest first, to the least loaded
-// workgroup; each workgroup runs its items in that order.  Returns false when
-// the batch does not fit the argument block (more workgroups or items), or
-// when the device's own schedule (split size t_dev, snake-dealt rows; its merge
-// launched whenever dev_merges) is estimated to finish no later.
+// workgroup; each workgroup runs its items in that order.  Gives up (false)
+// when the batch does not fit the argument block (more workgroups or items),
+// or when the device's own schedule (split size t_dev, snake-dealt rows; its
+// merge launched whenever dev_merges) is estimated to finish no later.
 constexpr int64_t kItemCostTokens = 64;      // per-item start-up, in tokens of streaming
 constexpr int64_t kMergeCostTokens = 256;    // the split merge launch, in tokens
 constexpr int64_t kScheduleCostTokens = 128; // the device schedule in the kernel prologue, in tokens
+
+// Least-loaded-first assignment over W workgroups: a binary min-heap of keys
+// load * 512 + workgroup (W <= 256), ties to the lower workgroup.
+struct LoadHeap {
+    uint64_t key[kPlanMaxWg];
+    int n;
+    void reset(int W) {
+        n = W;
+        for (int w = 0; w < W; ++w) key[w] = (uint64_t)w;     // already a heap
+    }
+    // Adds `cost` to the least loaded workgroup; returns it and its new load.
+    int add(int64_t cost, int64_t &new_load) {
+        const uint64_t k = key[0] + ((uint64_t)cost << 9);
+        const int w = (int)(k & 511u);
+        new_load = (int64_t)(k >> 9);
+        int i = 0;                               // sift the grown key down
+        for (;;) {
+            const int l = 2 * i + 1;
+            if (l >= n) break;
+            const int m = (l + 1 < n && key[l + 1] < key[l]) ? l + 1 : l;
+            if (key[m] >= k) break;
+            key[i] = key[m];
+            i = m;
+        }
+        key[i] = k;
+        return w;
+    }
+};
+
+struct PlanRow {
+    int32_t tokens, s, split;
+};
+
 bool plan_decode_host(int S, int num_kv_heads, const int32_t *lens_host, int appended, int W, int t_min,
                       int t_dev, bool dev_merges, DecodeHostPlan &plan, int &t_out, bool &any_split) {
     if (W < 1 || W > kPlanMaxWg || S > 4096 || num_kv_heads > 255) return false;
     int64_t max_len = 1;
     for (int s = 0; s < S; ++s) max_len = std::max<int64_t>(max_len, (int64_t)lens_host[s] + appended);
+    auto len_of = [&](int s) { return std::max<int64_t>((int64_t)lens_host[s] + appended, 1); };
     // The device schedule's estimated makespan: rows of full splits in session
     // order, then the short rows by block count (largest first), each row's
     // heads consecutive, dealt in snake order.
-    int64_t dev_cost;
-    {
-        std::vector<int64_t> rows;
-        std::vector<std::pair<int, int>> shorts;   // (-blocks, session)
-        for (int s = 0; s < S; ++s) {
-            const int64_t L = std::max<int64_t>((int64_t)lens_host[s] + appended, 0);
-            for (int64_t k = 0; k < L / t_dev; ++k) rows.push_back(t_dev);
-            if (L == 0 || L % t_dev) shorts.push_back({-(int)((L % t_dev + kBlock - 1) / kBlock), s});
-        }
-        std::stable_sort(shorts.begin(), shorts.end());
-        for (const auto &r : shorts) rows.push_back((int64_t)(-r.first) * kBlock);
-        std::vector<int64_t> load(W, 0);
-        int64_t item = 0;
-        for (int64_t t : rows)
-            for (int g = 0; g < num_kv_heads; ++g, ++item) {
-                const int64_t round = item / W, w = item % W;
-                load[(round & 1) ? W - 1 - w : w] += t + kItemCostTokens;
+    static thread_local std::vector<int64_t> dev_load;
+    static thread_local std::vector<int32_t> shorts;
+    dev_load.assign(W, 0);
+    shorts.clear();
+    int dw = 0, dround = 0;                     // snake position: round parity and slot
+    auto deal = [&](int64_t tokens) {
+        for (int g = 0; g < num_kv_heads; ++g) {
+            dev_load[(dround & 1) ? W - 1 - dw : dw] += tokens + kItemCostTokens;
+            if (++dw == W) {
+                dw = 0;
+                ++dround;
             }
-        dev_cost = *std::max_element(load.begin(), load.end()) + kScheduleCostTokens +
-                   (dev_merges ? kMergeCostTokens : 0);
-    }
-    struct Item {
-        int64_t tokens;
-        int s, split, g;
+        }
     };
-    std::vector<Item> items;
-    bool compact = false;                      // 16-bit items
+    for (int s = 0; s < S; ++s) {
+        const int64_t L = std::max<int64_t>((int64_t)lens_host[s] + appended, 0);
+        for (int64_t k = 0; k < L / t_dev; ++k) deal(t_dev);
+        if (L == 0 || L % t_dev) shorts.push_back((int32_t)((L % t_dev + kBlock - 1) / kBlock));
+    }
+    std::stable_sort(shorts.begin(), shorts.end(), std::greater<int32_t>());
+    for (int32_t b : shorts) deal((int64_t)b * kBlock);
+    const int64_t dev_cost = *std::max_element(dev_load.begin(), dev_load.end()) + kScheduleCostTokens +
+                             (dev_merges ? kMergeCostTokens : 0);
+
+    // Rows (session, split) of a split size, longest first (ties: session, split).
+    static thread_local std::vector<PlanRow> rows;
+    static thread_local LoadHeap heap;
+    bool compact = false;
     auto build = [&](int T) -> bool {
-        items.clear();
+        rows.clear();
         const int64_t ns_max = (max_len + T - 1) / T;
         compact = S <= 1024 && num_kv_heads <= 4 && ns_max <= 8;
-        const int cap = compact ? 2 * kPlanMaxItems : kPlanMaxItems;
+        const int64_t cap = compact ? 2 * kPlanMaxItems : kPlanMaxItems;
         if (ns_max > 2047) return false;
+        int64_t n_items = 0;
         for (int s = 0; s < S; ++s) {
-            const int64_t L = std::max<int64_t>((int64_t)lens_host[s] + appended, 1);
+            const int64_t L = len_of(s);
             const int ns = (int)((L + T - 1) / T);
+            n_items += (int64_t)ns * num_kv_heads;
+            if (n_items > cap) return false;
             for (int k = 0; k < ns; ++k)
-                for (int g = 0; g < num_kv_heads; ++g)
-                    items.push_back({std::min<int64_t>(L, (int64_t)(k + 1) * T) - (int64_t)k * T, s, k, g});
-            if ((int)items.size() > cap) return false;
+                rows.push_back({(int32_t)(std::min<int64_t>(L, (int64_t)(k + 1) * T) - (int64_t)k * T), s, k});
         }
-        std::stable_sort(items.begin(), items.end(),
-                         [](const Item &x, const Item &y) { return x.tokens > y.tokens; });
+        std::sort(rows.begin(), rows.end(), [](const PlanRow &x, const PlanRow &y) {
+            return x.tokens != y.tokens ? x.tokens > y.tokens : (x.s != y.s ? x.s < y.s : x.split < y.split);
+        });
         return true;
     };
-    typedef std::pair<int64_t, int> Load;      // (tokens, workgroup), least loaded on top
-    auto makespan = [&](std::vector<int> *owner) -> int64_t {
-        std::priority_queue<Load, std::vector<Load>, std::greater<Load>> heap;
-        for (int w = 0; w < W; ++w) heap.push(Load(0, w));
+    // LPT over the rows' items; optionally records the plan.  With a bound it
+    // stops as soon as the makespan reaches it.
+    auto assign = [&](int64_t bound, bool record) -> int64_t {
+        heap.reset(W);
         int64_t worst = 0;
-        for (size_t i = 0; i < items.size(); ++i) {
-            Load l = heap.top();
-            heap.pop();
-            l.first += items[i].tokens + kItemCostTokens;
-            worst = std::max(worst, l.first);
-            if (owner) (*owner)[i] = l.second;
-            heap.push(l);
+        int slot_of[kPlanMaxWg];
+        static thread_local std::vector<uint32_t> order;    // (workgroup << 16 | item) per item, in order
+        if (record) order.clear();
+        for (const PlanRow &r : rows)
+            for (int g = 0; g < num_kv_heads; ++g) {
+                int64_t nl;
+                const int w = heap.add(r.tokens + kItemCostTokens, nl);
+                worst = std::max(worst, nl);
+                if (!record && worst >= bound) return worst;    // cannot win
+                if (record) order.push_back(((uint32_t)w << 16) | (uint32_t)order.size());
+            }
+        if (!record) return worst;
+        // Per-workgroup item lists in assignment order.
+        int count[kPlanMaxWg + 1] = {0};
+        for (uint32_t o : order) ++count[(o >> 16) + 1];
+        for (int w = 0; w < W; ++w) count[w + 1] += count[w];
+        for (int w = 0; w <= W; ++w) plan.start[w] = (uint16_t)count[w];
+        plan.start[kPlanMaxWg + 1] = compact ? 1 : 0;
+        for (int w = 0; w < W; ++w) slot_of[w] = count[w];
+        size_t i = 0;
+        for (const PlanRow &r : rows) {
+            const bool last = (int64_t)(r.split + 1) * t_out >= len_of(r.s);
+            for (int g = 0; g < num_kv_heads; ++g, ++i) {
+                const int slot = slot_of[order[i] >> 16]++;
+                if (compact) {
+                    const uint32_t h = (uint32_t)r.s | ((uint32_t)g << 10) | ((uint32_t)r.split << 12) |
+                                       (last ? 0x8000u : 0u);
+                    uint32_t &word = plan.item[slot >> 1];
+                    const int sh = (slot & 1) * 16;
+                    word = (word & ~(0xFFFFu << sh)) | (h << sh);
+                } else {
+                    plan.item[slot] = (uint32_t)r.s | ((uint32_t)g << 12) | ((uint32_t)r.split << 20) |
+                                      (last ? 0x80000000u : 0u);
+                }
+            }
         }
         return worst;
     };
+    // Candidates are ranked by the snake dealing of their rows' items (linear
+    // time); the chosen one is then assigned longest-first to the least loaded
+    // workgroup, and kept only if that still beats the device schedule.
+    auto snake = [&]() -> int64_t {
+        static thread_local std::vector<int64_t> load;
+        load.assign(W, 0);
+        int w = 0, round = 0;
+        for (const PlanRow &r : rows)
+            for (int g = 0; g < num_kv_heads; ++g) {
+                load[(round & 1) ? W - 1 - w : w] += r.tokens + kItemCostTokens;
+                if (++w == W) {
+                    w = 0;
+                    ++round;
+                }
+            }
+        return *std::max_element(load.begin(), load.end());
+    };
     const int unit = 1024;
-    int cands[4] = {(int)((max_len + unit - 1) / unit * unit), 2048, 3072, 4096};
+    const int t_whole = (int)((max_len + unit - 1) / unit * unit);
+    const int cands[4] = {t_whole, 2048, 3072, 4096};
     int best_t = 0;
-    int64_t best_cost = INT64_MAX;
+    int64_t best_est = INT64_MAX;
     for (int T : cands) {
         T = std::max(T, t_min);
-        if (T % unit || T > (int)((max_len + unit - 1) / unit * unit) + unit) continue;
+        if (T % unit || T > t_whole) continue;
         if (!build(T)) continue;
-        const bool split = T < max_len;
-        const int64_t cost = makespan(nullptr) + (split ? kMergeCostTokens : 0);
-        if (cost < best_cost) {
-            best_cost = cost;
+        const int64_t est = snake() + (T < max_len ? kMergeCostTokens : 0);
+        if (est < best_est) {
+            best_est = est;
             best_t = T;
         }
     }
-    if (!best_t || best_cost >= dev_cost || !build(best_t)) return false;
-    std::vector<int> owner(items.size());
-    makespan(&owner);
-    std::vector<int> count(W + 1, 0);
-    for (int w : owner) ++count[w + 1];
-    for (int w = 0; w < W; ++w) count[w + 1] += count[w];
-    for (int w = 0; w <= W; ++w) plan.start[w] = (uint16_t)count[w];
-    plan.start[kPlanMaxWg + 1] = compact ? 1 : 0;
-    std::vector<int> fill(count.begin(), count.end() - 1);
-    for (size_t i = 0; i < items.size(); ++i) {
-        const Item &it = items[i];
-        const int64_t L = std::max<int64_t>((int64_t)lens_host[it.s] + appended, 1);
-        const bool last = (int64_t)(it.split + 1) * best_t >= L;
-        const int slot = fill[owner[i]]++;
-        if (compact) {
-            const uint32_t h = (uint32_t)it.s | ((uint32_t)it.g << 10) | ((uint32_t)it.split << 12) |
-                               (last ? 0x8000u : 0u);
-            uint32_t &word = plan.item[slot >> 1];
-            const int sh = (slot & 1) * 16;
-            word = (word & ~(0xFFFFu << sh)) | (h << sh);
-        } else {
-            plan.item[slot] = (uint32_t)it.s | ((uint32_t)it.g << 12) | ((uint32_t)it.split << 20) |
-                              (last ? 0x80000000u : 0u);
-        }
-    }
+    if (!best_t || !build(best_t)) return false;
     t_out = best_t;
     any_split = best_t < max_len;
-    return true;
+    const int64_t cost = assign(INT64_MAX, true) + (any_split ? kMergeCostTokens : 0);
+    return cost < dev_cost;
+}
+
+// The last host plans (one per batch shape), reused while every session keeps
+// its split count and the batch's tokens stay within 1/32 of the planned
+// ones: a decode loop's lengths grow by one token per step, which changes
+// neither the items nor, noticeably, their balance.
+struct CachedPlan {
+    bool used = false, host = false, split = false;
+    int S = 0, hkv = 0, appended = 0, W = 0, t_min = 0, t_dev = 0, T = 0;
+    bool dev_merges = false;
+    int64_t tokens = 0;
+    std::vector<uint16_t> nsplits;
+    DecodeHostPlan plan;
+};
+
+const CachedPlan *cached_decode_plan(int S, int hkv, const int32_t *lens_host, int appended, int W, int t_min,
+                                    int t_dev, bool dev_merges) {
+    static thread_local CachedPlan cache[4];
+    static thread_local int next_victim = 0;
+    int64_t tokens = 0;
+    for (int s = 0; s < S; ++s) tokens += (int64_t)lens_host[s] + appended;
+    for (CachedPlan &c : cache) {
+        if (!c.used || c.S != S || c.hkv != hkv || c.appended != appended || c.W != W || c.t_min != t_min ||
+            c.t_dev != t_dev || c.dev_merges != dev_merges)
+            continue;
+        if (std::llabs(tokens - c.tokens) * 32 > c.tokens) continue;
+        const int T = c.host ? c.T : t_dev;
+        bool same = true;
+        for (int s = 0; s < S && same; ++s) {
+            const int64_t L = std::max<int64_t>((int64_t)lens_host[s] + appended, 1);
+            same = (L + T - 1) / T == c.nsplits[s];
+        }
+        if (same) return &c;
+    }
+    CachedPlan &c = cache[next_victim];
+    next_victim = (next_victim + 1) % 4;
+    c.used = true;
+    c.S = S;
+    c.hkv = hkv;
+    c.appended = appended;
+    c.W = W;
+    c.t_min = t_min;
+    c.t_dev = t_dev;
+    c.dev_merges = dev_merges;
+    c.tokens = tokens;
+    c.host = plan_decode_host(S, hkv, lens_host, appended, W, t_min, t_dev, dev_merges, c.plan, c.T, c.split);
+    const int T = c.host ? c.T : t_dev;
+    c.nsplits.resize(S);
+    for (int s = 0; s < S; ++s) {
+        const int64_t L = std::max<int64_t>((int64_t)lens_host[s] + appended, 1);
+        c.nsplits[s] = (uint16_t)std::min<int64_t>((L + T - 1) / T, 65535);
+    }
+    return &c;
 }
 
 }  // namespace
@@ -925,13 +1037,10 @@ DecodeSchedule decode_schedule(const PoolGeom &p, int32_t num_sessions, const in
                                int32_t appended, const DecodePlan &plan, hipStream_t stream) {
     DecodeSchedule sc{plan.split_tokens, false, plan.max_splits > 1};
     if (context_lens_host) {
-        static thread_local DecodeHostPlan hp;
-        int T = 0;
-        bool split = false;
-        if (plan_decode_host(num_sessions, p.num_kv_heads, context_lens_host, appended, stream_cus(p, stream),
-                             std::max(plan.split_tokens, 1024), plan.split_tokens, plan.max_splits > 1, hp, T,
-                             split))
-            sc = DecodeSchedule{T, true, split};
+        const CachedPlan *c = cached_decode_plan(num_sessions, p.num_kv_heads, context_lens_host, appended,
+                                                 stream_cus(p, stream), std::max(plan.split_tokens, 1024),
+                                                 plan.split_tokens, plan.max_splits > 1);
+        if (c->host) sc = DecodeSchedule{c->T, true, c->split};
     }
     return sc;
 }
@@ -967,13 +1076,13 @@ hipError_t launch_decode(const PoolGeom &p, int layer, int32_t num_sessions, int
     dim3 cgrid(p.num_kv_heads, num_sessions);
     // Host lengths: the schedule is planned here and passed with the arguments.
     if (context_lens_host) {
-        static thread_local DecodeHostPlan hp;
-        int T = 0;
-        bool split = false;
-        if (plan_decode_host(num_sessions, p.num_kv_heads, context_lens_host, a.appended, (int)resident,
-                             std::max(plan.split_tokens, 1024), plan.split_tokens, plan.max_splits > 1, hp, T,
-                             split)) {
-            a.split_tokens = T;
+        const CachedPlan *c = cached_decode_plan(num_sessions, p.num_kv_heads, context_lens_host, a.appended,
+                                                 (int)resident, std::max(plan.split_tokens, 1024),
+                                                 plan.split_tokens, plan.max_splits > 1);
+        if (c->host) {
+            const DecodeHostPlan &hp = c->plan;
+            const bool split = c->split;
+            a.split_tokens = c->T;
             const dim3 grid((unsigned)resident);
             if (p.head_dim == 128)
                 hipLaunchKernelGGL((decode_kernel<128, 2, 8, true>), grid, dim3(kDecThreads), 0, stream, a, hp);
