@@ -373,10 +373,11 @@ ls_status kv_manager_append_blocks(ls_kv_manager *m, int32_t session, int32_t n,
  * speech and warm protections end) or finishes (running == 0: idle). */
 ls_status kv_manager_set_running(ls_kv_manager *m, int32_t session, int32_t running);
 
-/* Monitor inputs to T_next = T_play + T_reply (§5.1).  t_play_s: remaining
- * playback horizon, or < 0 when unknown (then unfinished_tokens x
- * seconds_per_token stands in).  observe_reply: one interval from playback
- * completion to the next completed user input (moving average). */
+/* Monitor inputs to T_next = T_play + T_reply (§5.1, the next-use estimate).
+ * t_play_s: seconds of the session's audio still to be played, or < 0 when
+ * unknown (then unfinished_tokens x seconds_per_token stands in).
+ * observe_reply: one measured gap between the end of the session's playback
+ * and the user's next finished utterance (averaged over the session). */
 ls_status kv_manager_set_playback(ls_kv_manager *m, int32_t session, double t_play_s,
                                   int64_t unfinished_tokens);
 ls_status kv_manager_observe_reply(ls_kv_manager *m, int32_t session, double interval_s);

@@ -3,7 +3,7 @@
 //
 // It implements the policy side of the paper's hierarchical KV manager:
 //   - next-use estimate T_next = T_play + T_reply per session (§5.1, Eq. for
-//     the next-use estimate): T_play is the remaining playback horizon, or,
+//     the next-use estimate): T_play is the audio still to be played, or,
 //     when the monitor gives none, unfinished response tokens times a playback
 //     rate (the progress-counter fallback of §5.1); T_reply is a per-session
 //     exponential moving average of observed reply intervals, or a workload
@@ -62,7 +62,7 @@ struct Session {
     bool warm = false;           // protected after a completed preload
     double warm_since = 0.0;
     uint32_t warm_epoch = 0;     // identifies the current protection in the FIFO
-    double t_play = -1.0;        // remaining playback horizon (s), < 0: unknown
+    double t_play = -1.0;        // audio still to be played (s), < 0: unknown
     int64_t unfinished_tokens = 0;
     bool has_reply = false;
     double reply_avg = 0.0;

@@ -307,7 +307,7 @@ class ManagerTrace:
 
     ``context_blocks[s]``: blocks of session s's reused multi-turn context at the
     start.  ``events``: tuples
-      ("play", s, t_play)       monitor update of the remaining playback horizon (s)
+      ("play", s, t_play)       monitor update: seconds of audio still to play
       ("pressure", n)           running requests need n more device blocks
       ("turn", s, t_avail, new_blocks, reply_s, t_play)
                                 speech start with t_avail seconds before the LLM
