@@ -22,20 +22,26 @@
 // one 16-byte LDS read.  Scores are exact fp32 sums of bf16 products; the
 // softmax scale is applied in fp32 (folding it into q before the MFMA would
 // round q * scale to bf16, an error that grows with the score magnitude).
-// Softmax statistics stay in fp32; a row's running max is raised (and O, l
-// rescaled) only when a unit's max exceeds it by more than 8 (log2 units),
-// which keeps every probability at most 256 and makes rescales rare.
+// Softmax statistics stay in fp32.  A row's running max m' is set from its
+// first 32 keys and raised only when a unit's probabilities, summed per lane,
+// exceed 2^16 (those sums are needed for the row sums anyway, so the common
+// path computes no maxima): then O and l are rescaled and the unit's
+// probabilities recomputed before its P V, so every probability that reaches
+// O is below 2^16.
 //
-// Pipeline: K runs one unit ahead of V.  Each 32-key unit takes two phases:
-// A computes the scores of unit u+1 while turning the exp2 arguments of unit
-// u into P; B accumulates P V of unit u while it tests the maxima of unit u+1
-// and scales its scores into exp2 arguments (S * scale * log2(e) - m').  Each MFMA
-// is followed by its share of the phase's VALU work, and the operands of the
-// next phase are read from LDS during the current one, so the softmax
-// arithmetic issues while the matrix core is busy and LDS latency stays
-// hidden.  Data moves from HBM straight into LDS (buffer loads with the
-// LDS-destination form: no register staging, no LDS write instructions),
-// three 64-key stages deep, one barrier per 64 keys.
+// Pipeline: K runs one unit ahead of P, and P one phase ahead of its P V.
+// Each 32-key unit takes two phases: A computes the scores of unit u+1 while
+// turning the exp2 arguments of unit u into P; B accumulates P V of unit u-1
+// while it scales the scores of unit u+1 into exp2 arguments
+// (S * scale * log2(e) - m'); after B the sums of unit u's P are tested, a
+// whole phase after they were computed, before unit u's P V in the next B.
+// Each MFMA is followed by its share of the phase's VALU work, and the
+// operands of the next phase are read from LDS during the current one, so the
+// softmax arithmetic issues while the matrix core is busy and LDS latency
+// stays hidden.  Data moves from HBM straight into LDS (buffer loads with the
+// LDS-destination form: no register staging, no LDS write instructions) two
+// 64-key stages ahead, into four stage buffers (a stage's V is read until the
+// tile after it), one barrier per 64 keys.
 //
 // Scheduling: all query tiles of one (session, KV head) pair run on one XCD,
 // so they stream the same keys through its L2; pairs are dealt to XCDs
@@ -61,7 +67,7 @@ constexpr int kPreThreads = kPreWaves * kWave;
 constexpr int kKeyTile = 64;             // keys per pipeline stage (4 blocks)
 constexpr int kBufferDword3P = 0x00020000;   // raw buffer, 32-bit data format
 constexpr float kLog2eP = 1.4426950408889634f;
-constexpr float kRescaleSlack = 8.0f;    // log2 units a row max may lag behind
+constexpr float kSumLimit = 65536.0f;    // per-lane sum of a unit's P above which m' is raised
 constexpr int kXcds = 8;                 // workgroups are dispatched round-robin over XCDs
 constexpr int kMaxPairs = 512;           // (session, KV head) pairs scheduled; more run in index order
 
@@ -198,16 +204,20 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     using C = Geo<D>;
     constexpr int KS = D / 32;           // 32-dim k-steps of QK
     constexpr int NDT = D / 16;          // 16-dim output tiles
-    // Three stages; separate arrays let the compiler track each one's loads.
+    // Four stage buffers (stage t in buffer t % 4); separate arrays let the
+    // compiler track each one's loads.
     __shared__ __attribute__((aligned(1024))) uint8_t k0[C::kStageBytes];
     __shared__ __attribute__((aligned(1024))) uint8_t k1[C::kStageBytes];
     __shared__ __attribute__((aligned(1024))) uint8_t k2[C::kStageBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t k3[C::kStageBytes];
     __shared__ __attribute__((aligned(1024))) uint8_t v0[C::kStageBytes];
     __shared__ __attribute__((aligned(1024))) uint8_t v1[C::kStageBytes];
     __shared__ __attribute__((aligned(1024))) uint8_t v2[C::kStageBytes];
+    __shared__ __attribute__((aligned(1024))) uint8_t v3[C::kStageBytes];
     __shared__ __attribute__((aligned(16))) int64_t sm_work[kMaxPairs];
     __shared__ int sm_items[kMaxPairs];
     __shared__ int sm_order[kMaxPairs];
+    __shared__ float sm_rank_work[kMaxPairs];
 
     const int tid = threadIdx.x;
     const int S = a.num_sessions;
@@ -219,10 +229,14 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     // ---- schedule.  Items are (session s, KV head g, query tile qt).  All query
     // tiles of one (s, g) pair run on one XCD, so they stream the same keys
     // through its L2 at about the same time.  Pairs are dealt to the 8 XCDs in
-    // snake order of decreasing work (longest-processing-time first); an XCD
-    // runs its pairs in that order, each pair's latest (longest) query tile
-    // first.  Workgroup i is dispatched to XCD i % 8 and is the (i / 8)-th
-    // item there; every workgroup derives the same schedule from the lengths.
+    // rounds of 8 in order of decreasing work: in each round the heaviest pair
+    // goes to the XCD with the least work so far, the next to the next-least,
+    // and so on (a longest-processing-time-first rule; the 4 or 8 KV heads of
+    // one session have equal work, and a fixed snake would send them to the
+    // same half of the XCDs every round).  An XCD runs its pairs in the order
+    // dealt, each pair's latest (longest) query tile first.  Workgroup i is
+    // dispatched to XCD i % 8 and is the (i / 8)-th item there; every
+    // workgroup derives the same schedule from the lengths.
     const int P = S * Hkv;
     // A turn longer than the grid's query tiles (max_new_len understated), a
     // negative turn or a negative context cannot be attended as given: flagged
@@ -255,13 +269,26 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
                 r += (w2.y > w) || (w2.y == w && q + 1 < p);
             }
             sm_order[r] = p;
+            sm_rank_work[r] = (float)w;
         }
         __syncthreads();
         const int xcd = (int)(blockIdx.x % kXcds);
         int slot = (int)(blockIdx.x / kXcds);
         int pick = -1;
+        // Every wave deals the rounds itself.  Lane 8 xi + xj compares the work
+        // of XCD xj with that of XCD xi; the ballot's byte xi then counts the
+        // XCDs ahead of XCD xi (less work, or equal work and a lower index),
+        // which is XCD xi's place in the round.  Work sums are floats: only
+        // their order matters, and every wave adds the same values in the same
+        // order.
+        const int xi = (tid % kWave) >> 3, xj = tid & 7;
+        float done = 0.f;                                 // work dealt to XCD xj so far
         for (int k = 0; kXcds * k < P; ++k) {
-            const int r = kXcds * k + ((k & 1) ? kXcds - 1 - xcd : xcd);
+            const float di = __shfl(done, xi);            // lane xi holds XCD xi
+            const uint64_t ahead = __ballot(done < di || (done == di && xj < xi));
+            const int r_j = kXcds * k + __popcll((ahead >> (8 * xj)) & 0xFF);
+            if (r_j < P) done += sm_rank_work[r_j];
+            const int r = kXcds * k + __popcll((ahead >> (8 * xcd)) & 0xFF);
             if (r >= P) break;
             const int cnt = sm_items[sm_order[r]];
             if (slot < cnt) {
@@ -361,11 +388,10 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     auto id_k = [&](int t) { return table_entry(table, 4 * t + 2 + blk, nb); };
     auto id_v = [&](int t) { return table_entry(table, 4 * t + blk, nb); };
 
-    float m[kRT], nm[kRT], lsum[kRT];     // running row maxima (raw scores),
-    f32x4 o[kRT][NDT];                    // -m * scale * log2(e), partial row sums
+    float nm[kRT], lsum[kRT];             // -m' (running row max * scale * log2 e),
+    f32x4 o[kRT][NDT];                    // partial row sums, unnormalised output
 #pragma unroll
     for (int rt = 0; rt < kRT; ++rt) {
-        m[rt] = -INFINITY;
         nm[rt] = 0.f;
         lsum[rt] = 0.f;
     }
@@ -374,7 +400,6 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) o[rt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
     const float sl2 = a.scale_log2;
-    const float slack_raw = kRescaleSlack / sl2;
     const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
 
     // ---- S^T = K Q^T of one 32-key unit for 2 key sub-tiles x 2 row tiles.
@@ -435,24 +460,12 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
                     if (4 * sb + i > lim) acc[rt][sb][i] = -INFINITY;
         }
     };
-    // Rescale test: a row's running max is raised (and its O and l rescaled)
-    // when the unit's max exceeds it by more than the slack.  The row max
-    // exceeds it iff one of the four lanes holding the row sees a local max
-    // that does, so the common path tests local maxima only.  scale > 0 is
-    // checked on the host, so masking and maxima commute with scaling.
-    float lm[kRT];
-    auto max_test = [&](const f32x4 (&acc)[kRT][2]) {
-        bool raise = false;
-#pragma unroll
-        for (int rt = 0; rt < kRT; ++rt) {
-            const f32x4 x0 = acc[rt][0], x1 = acc[rt][1];
-            lm[rt] = fmax3(fmax3(x0[0], x0[1], x0[2]), fmax3(x0[3], x1[0], x1[1]), fmax3(x1[2], x1[3], x1[3]));
-            raise = raise || lm[rt] > m[rt] + slack_raw;
-        }
-        return raise;
+    // Largest of a lane's 8 values of one row tile (NaN-propagating).
+    auto lane_max = [&](const f32x4 (&acc)[2]) {
+        const f32x4 x0 = acc[0], x1 = acc[1];
+        return fmax3(fmax3(x0[0], x0[1], x0[2]), fmax3(x0[3], x1[0], x1[1]), fmax3(x1[2], x1[3], x1[3]));
     };
-    // The rare raise: row maxima across the four lanes, then rescale.
-    // Scores -> exp2 arguments S * scale * log2(e) - m' (phase B, after the max test).
+    // Scores -> exp2 arguments S * scale * log2(e) - m' (phase B).
     auto scale_unit = [&](f32x4 (&acc)[kRT][2]) {
 #pragma unroll
         for (int rt = 0; rt < kRT; ++rt)
@@ -461,38 +474,53 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
 #pragma unroll
                 for (int i = 0; i < 4; ++i) acc[rt][sb][i] = __builtin_fmaf(acc[rt][sb][i], sl2, nm[rt]);
     };
-    // The raise, after scale_unit: the unit's exp2 arguments move with the max.
-    auto rescale = [&](f32x4 (&acc)[kRT][2]) {
-#pragma unroll
-        for (int rt = 0; rt < kRT; ++rt) {
-            const float m_new = __builtin_elementwise_maximum(m[rt], xmax16_32(lm[rt]));
-            const float alpha = __builtin_amdgcn_exp2f((m[rt] - m_new) * sl2);
-            lsum[rt] *= alpha;
-#pragma unroll
-            for (int dt = 0; dt < NDT; ++dt) o[rt][dt] *= alpha;
-            m[rt] = m_new;
-            const float nm_new = -m_new * sl2;
-            const float shift = nm_new - nm[rt];
-            nm[rt] = nm_new;
-            acc[rt][0] += shift;
-            acc[rt][1] += shift;
-        }
-    };
-    // P = exp2(S * scale * log2 e - m') in bf16 (B operand of PV) and row sums.
-    auto exp_unit = [&](const f32x4 (&acc)[kRT][2], bf16x8 (&pop)[kRT]) {
+    // P = exp2(S * scale * log2 e - m') in bf16 (B operand of PV), and the
+    // lane's sum of the rounded values per row tile.
+    auto exp_unit = [&](const f32x4 (&acc)[kRT][2], bf16x8 (&pop)[kRT], float (&us)[kRT]) {
 #pragma unroll
         for (int rt = 0; rt < kRT; ++rt) {
             uint32_t w[4];
+            us[rt] = 0.f;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const f32x4 &x = acc[rt][j >> 1];
                 const int i0 = 2 * (j & 1);
                 const bf16x2 pk = {(__bf16)__builtin_amdgcn_exp2f(x[i0]), (__bf16)__builtin_amdgcn_exp2f(x[i0 + 1])};
-                lsum[rt] = __builtin_amdgcn_fdot2_f32_bf16(pk, ones2, lsum[rt], false);
+                us[rt] = __builtin_amdgcn_fdot2_f32_bf16(pk, ones2, us[rt], false);
                 w[j] = __builtin_bit_cast(uint32_t, pk);
             }
             pop[rt] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
         }
+    };
+    // After the B phase that follows a unit's P (and before its P V): when
+    // some lane's sum exceeds the limit (a probability above 2^13, an infinite
+    // one included), the rows' maxima are raised to the unit's row maxima.  O
+    // and l (which hold the units before it) are rescaled, the exp2 arguments
+    // of the unit and of the next unit (already scaled) shifted, and the unit's
+    // P recomputed (at most 1 now).  Rows whose max did not move shift by 0.
+    // Then the unit's sums join l.
+    auto settle = [&](f32x4 (&acc)[kRT][2], f32x4 (&next)[kRT][2], bf16x8 (&pop)[kRT], float (&us)[kRT]) {
+        bool over = false;
+#pragma unroll
+        for (int rt = 0; rt < kRT; ++rt) over = over || us[rt] > kSumLimit;
+        if (__any(over)) {
+#pragma unroll
+            for (int rt = 0; rt < kRT; ++rt) {
+                const float shift = __builtin_elementwise_maximum(xmax16_32(lane_max(acc[rt])), 0.f);
+                const float alpha = __builtin_amdgcn_exp2f(-shift);
+                lsum[rt] *= alpha;
+#pragma unroll
+                for (int dt = 0; dt < NDT; ++dt) o[rt][dt] *= alpha;
+                nm[rt] -= shift;
+                acc[rt][0] -= shift;
+                acc[rt][1] -= shift;
+                next[rt][0] -= shift;
+                next[rt][1] -= shift;
+            }
+            exp_unit(acc, pop, us);
+        }
+#pragma unroll
+        for (int rt = 0; rt < kRT; ++rt) lsum[rt] += us[rt];
     };
     // Per-lane byte offset of the V chunk this lane reads, opaque for the same
     // reason as kroff.  Dims dt*16 + c16 of one lane are 256 bytes apart.
@@ -519,7 +547,7 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     constexpr int kPhaseMfma = 2 * KS * kRT;              // == NDT * kRT
     constexpr int kExpTrans = kRT * 4 * 2;                // exp phase: 2 exp ...
     constexpr int kExpValu = kRT * 4 * 2;                 // ... and cvt, dot2 per pair
-    constexpr int kMaxValu = kRT * 14;                    // max phase, scale FMAs
+    constexpr int kScaleValu = kRT * 8;                   // scale phase: the FMAs
     // Keeps the probabilities of a phase from being computed later (after the
     // masking branch that follows the phase).
     auto pin = [&](const bf16x8 (&pop)[kRT]) {
@@ -552,22 +580,29 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     };
 
     // ---- pipeline over 32-key units.  Key tile j (units 2j, 2j+1) reads
-    // stage j % 3: K of units 2j+1, 2j+2 and V of units 2j, 2j+1.  While it
-    // is processed, the loads of stage j+2 go into the third buffer pair (last
-    // read in tile j-1).  A tile runs four phases:
-    //   A0: scores of unit 2j+1 | P of unit 2j      | read V of unit 2j
-    //   B0: P V of unit 2j      | max of unit 2j+1  | read K of unit 2j+2
-    //   A1: scores of unit 2j+2 | P of unit 2j+1    | read V of unit 2j+1
-    //   -- barrier: stage j+1 has landed and every read of stage j is done --
-    //   B1: P V of unit 2j+1    | max of unit 2j+2  | read K of unit 2j+3
-    // A wave in a B phase runs at raised issue priority: of the two waves
-    // sharing a SIMD, the one feeding P V (light VALU) then issues its MFMAs
-    // first while the other's exp work fills the VALU slots (3.5-4% faster
-    // than equal priorities; raising A instead is no faster).
+    // stage j: K of units 2j+1, 2j+2 and V of units 2j, 2j+1; it also reads V
+    // of unit 2j-1 from stage j-1.  While it is processed, the loads of stage
+    // j+2 go into buffer (j+2) % 4, last read in tile j-1.  A tile runs four
+    // phases, each followed by the test of the P made one phase before:
+    //   A0: scores of unit 2j+1 | P of unit 2j          | read V of unit 2j-1
+    //   B0: P V of unit 2j-1    | scale of unit 2j+1    | read K of unit 2j+2
+    //       (test P of unit 2j)
+    //   A1: scores of unit 2j+2 | P of unit 2j+1        | read V of unit 2j
+    //   -- barrier: stage j+1 has landed; stage j-1 is fully read --
+    //   B1: P V of unit 2j      | scale of unit 2j+2    | read K of unit 2j+3
+    //       (test P of unit 2j+1)
+    // The last tile then reads V of its second unit and adds its P V.  A wave
+    // in a B phase runs at raised issue priority: of the two waves sharing a
+    // SIMD, the one feeding P V (light VALU) then issues its MFMAs first while
+    // the other's exp work fills the VALU slots.
     f32x4 sa[kRT][2], sb2[kRT][2];
+    bf16x8 pop_e[kRT], pop_o[kRT];        // P of the even and odd unit in flight
+    float us_e[kRT], us_o[kRT];
+#pragma unroll
+    for (int rt = 0; rt < kRT; ++rt) pop_o[rt] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
     int32_t idk = id_k(-1), idv = id_v(-1);
-    load_k(k2, idk);                      // stage -1: K unit 0 (its V part is empty)
-    load_v(v2, idv);
+    load_k(k3, idk);                      // stage -1: K unit 0 (its V part is empty)
+    load_v(v3, idv);
     idk = id_k(0); idv = id_v(0);
     load_k(k0, idk);
     load_v(v0, idv);
@@ -576,66 +611,75 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     load_v(v1, idv);
     idk = id_k(2); idv = id_v(2);
     stage_barrier<D>();                   // stages -1 and 0 have landed
-    read_k(k2 + C::kUnitBytes);           // unit 0 = second unit of stage -1
+    // V of unit -1 (second half of stage -1's V): zeros, so that the first
+    // tile's P V of that unit (with P = 0) adds nothing.
+    for (int ci = tid; ci < 2 * C::kBlockBytes / 16; ci += kPreThreads)
+        *reinterpret_cast<u32x4 *>(v3 + 2 * C::kBlockBytes + ci * 16) = u32x4{0u, 0u, 0u, 0u};
+    read_k(k3 + C::kUnitBytes);           // unit 0 = second unit of stage -1
     qk_mfma(sa);
     read_k(k0);                           // unit 1
     mask_unit(sa, 0);
-    {
-        const bool r = max_test(sa);
-        scale_unit(sa);
-        if (__any(r)) rescale(sa);
-    }
-    stage_barrier<D>();                   // stage -1 fully read: k2/v2 are free
+    // The first unit's row maxima start the running maxima (every row sees key 0).
+#pragma unroll
+    for (int rt = 0; rt < kRT; ++rt) nm[rt] = -xmax16_32(lane_max(sa[rt])) * sl2;
+    scale_unit(sa);
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): the zeros are written
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
 
     // The loads are issued on every path, so outstanding loads are counted
     // exactly; only the compute of tiles past the last one is skipped.
-    auto tile = [&](int j, const uint8_t *ks, uint8_t *vs, const uint8_t *knext, uint8_t *kn, uint8_t *vn) {
+    auto tile = [&](int j, const uint8_t *ks, uint8_t *vs, const uint8_t *vprev, const uint8_t *knext,
+                    uint8_t *kn, uint8_t *vn) {
         const int32_t ik = idk, iv = idv;
         idk = id_k(j + 3);
         idv = id_v(j + 3);
         const bool live = j < ntiles;
-        bf16x8 pop[kRT];
         if (live && (j + 1) * kKeyTile > kv_len) zero_v_tail(vs, j);
         load_k(kn, ik);
         load_v(vn, iv);
         if (live) {
             qk_mfma(sb2);                           // A0
-            exp_unit(sa, pop);
-            read_v(vs, 0);
+            exp_unit(sa, pop_e, us_e);
+            read_v(vprev, 1);
             order_phase<0, kPhaseMfma, NDT, kExpTrans, kExpValu>();
-            pin(pop);
+            pin(pop_e);
             mask_unit(sb2, j * kKeyTile + 32);
             __builtin_amdgcn_s_setprio(1);          // B phases issue first
-            pv_mfma(pop);                           // B0
-            const bool r0 = max_test(sb2);
+            pv_mfma(pop_o);                         // B0
             scale_unit(sb2);
             read_k(ks + C::kUnitBytes);
-            order_phase<0, kPhaseMfma, 2 * KS, 0, kMaxValu>();
+            order_phase<0, kPhaseMfma, 2 * KS, 0, kScaleValu>();
             __builtin_amdgcn_s_setprio(0);
-            if (__any(r0)) rescale(sb2);
+            settle(sa, sb2, pop_e, us_e);
             qk_mfma(sa);                            // A1
-            exp_unit(sb2, pop);
-            read_v(vs, 1);
+            exp_unit(sb2, pop_o, us_o);
+            read_v(vs, 0);
             order_phase<0, kPhaseMfma, NDT, kExpTrans, kExpValu>();
-            pin(pop);
+            pin(pop_o);
             mask_unit(sa, (j + 1) * kKeyTile);
         }
         stage_barrier<D>();
         if (live) {
             __builtin_amdgcn_s_setprio(1);
-            pv_mfma(pop);                           // B1
-            const bool r1 = max_test(sa);
+            pv_mfma(pop_e);                         // B1
             scale_unit(sa);
             read_k(knext);                          // (unused when tile j+1 is past the end)
-            order_phase<0, kPhaseMfma, 2 * KS, 0, kMaxValu>();
+            order_phase<0, kPhaseMfma, 2 * KS, 0, kScaleValu>();
             __builtin_amdgcn_s_setprio(0);
-            if (__any(r1)) rescale(sa);
+            settle(sb2, sa, pop_o, us_o);
+            if (j == ntiles - 1) {                  // the last unit's P V
+                read_v(vs, 1);
+                pv_mfma(pop_o);
+            }
         }
     };
-    for (int j = 0; j < ntiles; j += 3) {
-        tile(j, k0, v0, k1, k2, v2);
-        tile(j + 1, k1, v1, k2, k0, v0);
-        tile(j + 2, k2, v2, k0, k1, v1);
+    for (int j = 0; j < ntiles; j += 4) {
+        tile(j, k0, v0, v3, k1, k2, v2);
+        tile(j + 1, k1, v1, v0, k2, k3, v3);
+        tile(j + 2, k2, v2, v1, k3, k0, v0);
+        tile(j + 3, k3, v3, v2, k0, k1, v1);
     }
 
     // ---- normalise and write
