@@ -444,7 +444,7 @@ ls_status paged_attn_prefill(ls_kv_pool *pool, int32_t layer, int32_t num_sessio
         if (e != hipSuccess) return hip_fail(e, "append launch");
     }
     hipError_t e = launch_prefill(p, layer, num_sessions, num_q_heads, static_cast<const uint16_t *>(q),
-                                  cu_new_lens, reused_lens, total_new_tokens, max_new_len, block_tables,
+                                  cu_new_lens, reused_lens, lens_host, total_new_tokens, max_new_len, block_tables,
                                   max_blocks_per_session, scale, static_cast<uint16_t *>(out), err, stream);
     return e == hipSuccess ? LS_OK : hip_fail(e, "prefill launch");
 }

@@ -93,9 +93,9 @@ hipError_t launch_decode(const PoolGeom &p, int layer, int32_t num_sessions, int
                          unsigned int *err, hipStream_t stream);
 hipError_t launch_prefill(const PoolGeom &p, int layer, int32_t num_sessions, int32_t num_q_heads,
                           const uint16_t *q, const int32_t *cu_new_lens,
-                          const int32_t *reused_lens, int32_t total_tokens, int32_t max_new_len,
-                          const int32_t *block_tables, int32_t max_blocks, float scale,
-                          uint16_t *out, unsigned int *err, hipStream_t stream);
+                          const int32_t *reused_lens, const int32_t *lens_host, int32_t total_tokens,
+                          int32_t max_new_len, const int32_t *block_tables, int32_t max_blocks,
+                          float scale, uint16_t *out, unsigned int *err, hipStream_t stream);
 
 // ---------------------------------------------------------------------------
 // Device helpers

@@ -46,6 +46,9 @@
 // Scheduling: all query tiles of one (session, KV head) pair run on one XCD,
 // so they stream the same keys through its L2; pairs are dealt to XCDs
 // longest first (see the schedule in prefill_kernel).
+#include <algorithm>
+#include <type_traits>
+
 #include "common.h"
 
 namespace ls {
@@ -70,6 +73,7 @@ constexpr float kLog2eP = 1.4426950408889634f;
 constexpr float kSumLimit = 65536.0f;    // per-lane sum of a unit's P above which m' is raised
 constexpr int kXcds = 8;                 // workgroups are dispatched round-robin over XCDs
 constexpr int kMaxPairs = 512;           // (session, KV head) pairs scheduled; more run in index order
+constexpr int kPlanPairs = 256;          // pairs (and sessions) a host-dealt schedule holds
 
 struct PrefillArgs {
     const uint16_t *pool;          // layer base
@@ -88,6 +92,22 @@ struct PrefillArgs {
     float scale_log2;
     unsigned int *err;
 };
+
+// Schedule dealt on the host when the caller passes the lengths there: every
+// XCD's (session, KV head) pairs in the order that XCD runs them, with the
+// items (query tiles) of the XCD's entries before each one.
+struct PrefillHostPlan {
+    uint16_t start[kXcds + 1];           // XCD x runs entries [start[x], start[x + 1])
+    uint16_t pair[kPlanPairs];           // s * num_kv_heads + g
+    uint16_t session_items[kPlanPairs];  // query tiles planned for session s
+    uint32_t before[kPlanPairs];         // items of the XCD's entries before this one
+    uint32_t total[kXcds];               // items of XCD x
+};
+struct PrefillNoPlan {
+    int32_t unused;
+};
+template <bool kHost>
+using PrefillPlanArg = typename std::conditional<kHost, PrefillHostPlan, PrefillNoPlan>::type;
 
 // NaN-propagating maxima (v_maximum3_f32 on gfx950: no operand canonicalisation).
 __device__ __forceinline__ float fmax3(float a, float b, float c) {
@@ -199,8 +219,8 @@ __device__ __forceinline__ void order_phase() {
     }
 }
 
-template <int D>
-__global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
+template <int D, bool kHost>
+__global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a, PrefillPlanArg<kHost> plan) {
     using C = Geo<D>;
     constexpr int KS = D / 32;           // 32-dim k-steps of QK
     constexpr int NDT = D / 16;          // 16-dim output tiles
@@ -236,19 +256,39 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
     // same half of the XCDs every round).  An XCD runs its pairs in the order
     // dealt, each pair's latest (longest) query tile first.  Workgroup i is
     // dispatched to XCD i % 8 and is the (i / 8)-th item there; every
-    // workgroup derives the same schedule from the lengths.
+    // workgroup derives the same schedule from the lengths.  A schedule dealt
+    // on the host (same rule, each XCD's pairs then run longest item first)
+    // replaces all of this with one lookup.
     const int P = S * Hkv;
-    // A turn longer than the grid's query tiles (max_new_len understated), a
-    // negative turn or a negative context cannot be attended as given: flagged
-    // once, by the first workgroup (its rows past the tiles are not written).
+    // A turn longer than its planned query tiles (max_new_len understated, or
+    // device lengths longer than the host's), a negative turn or a negative
+    // context cannot be attended as given: flagged once, by the first
+    // workgroup (rows past the planned tiles are not written).
     if (blockIdx.x == 0)
         for (int sp = tid; sp < S; sp += kPreThreads) {
             const int nt = a.cu[sp + 1] - a.cu[sp];
-            if (nt < 0 || nt > QT * qtok || a.ctx[sp] < 0 || a.cu[sp] < 0 || a.cu[sp + 1] > a.total)
+            int planned = QT;
+            if constexpr (kHost) planned = plan.session_items[sp];
+            if (nt < 0 || nt > planned * qtok || a.ctx[sp] < 0 || a.cu[sp] < 0 || a.cu[sp + 1] > a.total)
                 flag_error(a.err, LS_DEVERR_LENGTH);
         }
     int s, g, qt;
-    if (P <= kMaxPairs) {
+    if constexpr (kHost) {
+        // Entry of this workgroup: the last one of its XCD whose earlier items
+        // are at most its slot (entries have items, so 'before' increases; an
+        // XCD has at most kPlanPairs / 8 entries, one per lane).
+        const int xcd = (int)(blockIdx.x % kXcds);
+        const uint32_t slot = blockIdx.x / kXcds;
+        if (slot >= plan.total[xcd]) return;
+        const int b = plan.start[xcd], m = plan.start[xcd + 1] - b;
+        const int ln = tid % kWave;
+        const bool passed = ln < m && plan.before[b + min(ln, m - 1)] <= slot;
+        const int e = b + __popcll(__ballot(passed)) - 1;
+        const uint32_t items = (e + 1 < b + m ? plan.before[e + 1] : plan.total[xcd]) - plan.before[e];
+        qt = (int)(items - 1 - (slot - plan.before[e]));
+        s = plan.pair[e] / Hkv;
+        g = plan.pair[e] % Hkv;
+    } else if (P <= kMaxPairs) {
         for (int p = tid; p < P; p += kPreThreads) {
             const int sp = p / Hkv;
             const int nt = max(a.cu[sp + 1] - a.cu[sp], 0);
@@ -699,11 +739,76 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a) {
 
 }  // namespace
 
+namespace {
+
+// Host dealing of the schedule (the device rule, on exact integer work, with
+// each XCD's pairs then ordered by decreasing item length c + n, so that the
+// items an XCD ends with are short).  Returns false when the batch exceeds the
+// plan's capacity (the device deals the schedule then).
+bool plan_prefill_host(int32_t S, int32_t hkv, int32_t qtok, const int32_t *lens, PrefillHostPlan &plan,
+                       int32_t &max_items) {
+    const int P = S * hkv;
+    if (S > kPlanPairs || P > kPlanPairs) return false;
+    struct Pair {
+        int64_t work, len;
+        int32_t p, items, deal;
+    };
+    Pair pr[kPlanPairs];
+    int np = 0;
+    for (int s = 0; s < S; ++s) {
+        const int32_t n = lens[2 * s], c = lens[2 * s + 1];
+        const int32_t items = (n + qtok - 1) / qtok;
+        plan.session_items[s] = (uint16_t)items;
+        if (items == 0) continue;
+        for (int g = 0; g < hkv; ++g)
+            pr[np++] = Pair{(int64_t)items * (2 * (int64_t)c + n), (int64_t)c + n, s * hkv + g, items, 0};
+    }
+    for (int s = S; s < kPlanPairs; ++s) plan.session_items[s] = 0;
+    std::stable_sort(pr, pr + np, [](const Pair &x, const Pair &y) { return x.work > y.work; });
+    // Rounds of 8: the round's k-th heaviest pair to the XCD with the k-th least work so far.
+    int64_t load[kXcds] = {};
+    int xcd_of[kPlanPairs];
+    for (int r0 = 0; r0 < np; r0 += kXcds) {
+        int rank[kXcds];
+        for (int x = 0; x < kXcds; ++x) rank[x] = x;
+        std::stable_sort(rank, rank + kXcds, [&](int x, int y) { return load[x] < load[y]; });
+        for (int k = 0; k < kXcds && r0 + k < np; ++k) {
+            xcd_of[r0 + k] = rank[k];
+            pr[r0 + k].deal = r0 + k;
+            load[rank[k]] += pr[r0 + k].work;
+        }
+    }
+    // Per XCD, entries by decreasing item length (ties in dealing order).
+    int idx[kPlanPairs];
+    for (int i = 0; i < np; ++i) idx[i] = i;
+    std::stable_sort(idx, idx + np, [&](int i, int j) {
+        if (xcd_of[i] != xcd_of[j]) return xcd_of[i] < xcd_of[j];
+        return pr[i].len > pr[j].len;
+    });
+    max_items = 0;
+    int e = 0;
+    for (int x = 0; x < kXcds; ++x) {
+        plan.start[x] = (uint16_t)e;
+        uint32_t acc = 0;
+        for (; e < np && xcd_of[idx[e]] == x; ++e) {
+            plan.pair[e] = (uint16_t)pr[idx[e]].p;
+            plan.before[e] = acc;
+            acc += (uint32_t)pr[idx[e]].items;
+        }
+        plan.total[x] = acc;
+        max_items = std::max(max_items, (int32_t)acc);
+    }
+    plan.start[kXcds] = (uint16_t)e;
+    return true;
+}
+
+}  // namespace
+
 hipError_t launch_prefill(const PoolGeom &p, int layer, int32_t num_sessions, int32_t num_q_heads,
                           const uint16_t *q, const int32_t *cu_new_lens,
-                          const int32_t *reused_lens, int32_t total_tokens, int32_t max_new_len,
-                          const int32_t *block_tables, int32_t max_blocks, float scale,
-                          uint16_t *out, unsigned int *err, hipStream_t stream) {
+                          const int32_t *reused_lens, const int32_t *lens_host, int32_t total_tokens,
+                          int32_t max_new_len, const int32_t *block_tables, int32_t max_blocks,
+                          float scale, uint16_t *out, unsigned int *err, hipStream_t stream) {
     if (num_sessions <= 0 || max_new_len <= 0) return hipSuccess;
     PrefillArgs a;
     a.pool = p.layer_base(layer);
@@ -722,15 +827,28 @@ hipError_t launch_prefill(const PoolGeom &p, int layer, int32_t num_sessions, in
     a.err = err;
     const int qtok = kPreRows / a.group;
     a.qtiles = (max_new_len + qtok - 1) / qtok;
+    PrefillHostPlan plan;
+    int32_t max_items = 0;
+    if (lens_host && plan_prefill_host(num_sessions, p.num_kv_heads, qtok, lens_host, plan, max_items)) {
+        if (max_items == 0) return hipSuccess;
+        const dim3 grid((unsigned)(kXcds * max_items));
+        if (p.head_dim == 128)
+            hipLaunchKernelGGL((prefill_kernel<128, true>), grid, dim3(kPreThreads), 0, stream, a, plan);
+        else
+            hipLaunchKernelGGL((prefill_kernel<64, true>), grid, dim3(kPreThreads), 0, stream, a, plan);
+        return hipGetLastError();
+    }
     // An XCD holds at most ceil(pairs / 8) pairs of at most qtiles items each;
     // workgroups past an XCD's item count exit at once.
     const int64_t pairs = (int64_t)num_sessions * p.num_kv_heads;
     const int64_t grid = (pairs + kXcds - 1) / kXcds * kXcds * a.qtiles;
     if (grid > 0x7FFFFFFFLL) return hipErrorInvalidConfiguration;
+    const PrefillNoPlan none{0};
+    const dim3 g((unsigned)grid);
     if (p.head_dim == 128)
-        hipLaunchKernelGGL(prefill_kernel<128>, dim3((unsigned)grid), dim3(kPreThreads), 0, stream, a);
+        hipLaunchKernelGGL((prefill_kernel<128, false>), g, dim3(kPreThreads), 0, stream, a, none);
     else
-        hipLaunchKernelGGL(prefill_kernel<64>, dim3((unsigned)grid), dim3(kPreThreads), 0, stream, a);
+        hipLaunchKernelGGL((prefill_kernel<64, false>), g, dim3(kPreThreads), 0, stream, a, none);
     return hipGetLastError();
 }
 

@@ -38,24 +38,27 @@ def _case(rng, n, c, hq, hkv, d, spare=3):
     return pool, tables, q, kn, vn
 
 
-def _run(kv, dp, q, kn, vn, n, c, tables, scale):
+def _run(kv, dp, q, kn, vn, n, c, tables, scale, host=False):
     cu = np.concatenate([[0], np.cumsum(n)]).astype(np.int32)
     out = torch.empty((q.shape[0], q.shape[1], q.shape[2]), dtype=torch.bfloat16, device="cuda")
+    lens_host = np.stack([np.asarray(n), np.asarray(c)], 1) if host else None
     kv.paged_attn_prefill(dp.pool, 0, bf16_dev(q), i32_dev(cu), i32_dev(c), int(np.max(n)),
-                          i32_dev(tables), scale, out, bf16_dev(kn), bf16_dev(vn))
+                          i32_dev(tables), scale, out, bf16_dev(kn), bf16_dev(vn), lens_host=lens_host)
     return out, cu
 
 
+@pytest.mark.parametrize("host", [False, True], ids=["device-lengths", "host-lengths"])
 @pytest.mark.parametrize("d,hq,hkv", [(128, 32, 4), (64, 8, 2), (128, 8, 8), (128, 16, 8),
                                       (64, 4, 1)])
-def test_prefill_ragged(kv, oracle_lib, d, hq, hkv):
-    """Turn lengths and contexts around tile and block boundaries, c = 0 included."""
+def test_prefill_ragged(kv, oracle_lib, d, hq, hkv, host):
+    """Turn lengths and contexts around tile and block boundaries, c = 0 included;
+    the schedule dealt in the kernel, or on the host from host lengths."""
     rng = np.random.default_rng(d + hq * 3 + hkv)
     n = [1, 17, 16, 130, 37, 255, 64]
     c = [0, 5, 300, 0, 1000, 77, 16]
     pool, tables, q, kn, vn = _case(rng, n, c, hq, hkv, d)
     dp = DevicePool(kv, pool, d)
-    out, cu = _run(kv, dp, q, kn, vn, np.array(n), np.array(c), tables, 1 / math.sqrt(d))
+    out, cu = _run(kv, dp, q, kn, vn, np.array(n), np.array(c), tables, 1 / math.sqrt(d), host=host)
     ref, ref_pool = oracle_lib.prefill(pool, 16, d, 0, q, kn, vn, cu, c, tables, 1 / math.sqrt(d),
                                        pool_out=True)
     assert_attn_close(out, ref, "prefill D=%d G=%d" % (d, hq // hkv))
@@ -126,7 +129,8 @@ def test_prefill_turn_longer_than_max_new_len_is_flagged(kv, oracle_lib):
 
 
 def test_prefill_host_lengths_same_result(kv):
-    """Host (n, c) pairs change validation and grid sizing only: same bits."""
+    """Host (n, c) pairs change validation and the schedule (dealt on the host),
+    not the arithmetic of any row: same bits, empty turns included."""
     rng = np.random.default_rng(43)
     d, hq, hkv = 128, 32, 4
     n, c = np.array([300, 1, 77, 0, 150]), np.array([900, 16, 0, 40, 333])
@@ -142,6 +146,48 @@ def test_prefill_host_lengths_same_result(kv):
         outs.append(out)
     assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
     assert kv.ls_device_errors() == 0
+
+
+@pytest.mark.parametrize("S", [64, 65])
+def test_prefill_host_plan_capacity(kv, oracle_lib, S):
+    """Host lengths with 4 KV heads: 64 sessions (256 session/KV-head pairs) fill
+    the host-dealt schedule; 65 sessions (260 pairs) exceed it and the kernel
+    deals the schedule itself.  Empty turns mixed in."""
+    rng = np.random.default_rng(900 + S)
+    d, hq, hkv = 64, 8, 4
+    n = rng.integers(0, 40, size=S)
+    n[1] = 0
+    n[S - 1] = 39
+    c = rng.integers(0, 200, size=S)
+    pool, tables, q, kn, vn = _case(rng, n, c, hq, hkv, d)
+    dp = DevicePool(kv, pool, d)
+    out, cu = _run(kv, dp, q, kn, vn, n, c, tables, 0.125, host=True)
+    ref = oracle_lib.prefill(pool, 16, d, 0, q, kn, vn, cu, c, tables, 0.125)
+    assert_attn_close(out, ref, "prefill, %d sessions x %d KV heads, host lengths" % (S, hkv))
+    assert kv.ls_device_errors() == 0
+
+
+def test_prefill_device_turn_longer_than_host_is_flagged(kv, oracle_lib):
+    """Host lengths that pass every host check but understate a turn on the
+    device: the host-dealt schedule has 8 query tiles (256 tokens) for a turn of
+    300.  The device flags LS_DEVERR_LENGTH; rows inside the planned tiles are
+    still right."""
+    rng = np.random.default_rng(44)
+    d, hq, hkv = 128, 32, 4                   # 32 tokens per query tile
+    n, c = np.array([300, 100]), np.array([500, 50])
+    pool, tables, q, kn, vn = _case(rng, n, c, hq, hkv, d)
+    assert tables.shape[1] * 16 >= 150 + 50       # the claimed lengths fit the table
+    dp = DevicePool(kv, pool, d)
+    kv.ls_device_errors()
+    cu = np.concatenate([[0], np.cumsum(n)]).astype(np.int32)
+    out = torch.zeros((q.shape[0], hq, d), dtype=torch.bfloat16, device="cuda")
+    claimed = np.stack([[250, 150], c], 1)    # adds up to the same 400 tokens
+    kv.paged_attn_prefill(dp.pool, 0, bf16_dev(q), i32_dev(cu), i32_dev(c), 300, i32_dev(tables),
+                          0.0884, out, bf16_dev(kn), bf16_dev(vn), lens_host=claimed)
+    assert kv.ls_device_errors() & kv.LS_DEVERR_LENGTH
+    covered = np.concatenate([np.arange(0, 256), np.arange(300, 400)])
+    ref = oracle_lib.prefill(pool, 16, d, 0, q, kn, vn, cu, c, tables, 0.0884, rows=covered)
+    assert_attn_close(out[torch.from_numpy(covered).cuda()], ref, "prefill rows inside the planned tiles")
 
 
 @pytest.mark.parametrize("shape", ["rising", "spike", "falling"])
