@@ -362,16 +362,20 @@ def talker_leg(torch, kv, W, args):
     log("talker: median %.1f us/step eager (p10 %.1f, p90 %.1f), %.1f us/step as one graph, %.0f GB/s; "
         "host lengths %.1f us/step eager, %.1f as one graph, %.0f GB/s" % (
             us, st["p10"], st["p90"], gst["median"], gbs, hst["median"], hgst["median"], hgbs))
+    # Headline figures are the calls as a serving loop makes them (lengths on
+    # the device and the host, like the decode headline); the same steps with
+    # device lengths only are reported beside them.
     return {"workload": "talker-shaped decode: 256 sessions, L0~U[512,4096], 16/2 heads, D=128, "
-                        "32 consecutive steps appending one token per session; 3 pool copies rotate per step",
-            "us_per_step": round(us, 2), "step_us": st,
-            "wall_us_per_step": round(wall * 1e6 / (args.reps * case.steps), 2),
-            "graph_us_per_step": round(gst["median"], 2), "graph_step_us": gst,
-            "host_lengths": {"us_per_step": round(hst["median"], 2), "step_us": hst,
-                             "graph_us_per_step": round(hgst["median"], 2), "graph_step_us": hgst,
-                             "value": round(hgbs, 1), "frac_hbm_peak": round(hgbs / HBM_PEAK_GBS, 4)},
+                        "32 consecutive steps appending one token per session; 3 pool copies rotate per step; "
+                        "lengths on the device and the host",
+            "us_per_step": round(hst["median"], 2), "step_us": hst,
+            "graph_us_per_step": round(hgst["median"], 2), "graph_step_us": hgst,
             "mb_per_step": round(total_bytes / case.steps / 1e6, 1),
-            "value": round(gbs, 1), "unit": "GB/s", "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)}
+            "value": round(hgbs, 1), "unit": "GB/s", "frac_hbm_peak": round(hgbs / HBM_PEAK_GBS, 4),
+            "device_lengths": {"us_per_step": round(us, 2), "step_us": st,
+                               "wall_us_per_step": round(wall * 1e6 / (args.reps * case.steps), 2),
+                               "graph_us_per_step": round(gst["median"], 2), "graph_step_us": gst,
+                               "value": round(gbs, 1), "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)}}
 
 
 def _hip_runtime():
@@ -544,6 +548,22 @@ def restore_leg(torch, kv, W, args, dec):
             log("partitioned overlap: restore on %d CUs %.2f ms (%.0f GB/s), decode on %d CUs %.1f us alone, %.1f us "
                 "concurrent" % (args.restore_cus, conc["side_ms"], part["restore_gbs"], n_cus - args.restore_cus,
                                 solo["us"], conc["us"]))
+            # Both knobs: the rate cap on the CU-masked side stream.  The copy then
+            # shares no CU with decode and its HBM traffic is bounded; slowdowns
+            # are against decode alone on every CU.
+            part["paced"] = []
+            for gbps in [r for r in args.rates if r > 0]:
+                nb_b = int(min(n, max(256, gbps * 1e9 * 0.04 // per_block)))
+                ids_b = b[:nb_b]
+                pt = overlap_decode(lambda st: kv.kv_blocks_restore(pool, ids_b, staging, max_gbps=gbps, stream=st),
+                                    dec_stream=dec_st, side_stream=res_st)
+                gbs_b = 2.0 * nb_b * per_block / (pt["side_ms"] * 1e-3) / 1e9
+                part["paced"].append({"max_gbps_payload": gbps, "restore_gbs_2n": round(gbs_b, 1),
+                                      "restore_ms": pt["side_ms"], "decode_us_concurrent": pt["us"],
+                                      "decode_slowdown_pct": round(100 * (pt["us"] * 1e-3 / dec_alone_ms - 1), 1)})
+                log("paced restore on %d CUs: cap %.0f GB/s payload, %.0f GB/s (2N), decode on %d CUs %.1f us "
+                    "(+%.1f%%)" % (args.restore_cus, gbps, gbs_b, n_cus - args.restore_cus, pt["us"],
+                                   part["paced"][-1]["decode_slowdown_pct"]))
             destroy_streams(masked)
 
     # host leg: pinned host staging -> device ring -> scatter, through the same call
