@@ -757,7 +757,8 @@ bool plan_prefill_host(int32_t S, int32_t hkv, int32_t qtok, const int32_t *lens
     int np = 0;
     for (int s = 0; s < S; ++s) {
         const int32_t n = lens[2 * s], c = lens[2 * s + 1];
-        const int32_t items = (n + qtok - 1) / qtok;
+        const int32_t items = (int32_t)(((int64_t)n + qtok - 1) / qtok);
+        if (items > 0xFFFF) return false;                  // beyond the plan's 16-bit counts
         plan.session_items[s] = (uint16_t)items;
         if (items == 0) continue;
         for (int g = 0; g < hkv; ++g)
@@ -799,7 +800,7 @@ bool plan_prefill_host(int32_t S, int32_t hkv, int32_t qtok, const int32_t *lens
         max_items = std::max(max_items, (int32_t)acc);
     }
     plan.start[kXcds] = (uint16_t)e;
-    return true;
+    return (int64_t)max_items * kXcds <= 0x7FFFFFFF;
 }
 
 }  // namespace

@@ -348,6 +348,16 @@ def test_schedule_mixed_batch_splits_long_sessions(lib):
     assert r == LS_OK and host and merge and split % 1024 == 0 and 2048 <= split < 8000
 
 
+def test_schedule_eight_heads_uses_wide_items(lib):
+    """Eight KV heads (beyond the 16-bit item form): still planned on the host,
+    split at 2048 tokens with the merge; the same lengths the GPU test runs."""
+    import numpy as np
+    rng = np.random.default_rng(225)
+    lens = np.concatenate([rng.integers(1, 3000, 20), [6000, 6001, 1, 2048]])
+    maxb = int(((lens + 1 + 15) // 16).max())
+    assert _sched(lib, 8, 16, lens, maxb, appended=1) == (LS_OK, 2048, True, True)
+
+
 def test_schedule_rejects_bad_host_lengths(lib):
     assert _sched(lib, 2, 16, [5, 0, 7], 10)[0] == LS_EINVAL          # an empty context
     assert _sched(lib, 2, 16, [5, 0, 7], 10, appended=1)[0] == LS_OK

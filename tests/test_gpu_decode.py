@@ -352,3 +352,27 @@ def test_thinker_decode_full_host_planned(kv, oracle_lib):
     ref = oracle_lib.decode(case.pool.data, 16, 128, 0, case.q[0], case.block_tables, case.context_lens, case.scale)
     assert_attn_close(out, ref, "thinker decode, host-planned (split %d)" % sc["split_tokens"])
     assert kv.ls_device_errors() == 0
+
+
+@pytest.mark.parametrize("d,hq,hkv", [(128, 16, 8), (64, 8, 8)])
+def test_host_planned_wide_items(kv, oracle_lib, d, hq, hkv):
+    """Eight KV heads: the host plan's items take the 32-bit form (the 16-bit form
+    holds at most 4 heads).  A few sessions are long enough to be split, so the
+    merge runs; the step's token is appended."""
+    rng = np.random.default_rng(225)
+    lens = np.concatenate([rng.integers(1, 3000, 20), [6000, 6001, 1, 2048]])
+    pool, tables, q, kn, vn = _synthetic(rng, lens, hq, hkv, d, True)
+    dp = DevicePool(kv, pool, d)
+    sc = _host_planned(kv, dp, len(lens), hq, tables.shape[1], lens, True)
+    log("schedule: %s" % sc)
+    assert sc["host_planned"] and sc["merge"], sc
+    ws = torch.zeros(kv.decode_workspace_bytes(dp.pool, len(lens), hq, tables.shape[1]), dtype=torch.uint8,
+                     device="cuda")
+    out = torch.empty((len(lens), hq, d), dtype=torch.bfloat16, device="cuda")
+    kv.paged_attn_decode(dp.pool, 0, bf16_dev(q), i32_dev(tables), i32_dev(lens), 1 / math.sqrt(d), out, ws,
+                         bf16_dev(kn), bf16_dev(vn), context_lens_host=lens)
+    ref, ref_pool = oracle_lib.decode(pool, 16, d, 0, q, tables, lens, 1 / math.sqrt(d), k_new=kn, v_new=vn,
+                                      pool_out=True)
+    assert_attn_close(out, ref, "host-planned, 8 KV heads, D=%d" % d)
+    assert np.array_equal(dp.host(), ref_pool)
+    assert kv.ls_device_errors() == 0
