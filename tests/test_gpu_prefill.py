@@ -250,3 +250,9 @@ def test_next_turn_prefill_full_sampled(kv, oracle_lib):
     assert_attn_close(out[torch.from_numpy(rows).cuda()], ref,
                       "next-turn prefill (%d sampled rows)" % len(rows))
     assert kv.ls_device_errors() == 0
+    # The timed form of the call (host lengths: schedule dealt on the host)
+    # computes every row with the same arithmetic: all rows, same bits.
+    out_h, _ = _run(kv, dp, case.q, case.k_new, case.v_new, n, case.reused_lens, case.block_tables,
+                    case.scale, host=True)
+    assert torch.equal(out_h.view(torch.int16), out.view(torch.int16))
+    assert kv.ls_device_errors() == 0
