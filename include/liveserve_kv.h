@@ -246,8 +246,8 @@ ls_status paged_attn_prefill(ls_kv_pool *pool, int32_t layer, int32_t num_sessio
  *                   otherwise).  Two copies that may run at the same time (different
  *                   streams) need different rings.  Ignored (may be NULL) with device
  *                   staging.
- *   max_gbps        0: full rate (a persistent grid of four 256-thread workgroups per
- *                   CU the stream may use).  r > 0: a rate-bounded copy of at most r GB/s
+ *   max_gbps        0: full rate (a persistent grid of four (restore) or six (stash)
+ *                   256-thread workgroups per CU the stream may use).  r > 0: a rate-bounded copy of at most r GB/s
  *                   (10^9 bytes per second) of payload, for background work beside live
  *                   decode (§5.2: preloads must not interfere with live requests; the
  *                   KV manager's admission divides bytes by such a rate).  It runs one
