@@ -211,24 +211,39 @@ ls_status paged_attn_decode_static(ls_kv_pool *pool, int32_t layer, int32_t num_
  *   lens_host      optional host int32 [num_sessions][2] = (n_s, c_s), the same values
  *                  as the device arrays (NULL: nothing is checked on the host).  When
  *                  given, the host checks every turn against max_new_len, the table
- *                  and total_new_tokens (LS_EINVAL) before anything is enqueued.
+ *                  and total_new_tokens (LS_EINVAL) before anything is enqueued, and
+ *                  deals the query tiles to the XCDs itself (up to 256 sessions and
+ *                  256 session/KV-head pairs; beyond that the kernel deals them).  A
+ *                  device turn longer than its planned tiles is flagged
+ *                  (LS_DEVERR_LENGTH); its rows past them are not written.
  *   total_new_tokens, max_new_len   host ints: cu[S] and max_s n_s (grid sizing).
  *                  A turn longer than max_new_len (device lengths only) is flagged
  *                  (LS_DEVERR_LENGTH) and its rows past max_new_len are not written.
  *   block_tables   device int32 [num_sessions][max_blocks_per_session], covering
  *                  c_s + n_s tokens
  *   out            device bf16 [total_new_tokens][num_q_heads][head_dim]
+ *   workspace      optional device memory (16-byte aligned) of workspace_bytes >=
+ *                  LS_PREFILL_WORKSPACE_BYTES, or NULL (LS_ENOMEM if too small,
+ *                  LS_EINVAL if misaligned).  With host lengths the workgroups then stay
+ *                  resident, one per CU, and take query tiles in order through a
+ *                  counter per XCD kept here; an XCD whose tiles run out takes the next
+ *                  tiles of the XCD with the most left, so XCDs of different speeds
+ *                  finish together.  The call clears it first (its contents on entry do
+ *                  not matter).  Calls that may run at the same time need different
+ *                  workspaces.  Unused without host lengths.
  *
  * Supported: head_dim 128 or 64, num_q_heads / num_kv_heads in {1, 2, 4, 8}.
  * Errors as for paged_attn_decode.
  */
+#define LS_PREFILL_WORKSPACE_BYTES ((size_t)256)
 ls_status paged_attn_prefill(ls_kv_pool *pool, int32_t layer, int32_t num_sessions,
                              int32_t num_q_heads, const void *q, const void *k_new,
                              const void *v_new, const int32_t *cu_new_lens,
                              const int32_t *reused_lens, const int32_t *lens_host,
                              int32_t total_new_tokens, int32_t max_new_len,
                              const int32_t *block_tables, int32_t max_blocks_per_session,
-                             float scale, void *out, hipStream_t stream);
+                             float scale, void *out, void *workspace, size_t workspace_bytes,
+                             hipStream_t stream);
 
 /*
  * Arguments shared by the three block-copy calls below.
@@ -247,7 +262,8 @@ ls_status paged_attn_prefill(ls_kv_pool *pool, int32_t layer, int32_t num_sessio
  *                   streams) need different rings.  Ignored (may be NULL) with device
  *                   staging.
  *   max_gbps        0: full rate (a persistent grid of four (restore) or six (stash)
- *                   256-thread workgroups per CU the stream may use).  r > 0: a rate-bounded copy of at most r GB/s
+ *                   256-thread workgroups per CU the stream may use).  r > 0: a
+ *                   rate-bounded copy of at most r GB/s
  *                   (10^9 bytes per second) of payload, for background work beside live
  *                   decode (§5.2: preloads must not interfere with live requests; the
  *                   KV manager's admission divides bytes by such a rate).  It runs one

@@ -411,7 +411,8 @@ ls_status paged_attn_prefill(ls_kv_pool *pool, int32_t layer, int32_t num_sessio
                              const int32_t *reused_lens, const int32_t *lens_host,
                              int32_t total_new_tokens, int32_t max_new_len,
                              const int32_t *block_tables, int32_t max_blocks_per_session,
-                             float scale, void *out, hipStream_t stream) {
+                             float scale, void *out, void *workspace, size_t workspace_bytes,
+                             hipStream_t stream) {
     if (ls_status st = check_pool(pool)) return st;
     const PoolGeom &p = pool->geom;
     if (layer < 0 || layer >= p.num_layers)
@@ -429,6 +430,11 @@ ls_status paged_attn_prefill(ls_kv_pool *pool, int32_t layer, int32_t num_sessio
         return fail(LS_EINVAL, "max_new_len (%d) exceeds total_new_tokens (%d)", max_new_len,
                     total_new_tokens);
     if (!(scale > 0.f) || scale != scale) return fail(LS_EINVAL, "scale must be a positive number");
+    if (workspace && workspace_bytes < LS_PREFILL_WORKSPACE_BYTES)
+        return fail(LS_ENOMEM, "prefill workspace of %zu bytes, %zu needed", workspace_bytes,
+                    LS_PREFILL_WORKSPACE_BYTES);
+    if (reinterpret_cast<uintptr_t>(workspace) % 16)
+        return fail(LS_EINVAL, "prefill workspace must be 16-byte aligned");
     if (lens_host)
         if (ls_status st = check_prefill_lens_host(num_sessions, lens_host, total_new_tokens, max_new_len,
                                                    max_blocks_per_session))
@@ -445,7 +451,8 @@ ls_status paged_attn_prefill(ls_kv_pool *pool, int32_t layer, int32_t num_sessio
     }
     hipError_t e = launch_prefill(p, layer, num_sessions, num_q_heads, static_cast<const uint16_t *>(q),
                                   cu_new_lens, reused_lens, lens_host, total_new_tokens, max_new_len, block_tables,
-                                  max_blocks_per_session, scale, static_cast<uint16_t *>(out), err, stream);
+                                  max_blocks_per_session, scale, static_cast<uint16_t *>(out),
+                                  static_cast<uint32_t *>(workspace), err, stream);
     return e == hipSuccess ? LS_OK : hip_fail(e, "prefill launch");
 }
 

@@ -95,7 +95,7 @@ hipError_t launch_prefill(const PoolGeom &p, int layer, int32_t num_sessions, in
                           const uint16_t *q, const int32_t *cu_new_lens,
                           const int32_t *reused_lens, const int32_t *lens_host, int32_t total_tokens,
                           int32_t max_new_len, const int32_t *block_tables, int32_t max_blocks,
-                          float scale, uint16_t *out, unsigned int *err, hipStream_t stream);
+                          float scale, uint16_t *out, uint32_t *queue, unsigned int *err, hipStream_t stream);
 
 // ---------------------------------------------------------------------------
 // Device helpers

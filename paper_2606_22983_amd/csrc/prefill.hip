@@ -91,6 +91,7 @@ struct PrefillArgs {
     int32_t max_blocks;
     float scale_log2;
     unsigned int *err;
+    uint32_t *queue;               // per-XCD item counters (resident workgroups), or null
 };
 
 // Schedule dealt on the host when the caller passes the lengths there: every
@@ -238,6 +239,7 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a, Pre
     __shared__ int sm_items[kMaxPairs];
     __shared__ int sm_order[kMaxPairs];
     __shared__ float sm_rank_work[kMaxPairs];
+    __shared__ int sm_grab[2];
 
     const int tid = threadIdx.x;
     const int S = a.num_sessions;
@@ -245,6 +247,396 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a, Pre
     const int qtok = kPreRows / G;       // new tokens per query tile
     const int QT = a.qtiles;
     const int Hkv = a.num_kv_heads;
+
+    // ---- one item: rows of query tile qt of session s, KV head g.
+    auto run_item = [&](const int s, const int g, const int qt) {
+        const int n = a.cu[s + 1] - a.cu[s];
+        const int j0 = qt * qtok;
+        if (j0 >= n || a.cu[s] < 0 || a.cu[s + 1] > a.total) return;   // (lengths outside q: flagged above)
+        const int c = a.ctx[s];
+        const int j_last = min(j0 + qtok, n) - 1;
+        const int kv_len = c + n;
+        int nblk_valid = (kv_len + kBlock - 1) / kBlock;
+        if (nblk_valid > a.max_blocks) {
+            nblk_valid = a.max_blocks;
+            if (tid == 0) flag_error(a.err, LS_DEVERR_LENGTH);
+        }
+        const int kv_end = c + j_last + 1;                    // keys this tile can see
+        const int ntiles = (kv_end + kKeyTile - 1) / kKeyTile;
+        const int nb = min(nblk_valid, ntiles * 4);           // blocks any row here can see
+
+        const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+        const int lane = tid % kWave;
+        const int c16 = lane & 15;
+        const int g4 = lane >> 4;
+        const int hq_total = Hkv * G;
+
+        // Rows of this lane (one per 16-row tile): r = wave*32 + rt*16 + c16.
+        int row_lim[kRT];
+        int64_t row_out[kRT];
+        bool row_ok[kRT];
+        bf16x8 qop[kRT][KS];
+    #pragma unroll
+        for (int rt = 0; rt < kRT; ++rt) {
+            const int r = wave * kWaveRows + rt * 16 + c16;
+            const int jl = j0 + r / G;
+            const int h = r % G;
+            row_ok[rt] = jl < n;
+            const int jc = min(jl, n - 1);
+            row_lim[rt] = c + jc;
+            const int64_t tok = (int64_t)a.cu[s] + jc;
+            row_out[rt] = (tok * hq_total + g * G + h) * D;
+            const uint16_t *qrow = a.q + row_out[rt];
+    #pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                qop[rt][ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(qrow + ks * 32 + g4 * 8));
+        }
+        // Wait for q here, before the first stage loads are issued, so that no
+        // wait for q remains inside the key loop (vmcnt(0), other counters untouched).
+        __builtin_amdgcn_s_waitcnt(0x0F70);
+        // smallest causal limit among this wave's rows: units past it need masking
+        const int wave_lim_min = c + min(j0 + (wave * kWaveRows) / G, n - 1);
+
+        // ---- this wave's share of every stage: kLoadsK kilobytes of one K block
+        // and of one V block (block 'blk' of the stage), at fixed lane offsets.
+        const int blk = (wave * C::kLoadsK) / C::kKbPerBlock;
+        int k_voff[C::kLoadsK], v_voff[C::kLoadsK], kb_off[C::kLoadsK];
+    #pragma unroll
+        for (int e = 0; e < C::kLoadsK; ++e) {
+            const int q = (wave * C::kLoadsK + e) % C::kKbPerBlock;       // kilobyte within the block
+            kb_off[e] = blk * C::kBlockBytes + q * 1024;
+            // K: lane -> (token, slot); fetch the chunk that belongs in that slot
+            const int t = q * (1024 / (D * 2)) + lane / C::kRowChunks;
+            const int sl = lane % C::kRowChunks;
+            k_voff[e] = ((sl ^ kswz<D>(blk & 1, t)) * kBlock + t) * 16;   // chunk-major K tile
+            // V: lane -> chunk position p = half*D + dim
+            const int p = q * 64 + lane;
+            v_voff[e] = (p % D) * 32 + (p / D) * 16;
+        }
+        const int32_t *table = a.block_tables + (int64_t)s * a.max_blocks;
+        const uint32_t slab_elems = (uint32_t)(2 * Hkv * kBlock * D);
+        const uint32_t nblocks32 = (uint32_t)min(a.num_blocks, (int64_t)0x7fffffff);
+        const uint16_t *kbase = a.pool + (int64_t)g * (kBlock * D);
+        const uint16_t *vbase = kbase + (int64_t)Hkv * (kBlock * D);
+        auto load_k = [&](uint8_t *stage, int32_t b) {
+    #pragma unroll
+            for (int e = 0; e < C::kLoadsK; ++e) load_kb<D>(kbase, slab_elems, nblocks32, b, stage + kb_off[e], k_voff[e]);
+        };
+        auto load_v = [&](uint8_t *stage, int32_t b) {
+    #pragma unroll
+            for (int e = 0; e < C::kLoadsK; ++e) load_kb<D>(vbase, slab_elems, nblocks32, b, stage + kb_off[e], v_voff[e]);
+        };
+        auto id_k = [&](int t) { return table_entry(table, 4 * t + 2 + blk, nb); };
+        auto id_v = [&](int t) { return table_entry(table, 4 * t + blk, nb); };
+
+        float nm[kRT], lsum[kRT];             // -m' (running row max * scale * log2 e),
+        f32x4 o[kRT][NDT];                    // partial row sums, unnormalised output
+    #pragma unroll
+        for (int rt = 0; rt < kRT; ++rt) {
+            nm[rt] = 0.f;
+            lsum[rt] = 0.f;
+        }
+    #pragma unroll
+        for (int rt = 0; rt < kRT; ++rt)
+    #pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) o[rt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        const float sl2 = a.scale_log2;
+        const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
+
+        // ---- S^T = K Q^T of one 32-key unit for 2 key sub-tiles x 2 row tiles.
+        // A-row r of sub-tile sb is token 8*((r>>2)&1) + 4*sb + (r&3) of block
+        // r>>3, i.e. unit key 8*(r>>2) + 4*sb + (r&3).  Per-lane byte offsets of
+        // the K rows read for sub-tile sb and k-step ks, relative to the unit.
+        // They are made opaque to the compiler so that no constant part is split
+        // off the address: the split loses the LDS alias information that lets
+        // these reads overlap the loads still in flight.
+        int kroff[2][KS];
+    #pragma unroll
+        for (int sb = 0; sb < 2; ++sb) {
+            const int b = c16 >> 3;
+            const int t = 8 * ((c16 >> 2) & 1) + 4 * sb + (c16 & 3);
+            const int sw = kswz<D>(b, t);
+    #pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                kroff[sb][ks] = b * C::kBlockBytes + t * (D * 2) + ((ks * 4 + g4) ^ sw) * 16;
+                asm volatile("" : "+v"(kroff[sb][ks]));
+            }
+        }
+        // Operands are read from LDS one phase before the MFMAs that use them:
+        // kop (K of the next unit) while the current P V runs, vop (V of the
+        // current unit) while the next scores are computed.
+        bf16x8 kop[2][KS];
+        bf16x8 vop[NDT];
+        auto read_k = [&](const uint8_t *lk) {
+    #pragma unroll
+            for (int sb = 0; sb < 2; ++sb)
+    #pragma unroll
+                for (int ks = 0; ks < KS; ++ks)
+                    kop[sb][ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(lk + kroff[sb][ks]));
+        };
+        auto qk_mfma = [&](f32x4 (&acc)[kRT][2]) {
+    #pragma unroll
+            for (int sb = 0; sb < 2; ++sb) {
+    #pragma unroll
+                for (int rt = 0; rt < kRT; ++rt) acc[rt][sb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    #pragma unroll
+                for (int ks = 0; ks < KS; ++ks)
+    #pragma unroll
+                    for (int rt = 0; rt < kRT; ++rt)
+                        acc[rt][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop[sb][ks], qop[rt][ks], acc[rt][sb], 0, 0, 0);
+            }
+        };
+        // Causal mask of a unit whose first key is key0 (lane group g4 holds unit
+        // keys 8*g4 + 4*sb + i); only units that reach past the smallest causal
+        // limit of the wave's rows need it.
+        auto mask_unit = [&](f32x4 (&acc)[kRT][2], int key0) {
+            if (key0 + 31 <= wave_lim_min) return;
+    #pragma unroll
+            for (int rt = 0; rt < kRT; ++rt) {
+                const int lim = row_lim[rt] - key0 - 8 * g4;
+    #pragma unroll
+                for (int sb = 0; sb < 2; ++sb)
+    #pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        if (4 * sb + i > lim) acc[rt][sb][i] = -INFINITY;
+            }
+        };
+        // Largest of a lane's 8 values of one row tile (NaN-propagating).
+        auto lane_max = [&](const f32x4 (&acc)[2]) {
+            const f32x4 x0 = acc[0], x1 = acc[1];
+            return fmax3(fmax3(x0[0], x0[1], x0[2]), fmax3(x0[3], x1[0], x1[1]), fmax3(x1[2], x1[3], x1[3]));
+        };
+        // Scores -> exp2 arguments S * scale * log2(e) - m' (phase B).
+        auto scale_unit = [&](f32x4 (&acc)[kRT][2]) {
+    #pragma unroll
+            for (int rt = 0; rt < kRT; ++rt)
+    #pragma unroll
+                for (int sb = 0; sb < 2; ++sb)
+    #pragma unroll
+                    for (int i = 0; i < 4; ++i) acc[rt][sb][i] = __builtin_fmaf(acc[rt][sb][i], sl2, nm[rt]);
+        };
+        // P = exp2(S * scale * log2 e - m') in bf16 (B operand of PV), and the
+        // lane's sum of the rounded values per row tile.
+        auto exp_unit = [&](const f32x4 (&acc)[kRT][2], bf16x8 (&pop)[kRT], float (&us)[kRT]) {
+    #pragma unroll
+            for (int rt = 0; rt < kRT; ++rt) {
+                uint32_t w[4];
+                us[rt] = 0.f;
+    #pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const f32x4 &x = acc[rt][j >> 1];
+                    const int i0 = 2 * (j & 1);
+                    const bf16x2 pk = {(__bf16)__builtin_amdgcn_exp2f(x[i0]), (__bf16)__builtin_amdgcn_exp2f(x[i0 + 1])};
+                    us[rt] = __builtin_amdgcn_fdot2_f32_bf16(pk, ones2, us[rt], false);
+                    w[j] = __builtin_bit_cast(uint32_t, pk);
+                }
+                pop[rt] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
+            }
+        };
+        // After the B phase that follows a unit's P (and before its P V): when
+        // some lane's sum exceeds the limit (a probability above 2^13, an infinite
+        // one included), the rows' maxima are raised to the unit's row maxima.  O
+        // and l (which hold the units before it) are rescaled, the exp2 arguments
+        // of the unit and of the next unit (already scaled) shifted, and the unit's
+        // P recomputed (at most 1 now).  Rows whose max did not move shift by 0.
+        // Then the unit's sums join l.
+        auto settle = [&](f32x4 (&acc)[kRT][2], f32x4 (&next)[kRT][2], bf16x8 (&pop)[kRT], float (&us)[kRT]) {
+            bool over = false;
+    #pragma unroll
+            for (int rt = 0; rt < kRT; ++rt) over = over || us[rt] > kSumLimit;
+            if (__any(over)) {
+    #pragma unroll
+                for (int rt = 0; rt < kRT; ++rt) {
+                    const float shift = __builtin_elementwise_maximum(xmax16_32(lane_max(acc[rt])), 0.f);
+                    const float alpha = __builtin_amdgcn_exp2f(-shift);
+                    lsum[rt] *= alpha;
+    #pragma unroll
+                    for (int dt = 0; dt < NDT; ++dt) o[rt][dt] *= alpha;
+                    nm[rt] -= shift;
+                    acc[rt][0] -= shift;
+                    acc[rt][1] -= shift;
+                    next[rt][0] -= shift;
+                    next[rt][1] -= shift;
+                }
+                exp_unit(acc, pop, us);
+            }
+    #pragma unroll
+            for (int rt = 0; rt < kRT; ++rt) lsum[rt] += us[rt];
+        };
+        // Per-lane byte offset of the V chunk this lane reads, opaque for the same
+        // reason as kroff.  Dims dt*16 + c16 of one lane are 256 bytes apart.
+        int vroff = (g4 >> 1) * C::kBlockBytes + ((g4 & 1) * D + c16) * 16;
+        asm volatile("" : "+v"(vroff));
+        auto read_v = [&](const uint8_t *lv, int h) {
+            const uint8_t *blkv = lv + 2 * h * C::kBlockBytes + vroff;
+    #pragma unroll
+            for (int dt = 0; dt < NDT; ++dt)
+                vop[dt] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(blkv + dt * 256));
+        };
+        // O^T += V^T P^T for one unit.
+        auto pv_mfma = [&](const bf16x8 (&pop)[kRT]) {
+    #pragma unroll
+            for (int dt = 0; dt < NDT; ++dt)
+    #pragma unroll
+                for (int rt = 0; rt < kRT; ++rt)
+                    o[rt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop[dt], pop[rt], o[rt][dt], 0, 0, 0);
+        };
+        // Instruction order inside a phase: each MFMA is followed by a share of
+        // the phase's VALU work and, every other MFMA, by one operand read for the
+        // next phase, so that the softmax arithmetic issues while the matrix core
+        // is busy and every LDS read has a whole phase to return.
+        constexpr int kPhaseMfma = 2 * KS * kRT;              // == NDT * kRT
+        constexpr int kExpTrans = kRT * 4 * 2;                // exp phase: 2 exp ...
+        constexpr int kExpValu = kRT * 4 * 2;                 // ... and cvt, dot2 per pair
+        constexpr int kScaleValu = kRT * 8;                   // scale phase: the FMAs
+        // Keeps the probabilities of a phase from being computed later (after the
+        // masking branch that follows the phase).
+        auto pin = [&](const bf16x8 (&pop)[kRT]) {
+    #pragma unroll
+            for (int rt = 0; rt < kRT; ++rt) asm volatile("" ::"v"(pop[rt]));
+        };
+        // Values of keys at or past kv_len (the rest of the session's last block,
+        // or blocks never loaded) are zeroed in the staged V tile of key tile j
+        // before it is used, so that 0 * NaN cannot reach O.  Only the last key
+        // tile can hold such keys; one extra LDS barrier, once per workgroup.
+        auto zero_v_tail = [&](uint8_t *lv, int j) {
+            constexpr int kChunks = 4 * 2 * D;                    // (block, half, dim) chunks of 8 tokens
+            for (int ci = tid; ci < kChunks; ci += kPreThreads) {
+                const int bi = ci / (2 * D), hf = (ci / D) & 1;
+                const int t0 = j * kKeyTile + bi * kBlock + hf * 8;
+                if (t0 + 8 <= kv_len) continue;
+                u32x4 *chunk = reinterpret_cast<u32x4 *>(lv + ci * 16);
+                u32x4 x = *chunk;
+    #pragma unroll
+                for (int w = 0; w < 4; ++w) {
+                    const int t = t0 + 2 * w;
+                    x[w] &= t + 1 < kv_len ? 0xFFFFFFFFu : (t < kv_len ? 0x0000FFFFu : 0u);
+                }
+                *chunk = x;
+            }
+            __builtin_amdgcn_s_waitcnt(0xC07F);                   // lgkmcnt(0) only
+            asm volatile("" ::: "memory");
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+        };
+
+        // ---- pipeline over 32-key units.  Key tile j (units 2j, 2j+1) reads
+        // stage j: K of units 2j+1, 2j+2 and V of units 2j, 2j+1; it also reads V
+        // of unit 2j-1 from stage j-1.  While it is processed, the loads of stage
+        // j+2 go into buffer (j+2) % 4, last read in tile j-1.  A tile runs four
+        // phases, each followed by the test of the P made one phase before:
+        //   A0: scores of unit 2j+1 | P of unit 2j          | read V of unit 2j-1
+        //   B0: P V of unit 2j-1    | scale of unit 2j+1    | read K of unit 2j+2
+        //       (test P of unit 2j)
+        //   A1: scores of unit 2j+2 | P of unit 2j+1        | read V of unit 2j
+        //   -- barrier: stage j+1 has landed; stage j-1 is fully read --
+        //   B1: P V of unit 2j      | scale of unit 2j+2    | read K of unit 2j+3
+        //       (test P of unit 2j+1)
+        // The last tile then reads V of its second unit and adds its P V.  A wave
+        // in a B phase runs at raised issue priority: of the two waves sharing a
+        // SIMD, the one feeding P V (light VALU) then issues its MFMAs first while
+        // the other's exp work fills the VALU slots.
+        f32x4 sa[kRT][2], sb2[kRT][2];
+        bf16x8 pop_e[kRT], pop_o[kRT];        // P of the even and odd unit in flight
+        float us_e[kRT], us_o[kRT];
+    #pragma unroll
+        for (int rt = 0; rt < kRT; ++rt) pop_o[rt] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+        int32_t idk = id_k(-1), idv = id_v(-1);
+        load_k(k3, idk);                      // stage -1: K unit 0 (its V part is empty)
+        load_v(v3, idv);
+        idk = id_k(0); idv = id_v(0);
+        load_k(k0, idk);
+        load_v(v0, idv);
+        idk = id_k(1); idv = id_v(1);
+        load_k(k1, idk);
+        load_v(v1, idv);
+        idk = id_k(2); idv = id_v(2);
+        stage_barrier<D>();                   // stages -1 and 0 have landed
+        // V of unit -1 (second half of stage -1's V): zeros, so that the first
+        // tile's P V of that unit (with P = 0) adds nothing.
+        for (int ci = tid; ci < 2 * C::kBlockBytes / 16; ci += kPreThreads)
+            *reinterpret_cast<u32x4 *>(v3 + 2 * C::kBlockBytes + ci * 16) = u32x4{0u, 0u, 0u, 0u};
+        read_k(k3 + C::kUnitBytes);           // unit 0 = second unit of stage -1
+        qk_mfma(sa);
+        read_k(k0);                           // unit 1
+        mask_unit(sa, 0);
+        // The first unit's row maxima start the running maxima (every row sees key 0).
+    #pragma unroll
+        for (int rt = 0; rt < kRT; ++rt) nm[rt] = -xmax16_32(lane_max(sa[rt])) * sl2;
+        scale_unit(sa);
+        __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): the zeros are written
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+
+        // The loads are issued on every path, so outstanding loads are counted
+        // exactly; only the compute of tiles past the last one is skipped.
+        auto tile = [&](int j, const uint8_t *ks, uint8_t *vs, const uint8_t *vprev, const uint8_t *knext,
+                        uint8_t *kn, uint8_t *vn) {
+            const int32_t ik = idk, iv = idv;
+            idk = id_k(j + 3);
+            idv = id_v(j + 3);
+            const bool live = j < ntiles;
+            if (live && (j + 1) * kKeyTile > kv_len) zero_v_tail(vs, j);
+            load_k(kn, ik);
+            load_v(vn, iv);
+            if (live) {
+                qk_mfma(sb2);                           // A0
+                exp_unit(sa, pop_e, us_e);
+                read_v(vprev, 1);
+                order_phase<0, kPhaseMfma, NDT, kExpTrans, kExpValu>();
+                pin(pop_e);
+                mask_unit(sb2, j * kKeyTile + 32);
+                __builtin_amdgcn_s_setprio(1);          // B phases issue first
+                pv_mfma(pop_o);                         // B0
+                scale_unit(sb2);
+                read_k(ks + C::kUnitBytes);
+                order_phase<0, kPhaseMfma, 2 * KS, 0, kScaleValu>();
+                __builtin_amdgcn_s_setprio(0);
+                settle(sa, sb2, pop_e, us_e);
+                qk_mfma(sa);                            // A1
+                exp_unit(sb2, pop_o, us_o);
+                read_v(vs, 0);
+                order_phase<0, kPhaseMfma, NDT, kExpTrans, kExpValu>();
+                pin(pop_o);
+                mask_unit(sa, (j + 1) * kKeyTile);
+            }
+            stage_barrier<D>();
+            if (live) {
+                __builtin_amdgcn_s_setprio(1);
+                pv_mfma(pop_e);                         // B1
+                scale_unit(sa);
+                read_k(knext);                          // (unused when tile j+1 is past the end)
+                order_phase<0, kPhaseMfma, 2 * KS, 0, kScaleValu>();
+                __builtin_amdgcn_s_setprio(0);
+                settle(sb2, sa, pop_o, us_o);
+                if (j == ntiles - 1) {                  // the last unit's P V
+                    read_v(vs, 1);
+                    pv_mfma(pop_o);
+                }
+            }
+        };
+        for (int j = 0; j < ntiles; j += 4) {
+            tile(j, k0, v0, v3, k1, k2, v2);
+            tile(j + 1, k1, v1, v0, k2, k3, v3);
+            tile(j + 2, k2, v2, v1, k3, k0, v0);
+            tile(j + 3, k3, v3, v2, k0, k1, v1);
+        }
+
+        // ---- normalise and write
+    #pragma unroll
+        for (int rt = 0; rt < kRT; ++rt) {
+            const float inv = 1.f / xsum16_32(lsum[rt]);
+            if (!row_ok[rt]) continue;
+            uint16_t *orow = a.out + row_out[rt];
+    #pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) {
+                const u32x2 w = u32x2{pack_bf16x2(o[rt][dt][0] * inv, o[rt][dt][1] * inv),
+                                      pack_bf16x2(o[rt][dt][2] * inv, o[rt][dt][3] * inv)};
+                *reinterpret_cast<u32x2 *>(orow + dt * 16 + g4 * 4) = w;
+            }
+        }
+    };
 
     // ---- schedule.  Items are (session s, KV head g, query tile qt).  All query
     // tiles of one (s, g) pair run on one XCD, so they stream the same keys
@@ -274,20 +666,66 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a, Pre
         }
     int s, g, qt;
     if constexpr (kHost) {
-        // Entry of this workgroup: the last one of its XCD whose earlier items
-        // are at most its slot (entries have items, so 'before' increases; an
-        // XCD has at most kPlanPairs / 8 entries, one per lane).
-        const int xcd = (int)(blockIdx.x % kXcds);
-        const uint32_t slot = blockIdx.x / kXcds;
-        if (slot >= plan.total[xcd]) return;
-        const int b = plan.start[xcd], m = plan.start[xcd + 1] - b;
-        const int ln = tid % kWave;
-        const bool passed = ln < m && plan.before[b + min(ln, m - 1)] <= slot;
-        const int e = b + __popcll(__ballot(passed)) - 1;
-        const uint32_t items = (e + 1 < b + m ? plan.before[e + 1] : plan.total[xcd]) - plan.before[e];
-        qt = (int)(items - 1 - (slot - plan.before[e]));
-        s = plan.pair[e] / Hkv;
-        g = plan.pair[e] % Hkv;
+        // Item `slot` of XCD x's list: the entry of the last pair whose earlier
+        // items are at most the slot (entries have items, so 'before' increases;
+        // an XCD has at most kPlanPairs / 8 entries, one per lane).
+        auto lookup = [&](int x, uint32_t slot) {
+            const int b = plan.start[x], m = plan.start[x + 1] - b;
+            const int ln = tid % kWave;
+            const bool passed = ln < m && plan.before[b + min(ln, m - 1)] <= slot;
+            const int e = b + __popcll(__ballot(passed)) - 1;
+            const uint32_t items = (e + 1 < b + m ? plan.before[e + 1] : plan.total[x]) - plan.before[e];
+            qt = (int)(items - 1 - (slot - plan.before[e]));
+            s = plan.pair[e] / Hkv;
+            g = plan.pair[e] % Hkv;
+        };
+        // Without counters, workgroup i takes item i / 8 of XCD i % 8.  With
+        // them (a.queue), workgroup i takes the next item of XCD i % 8's list
+        // through a counter per XCD, and once that list is exhausted, the next
+        // item of the XCD with the most items left (the grid has ~10% more
+        // workgroups than items; the ones that find every list exhausted end).
+        // XCDs run at different speeds (several percent apart), so with a fixed
+        // deal the fast ones idle at the end.  Each list is tried at most once
+        // after it ran out, so the search ends.
+        const int home = (int)(blockIdx.x % kXcds);
+        if (a.queue) {
+            if (tid == 0) {
+                int gx = -1;
+                uint32_t gs = atomicAdd(&a.queue[home], 1u);
+                if (gs < plan.total[home]) {
+                    gx = home;
+                } else {
+                    uint32_t tried = 1u << home;
+                    while (gx < 0) {
+                        int best = -1;
+                        int64_t most = 0;
+                        for (int y = 0; y < kXcds; ++y) {
+                            if ((tried >> y) & 1u) continue;
+                            const int64_t left =
+                                (int64_t)plan.total[y] -
+                                (int64_t)__hip_atomic_load(&a.queue[y], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                            if (left > most) {
+                                most = left;
+                                best = y;
+                            }
+                        }
+                        if (best < 0) break;                       // every list is exhausted
+                        gs = atomicAdd(&a.queue[best], 1u);
+                        if (gs < plan.total[best]) gx = best;
+                        else tried |= 1u << best;
+                    }
+                }
+                sm_grab[0] = gx;
+                sm_grab[1] = (int)gs;
+            }
+            __syncthreads();
+            if (sm_grab[0] < 0) return;
+            lookup(sm_grab[0], (uint32_t)sm_grab[1]);
+        } else {
+            const uint32_t slot = blockIdx.x / kXcds;
+            if (slot >= plan.total[home]) return;
+            lookup(home, slot);
+        }
     } else if (P <= kMaxPairs) {
         for (int p = tid; p < P; p += kPreThreads) {
             const int sp = p / Hkv;
@@ -349,392 +787,7 @@ __global__ __launch_bounds__(kPreThreads) void prefill_kernel(PrefillArgs a, Pre
         s = (int)(lg / ((int64_t)QT * Hkv));
     }
 
-    const int n = a.cu[s + 1] - a.cu[s];
-    const int j0 = qt * qtok;
-    if (j0 >= n || a.cu[s] < 0 || a.cu[s + 1] > a.total) return;   // (lengths outside q: flagged above)
-    const int c = a.ctx[s];
-    const int j_last = min(j0 + qtok, n) - 1;
-    const int kv_len = c + n;
-    int nblk_valid = (kv_len + kBlock - 1) / kBlock;
-    if (nblk_valid > a.max_blocks) {
-        nblk_valid = a.max_blocks;
-        if (tid == 0) flag_error(a.err, LS_DEVERR_LENGTH);
-    }
-    const int kv_end = c + j_last + 1;                    // keys this tile can see
-    const int ntiles = (kv_end + kKeyTile - 1) / kKeyTile;
-    const int nb = min(nblk_valid, ntiles * 4);           // blocks any row here can see
-
-    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
-    const int lane = tid % kWave;
-    const int c16 = lane & 15;
-    const int g4 = lane >> 4;
-    const int hq_total = Hkv * G;
-
-    // Rows of this lane (one per 16-row tile): r = wave*32 + rt*16 + c16.
-    int row_lim[kRT];
-    int64_t row_out[kRT];
-    bool row_ok[kRT];
-    bf16x8 qop[kRT][KS];
-#pragma unroll
-    for (int rt = 0; rt < kRT; ++rt) {
-        const int r = wave * kWaveRows + rt * 16 + c16;
-        const int jl = j0 + r / G;
-        const int h = r % G;
-        row_ok[rt] = jl < n;
-        const int jc = min(jl, n - 1);
-        row_lim[rt] = c + jc;
-        const int64_t tok = (int64_t)a.cu[s] + jc;
-        row_out[rt] = (tok * hq_total + g * G + h) * D;
-        const uint16_t *qrow = a.q + row_out[rt];
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-            qop[rt][ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(qrow + ks * 32 + g4 * 8));
-    }
-    // Wait for q here, before the first stage loads are issued, so that no
-    // wait for q remains inside the key loop (vmcnt(0), other counters untouched).
-    __builtin_amdgcn_s_waitcnt(0x0F70);
-    // smallest causal limit among this wave's rows: units past it need masking
-    const int wave_lim_min = c + min(j0 + (wave * kWaveRows) / G, n - 1);
-
-    // ---- this wave's share of every stage: kLoadsK kilobytes of one K block
-    // and of one V block (block 'blk' of the stage), at fixed lane offsets.
-    const int blk = (wave * C::kLoadsK) / C::kKbPerBlock;
-    int k_voff[C::kLoadsK], v_voff[C::kLoadsK], kb_off[C::kLoadsK];
-#pragma unroll
-    for (int e = 0; e < C::kLoadsK; ++e) {
-        const int q = (wave * C::kLoadsK + e) % C::kKbPerBlock;       // kilobyte within the block
-        kb_off[e] = blk * C::kBlockBytes + q * 1024;
-        // K: lane -> (token, slot); fetch the chunk that belongs in that slot
-        const int t = q * (1024 / (D * 2)) + lane / C::kRowChunks;
-        const int sl = lane % C::kRowChunks;
-        k_voff[e] = ((sl ^ kswz<D>(blk & 1, t)) * kBlock + t) * 16;   // chunk-major K tile
-        // V: lane -> chunk position p = half*D + dim
-        const int p = q * 64 + lane;
-        v_voff[e] = (p % D) * 32 + (p / D) * 16;
-    }
-    const int32_t *table = a.block_tables + (int64_t)s * a.max_blocks;
-    const uint32_t slab_elems = (uint32_t)(2 * Hkv * kBlock * D);
-    const uint32_t nblocks32 = (uint32_t)min(a.num_blocks, (int64_t)0x7fffffff);
-    const uint16_t *kbase = a.pool + (int64_t)g * (kBlock * D);
-    const uint16_t *vbase = kbase + (int64_t)Hkv * (kBlock * D);
-    auto load_k = [&](uint8_t *stage, int32_t b) {
-#pragma unroll
-        for (int e = 0; e < C::kLoadsK; ++e) load_kb<D>(kbase, slab_elems, nblocks32, b, stage + kb_off[e], k_voff[e]);
-    };
-    auto load_v = [&](uint8_t *stage, int32_t b) {
-#pragma unroll
-        for (int e = 0; e < C::kLoadsK; ++e) load_kb<D>(vbase, slab_elems, nblocks32, b, stage + kb_off[e], v_voff[e]);
-    };
-    auto id_k = [&](int t) { return table_entry(table, 4 * t + 2 + blk, nb); };
-    auto id_v = [&](int t) { return table_entry(table, 4 * t + blk, nb); };
-
-    float nm[kRT], lsum[kRT];             // -m' (running row max * scale * log2 e),
-    f32x4 o[kRT][NDT];                    // partial row sums, unnormalised output
-#pragma unroll
-    for (int rt = 0; rt < kRT; ++rt) {
-        nm[rt] = 0.f;
-        lsum[rt] = 0.f;
-    }
-#pragma unroll
-    for (int rt = 0; rt < kRT; ++rt)
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) o[rt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const float sl2 = a.scale_log2;
-    const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
-
-    // ---- S^T = K Q^T of one 32-key unit for 2 key sub-tiles x 2 row tiles.
-    // A-row r of sub-tile sb is token 8*((r>>2)&1) + 4*sb + (r&3) of block
-    // r>>3, i.e. unit key 8*(r>>2) + 4*sb + (r&3).  Per-lane byte offsets of
-    // the K rows read for sub-tile sb and k-step ks, relative to the unit.
-    // They are made opaque to the compiler so that no constant part is split
-    // off the address: the split loses the LDS alias information that lets
-    // these reads overlap the loads still in flight.
-    int kroff[2][KS];
-#pragma unroll
-    for (int sb = 0; sb < 2; ++sb) {
-        const int b = c16 >> 3;
-        const int t = 8 * ((c16 >> 2) & 1) + 4 * sb + (c16 & 3);
-        const int sw = kswz<D>(b, t);
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            kroff[sb][ks] = b * C::kBlockBytes + t * (D * 2) + ((ks * 4 + g4) ^ sw) * 16;
-            asm volatile("" : "+v"(kroff[sb][ks]));
-        }
-    }
-    // Operands are read from LDS one phase before the MFMAs that use them:
-    // kop (K of the next unit) while the current P V runs, vop (V of the
-    // current unit) while the next scores are computed.
-    bf16x8 kop[2][KS];
-    bf16x8 vop[NDT];
-    auto read_k = [&](const uint8_t *lk) {
-#pragma unroll
-        for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
-                kop[sb][ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(lk + kroff[sb][ks]));
-    };
-    auto qk_mfma = [&](f32x4 (&acc)[kRT][2]) {
-#pragma unroll
-        for (int sb = 0; sb < 2; ++sb) {
-#pragma unroll
-            for (int rt = 0; rt < kRT; ++rt) acc[rt][sb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-                for (int rt = 0; rt < kRT; ++rt)
-                    acc[rt][sb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop[sb][ks], qop[rt][ks], acc[rt][sb], 0, 0, 0);
-        }
-    };
-    // Causal mask of a unit whose first key is key0 (lane group g4 holds unit
-    // keys 8*g4 + 4*sb + i); only units that reach past the smallest causal
-    // limit of the wave's rows need it.
-    auto mask_unit = [&](f32x4 (&acc)[kRT][2], int key0) {
-        if (key0 + 31 <= wave_lim_min) return;
-#pragma unroll
-        for (int rt = 0; rt < kRT; ++rt) {
-            const int lim = row_lim[rt] - key0 - 8 * g4;
-#pragma unroll
-            for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    if (4 * sb + i > lim) acc[rt][sb][i] = -INFINITY;
-        }
-    };
-    // Largest of a lane's 8 values of one row tile (NaN-propagating).
-    auto lane_max = [&](const f32x4 (&acc)[2]) {
-        const f32x4 x0 = acc[0], x1 = acc[1];
-        return fmax3(fmax3(x0[0], x0[1], x0[2]), fmax3(x0[3], x1[0], x1[1]), fmax3(x1[2], x1[3], x1[3]));
-    };
-    // Scores -> exp2 arguments S * scale * log2(e) - m' (phase B).
-    auto scale_unit = [&](f32x4 (&acc)[kRT][2]) {
-#pragma unroll
-        for (int rt = 0; rt < kRT; ++rt)
-#pragma unroll
-            for (int sb = 0; sb < 2; ++sb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) acc[rt][sb][i] = __builtin_fmaf(acc[rt][sb][i], sl2, nm[rt]);
-    };
-    // P = exp2(S * scale * log2 e - m') in bf16 (B operand of PV), and the
-    // lane's sum of the rounded values per row tile.
-    auto exp_unit = [&](const f32x4 (&acc)[kRT][2], bf16x8 (&pop)[kRT], float (&us)[kRT]) {
-#pragma unroll
-        for (int rt = 0; rt < kRT; ++rt) {
-            uint32_t w[4];
-            us[rt] = 0.f;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const f32x4 &x = acc[rt][j >> 1];
-                const int i0 = 2 * (j & 1);
-                const bf16x2 pk = {(__bf16)__builtin_amdgcn_exp2f(x[i0]), (__bf16)__builtin_amdgcn_exp2f(x[i0 + 1])};
-                us[rt] = __builtin_amdgcn_fdot2_f32_bf16(pk, ones2, us[rt], false);
-                w[j] = __builtin_bit_cast(uint32_t, pk);
-            }
-            pop[rt] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
-        }
-    };
-    // After the B phase that follows a unit's P (and before its P V): when
-    // some lane's sum exceeds the limit (a probability above 2^13, an infinite
-    // one included), the rows' maxima are raised to the unit's row maxima.  O
-    // and l (which hold the units before it) are rescaled, the exp2 arguments
-    // of the unit and of the next unit (already scaled) shifted, and the unit's
-    // P recomputed (at most 1 now).  Rows whose max did not move shift by 0.
-    // Then the unit's sums join l.
-    auto settle = [&](f32x4 (&acc)[kRT][2], f32x4 (&next)[kRT][2], bf16x8 (&pop)[kRT], float (&us)[kRT]) {
-        bool over = false;
-#pragma unroll
-        for (int rt = 0; rt < kRT; ++rt) over = over || us[rt] > kSumLimit;
-        if (__any(over)) {
-#pragma unroll
-            for (int rt = 0; rt < kRT; ++rt) {
-                const float shift = __builtin_elementwise_maximum(xmax16_32(lane_max(acc[rt])), 0.f);
-                const float alpha = __builtin_amdgcn_exp2f(-shift);
-                lsum[rt] *= alpha;
-#pragma unroll
-                for (int dt = 0; dt < NDT; ++dt) o[rt][dt] *= alpha;
-                nm[rt] -= shift;
-                acc[rt][0] -= shift;
-                acc[rt][1] -= shift;
-                next[rt][0] -= shift;
-                next[rt][1] -= shift;
-            }
-            exp_unit(acc, pop, us);
-        }
-#pragma unroll
-        for (int rt = 0; rt < kRT; ++rt) lsum[rt] += us[rt];
-    };
-    // Per-lane byte offset of the V chunk this lane reads, opaque for the same
-    // reason as kroff.  Dims dt*16 + c16 of one lane are 256 bytes apart.
-    int vroff = (g4 >> 1) * C::kBlockBytes + ((g4 & 1) * D + c16) * 16;
-    asm volatile("" : "+v"(vroff));
-    auto read_v = [&](const uint8_t *lv, int h) {
-        const uint8_t *blkv = lv + 2 * h * C::kBlockBytes + vroff;
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt)
-            vop[dt] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(blkv + dt * 256));
-    };
-    // O^T += V^T P^T for one unit.
-    auto pv_mfma = [&](const bf16x8 (&pop)[kRT]) {
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-            for (int rt = 0; rt < kRT; ++rt)
-                o[rt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop[dt], pop[rt], o[rt][dt], 0, 0, 0);
-    };
-    // Instruction order inside a phase: each MFMA is followed by a share of
-    // the phase's VALU work and, every other MFMA, by one operand read for the
-    // next phase, so that the softmax arithmetic issues while the matrix core
-    // is busy and every LDS read has a whole phase to return.
-    constexpr int kPhaseMfma = 2 * KS * kRT;              // == NDT * kRT
-    constexpr int kExpTrans = kRT * 4 * 2;                // exp phase: 2 exp ...
-    constexpr int kExpValu = kRT * 4 * 2;                 // ... and cvt, dot2 per pair
-    constexpr int kScaleValu = kRT * 8;                   // scale phase: the FMAs
-    // Keeps the probabilities of a phase from being computed later (after the
-    // masking branch that follows the phase).
-    auto pin = [&](const bf16x8 (&pop)[kRT]) {
-#pragma unroll
-        for (int rt = 0; rt < kRT; ++rt) asm volatile("" ::"v"(pop[rt]));
-    };
-    // Values of keys at or past kv_len (the rest of the session's last block,
-    // or blocks never loaded) are zeroed in the staged V tile of key tile j
-    // before it is used, so that 0 * NaN cannot reach O.  Only the last key
-    // tile can hold such keys; one extra LDS barrier, once per workgroup.
-    auto zero_v_tail = [&](uint8_t *lv, int j) {
-        constexpr int kChunks = 4 * 2 * D;                    // (block, half, dim) chunks of 8 tokens
-        for (int ci = tid; ci < kChunks; ci += kPreThreads) {
-            const int bi = ci / (2 * D), hf = (ci / D) & 1;
-            const int t0 = j * kKeyTile + bi * kBlock + hf * 8;
-            if (t0 + 8 <= kv_len) continue;
-            u32x4 *chunk = reinterpret_cast<u32x4 *>(lv + ci * 16);
-            u32x4 x = *chunk;
-#pragma unroll
-            for (int w = 0; w < 4; ++w) {
-                const int t = t0 + 2 * w;
-                x[w] &= t + 1 < kv_len ? 0xFFFFFFFFu : (t < kv_len ? 0x0000FFFFu : 0u);
-            }
-            *chunk = x;
-        }
-        __builtin_amdgcn_s_waitcnt(0xC07F);                   // lgkmcnt(0) only
-        asm volatile("" ::: "memory");
-        __builtin_amdgcn_s_barrier();
-        asm volatile("" ::: "memory");
-    };
-
-    // ---- pipeline over 32-key units.  Key tile j (units 2j, 2j+1) reads
-    // stage j: K of units 2j+1, 2j+2 and V of units 2j, 2j+1; it also reads V
-    // of unit 2j-1 from stage j-1.  While it is processed, the loads of stage
-    // j+2 go into buffer (j+2) % 4, last read in tile j-1.  A tile runs four
-    // phases, each followed by the test of the P made one phase before:
-    //   A0: scores of unit 2j+1 | P of unit 2j          | read V of unit 2j-1
-    //   B0: P V of unit 2j-1    | scale of unit 2j+1    | read K of unit 2j+2
-    //       (test P of unit 2j)
-    //   A1: scores of unit 2j+2 | P of unit 2j+1        | read V of unit 2j
-    //   -- barrier: stage j+1 has landed; stage j-1 is fully read --
-    //   B1: P V of unit 2j      | scale of unit 2j+2    | read K of unit 2j+3
-    //       (test P of unit 2j+1)
-    // The last tile then reads V of its second unit and adds its P V.  A wave
-    // in a B phase runs at raised issue priority: of the two waves sharing a
-    // SIMD, the one feeding P V (light VALU) then issues its MFMAs first while
-    // the other's exp work fills the VALU slots.
-    f32x4 sa[kRT][2], sb2[kRT][2];
-    bf16x8 pop_e[kRT], pop_o[kRT];        // P of the even and odd unit in flight
-    float us_e[kRT], us_o[kRT];
-#pragma unroll
-    for (int rt = 0; rt < kRT; ++rt) pop_o[rt] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
-    int32_t idk = id_k(-1), idv = id_v(-1);
-    load_k(k3, idk);                      // stage -1: K unit 0 (its V part is empty)
-    load_v(v3, idv);
-    idk = id_k(0); idv = id_v(0);
-    load_k(k0, idk);
-    load_v(v0, idv);
-    idk = id_k(1); idv = id_v(1);
-    load_k(k1, idk);
-    load_v(v1, idv);
-    idk = id_k(2); idv = id_v(2);
-    stage_barrier<D>();                   // stages -1 and 0 have landed
-    // V of unit -1 (second half of stage -1's V): zeros, so that the first
-    // tile's P V of that unit (with P = 0) adds nothing.
-    for (int ci = tid; ci < 2 * C::kBlockBytes / 16; ci += kPreThreads)
-        *reinterpret_cast<u32x4 *>(v3 + 2 * C::kBlockBytes + ci * 16) = u32x4{0u, 0u, 0u, 0u};
-    read_k(k3 + C::kUnitBytes);           // unit 0 = second unit of stage -1
-    qk_mfma(sa);
-    read_k(k0);                           // unit 1
-    mask_unit(sa, 0);
-    // The first unit's row maxima start the running maxima (every row sees key 0).
-#pragma unroll
-    for (int rt = 0; rt < kRT; ++rt) nm[rt] = -xmax16_32(lane_max(sa[rt])) * sl2;
-    scale_unit(sa);
-    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): the zeros are written
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-
-    // The loads are issued on every path, so outstanding loads are counted
-    // exactly; only the compute of tiles past the last one is skipped.
-    auto tile = [&](int j, const uint8_t *ks, uint8_t *vs, const uint8_t *vprev, const uint8_t *knext,
-                    uint8_t *kn, uint8_t *vn) {
-        const int32_t ik = idk, iv = idv;
-        idk = id_k(j + 3);
-        idv = id_v(j + 3);
-        const bool live = j < ntiles;
-        if (live && (j + 1) * kKeyTile > kv_len) zero_v_tail(vs, j);
-        load_k(kn, ik);
-        load_v(vn, iv);
-        if (live) {
-            qk_mfma(sb2);                           // A0
-            exp_unit(sa, pop_e, us_e);
-            read_v(vprev, 1);
-            order_phase<0, kPhaseMfma, NDT, kExpTrans, kExpValu>();
-            pin(pop_e);
-            mask_unit(sb2, j * kKeyTile + 32);
-            __builtin_amdgcn_s_setprio(1);          // B phases issue first
-            pv_mfma(pop_o);                         // B0
-            scale_unit(sb2);
-            read_k(ks + C::kUnitBytes);
-            order_phase<0, kPhaseMfma, 2 * KS, 0, kScaleValu>();
-            __builtin_amdgcn_s_setprio(0);
-            settle(sa, sb2, pop_e, us_e);
-            qk_mfma(sa);                            // A1
-            exp_unit(sb2, pop_o, us_o);
-            read_v(vs, 0);
-            order_phase<0, kPhaseMfma, NDT, kExpTrans, kExpValu>();
-            pin(pop_o);
-            mask_unit(sa, (j + 1) * kKeyTile);
-        }
-        stage_barrier<D>();
-        if (live) {
-            __builtin_amdgcn_s_setprio(1);
-            pv_mfma(pop_e);                         // B1
-            scale_unit(sa);
-            read_k(knext);                          // (unused when tile j+1 is past the end)
-            order_phase<0, kPhaseMfma, 2 * KS, 0, kScaleValu>();
-            __builtin_amdgcn_s_setprio(0);
-            settle(sb2, sa, pop_o, us_o);
-            if (j == ntiles - 1) {                  // the last unit's P V
-                read_v(vs, 1);
-                pv_mfma(pop_o);
-            }
-        }
-    };
-    for (int j = 0; j < ntiles; j += 4) {
-        tile(j, k0, v0, v3, k1, k2, v2);
-        tile(j + 1, k1, v1, v0, k2, k3, v3);
-        tile(j + 2, k2, v2, v1, k3, k0, v0);
-        tile(j + 3, k3, v3, v2, k0, k1, v1);
-    }
-
-    // ---- normalise and write
-#pragma unroll
-    for (int rt = 0; rt < kRT; ++rt) {
-        const float inv = 1.f / xsum16_32(lsum[rt]);
-        if (!row_ok[rt]) continue;
-        uint16_t *orow = a.out + row_out[rt];
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) {
-            const u32x2 w = u32x2{pack_bf16x2(o[rt][dt][0] * inv, o[rt][dt][1] * inv),
-                                  pack_bf16x2(o[rt][dt][2] * inv, o[rt][dt][3] * inv)};
-            *reinterpret_cast<u32x2 *>(orow + dt * 16 + g4 * 4) = w;
-        }
-    }
+    run_item(s, g, qt);
 }
 
 }  // namespace
@@ -805,11 +858,17 @@ bool plan_prefill_host(int32_t S, int32_t hkv, int32_t qtok, const int32_t *lens
 
 }  // namespace
 
+// Zeroes the per-XCD item counters of a call (a kernel rather than a memset,
+// so that the call can be captured in a graph).
+__global__ void clear_queue_kernel(uint32_t *queue) {
+    if (threadIdx.x < kXcds) queue[threadIdx.x] = 0u;
+}
+
 hipError_t launch_prefill(const PoolGeom &p, int layer, int32_t num_sessions, int32_t num_q_heads,
                           const uint16_t *q, const int32_t *cu_new_lens,
                           const int32_t *reused_lens, const int32_t *lens_host, int32_t total_tokens,
                           int32_t max_new_len, const int32_t *block_tables, int32_t max_blocks,
-                          float scale, uint16_t *out, unsigned int *err, hipStream_t stream) {
+                          float scale, uint16_t *out, uint32_t *queue, unsigned int *err, hipStream_t stream) {
     if (num_sessions <= 0 || max_new_len <= 0) return hipSuccess;
     PrefillArgs a;
     a.pool = p.layer_base(layer);
@@ -826,13 +885,24 @@ hipError_t launch_prefill(const PoolGeom &p, int layer, int32_t num_sessions, in
     a.max_blocks = max_blocks;
     a.scale_log2 = scale * kLog2eP;
     a.err = err;
+    a.queue = nullptr;
     const int qtok = kPreRows / a.group;
     a.qtiles = (max_new_len + qtok - 1) / qtok;
     PrefillHostPlan plan;
     int32_t max_items = 0;
     if (lens_host && plan_prefill_host(num_sessions, p.num_kv_heads, qtok, lens_host, plan, max_items)) {
         if (max_items == 0) return hipSuccess;
-        const dim3 grid((unsigned)(kXcds * max_items));
+        dim3 grid((unsigned)(kXcds * max_items));
+        if (queue) {
+            // Items are taken through the counters; ~10% more workgroups than
+            // items let the faster XCDs take over the slower ones' last items.
+            hipLaunchKernelGGL(clear_queue_kernel, dim3(1), dim3(kWave), 0, stream, queue);
+            a.queue = queue;
+            int64_t items = 0;
+            for (int x = 0; x < kXcds; ++x) items += plan.total[x];
+            const int64_t per_xcd = (items + kXcds - 1) / kXcds + (items + 10 * kXcds - 1) / (10 * kXcds);
+            grid = dim3((unsigned)(kXcds * per_xcd));
+        }
         if (p.head_dim == 128)
             hipLaunchKernelGGL((prefill_kernel<128, true>), grid, dim3(kPreThreads), 0, stream, a, plan);
         else

@@ -47,7 +47,7 @@ _lib.ls_decode_schedule.restype = ctypes.c_int
 _lib.paged_attn_decode_static.argtypes = [_p, _i32, _i32, _i32, _p, _p, _p, _p, _i32, _p, _p, _f32,
                                           _p, _p]
 _lib.paged_attn_prefill.argtypes = [_p, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _i32, _i32, _p,
-                                    _i32, _f32, _p, _p]
+                                    _i32, _f32, _p, _p, _sz, _p]
 _f64 = ctypes.c_double
 _lib.kv_blocks_stash.argtypes = [_p, _i32, _p, _p, _p, _sz, _i32, _p, _sz, _f64, _p]
 _lib.kv_blocks_restore.argtypes = [_p, _i32, _p, _p, _p, _sz, _i32, _p, _sz, _f64, _p]
@@ -65,6 +65,7 @@ for _f in (_lib.kv_pool_create, _lib.kv_pool_destroy, _lib.paged_attn_decode,
 
 LS_OK, LS_EINVAL, LS_ENOMEM, LS_EHIP, LS_EUNSUPPORTED = 0, -22, -12, -5, -95
 LS_DEVERR_BLOCK_ID, LS_DEVERR_LENGTH, LS_DEVERR_INTERNAL = 0x1, 0x2, 0x4
+PREFILL_WORKSPACE_BYTES = 256     # LS_PREFILL_WORKSPACE_BYTES
 
 
 class LiveServeError(RuntimeError):
@@ -263,9 +264,12 @@ def paged_attn_prefill(pool: KVPool, layer: int, q: torch.Tensor, cu_new_lens: t
                        reused_lens: torch.Tensor, max_new_len: int, block_tables: torch.Tensor,
                        scale: float, out: torch.Tensor, k_new: Optional[torch.Tensor] = None,
                        v_new: Optional[torch.Tensor] = None, lens_host=None,
-                       stream=None) -> torch.Tensor:
+                       workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     """q/out: [T][Hq][D] bf16; cu_new_lens int32 [S+1]; reused_lens int32 [S];
-    k_new/v_new [T][Hkv][D] bf16; lens_host: optional host [S][2] of (n_s, c_s)."""
+    k_new/v_new [T][Hkv][D] bf16; lens_host: optional host [S][2] of (n_s, c_s);
+    workspace: optional device tensor of PREFILL_WORKSPACE_BYTES bytes (item
+    counters that let faster XCDs take over the slower ones' last tiles; used
+    with lens_host)."""
     if q.dim() != 3:
         raise ValueError("q must be [T][Hq][D]")
     total, hq = q.shape[0], q.shape[1]
@@ -285,10 +289,13 @@ def paged_attn_prefill(pool: KVPool, layer: int, q: torch.Tensor, cu_new_lens: t
         if t is not None:
             _dev(t, name)
     keep, hl = _host_i32(lens_host, "lens_host", 2 * s)
+    if workspace is not None:
+        _dev(workspace, "workspace")
     _check(_lib.paged_attn_prefill(pool.handle, layer, s, hq, _ptr(q), _ptr(k_new), _ptr(v_new),
                                    _ptr(cu_new_lens), _ptr(reused_lens), hl, total,
                                    int(max_new_len), _ptr(block_tables), block_tables.shape[1],
-                                   float(scale), _ptr(out), _stream(stream)),
+                                   float(scale), _ptr(out), _ptr(workspace),
+                                   0 if workspace is None else _nbytes(workspace), _stream(stream)),
            "paged_attn_prefill")
     del keep
     return out

@@ -147,14 +147,15 @@ def test_workspace_query(lib, pool):
 
 def _prefill(lib, pool, **kw):
     a = dict(layer=0, S=2, hq=32, q=F, kn=None, vn=None, cu=F, ctx=F, lens_host=None, total=100,
-             maxn=60, bt=F, maxb=8, scale=0.088, out=F)
+             maxn=60, bt=F, maxb=8, scale=0.088, out=F, ws=None, wsb=0)
     a.update(kw)
     return lib.paged_attn_prefill(pool, a["layer"], a["S"], a["hq"], ctypes.c_void_p(a["q"]),
                                   ctypes.c_void_p(a["kn"]), ctypes.c_void_p(a["vn"]),
                                   ctypes.c_void_p(a["cu"]), ctypes.c_void_p(a["ctx"]),
                                   _i32s(a["lens_host"]), a["total"], a["maxn"],
                                   ctypes.c_void_p(a["bt"]), a["maxb"], ctypes.c_float(a["scale"]),
-                                  ctypes.c_void_p(a["out"]), None)
+                                  ctypes.c_void_p(a["out"]), ctypes.c_void_p(a["ws"]),
+                                  ctypes.c_size_t(a["wsb"]), None)
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -170,6 +171,9 @@ def _prefill(lib, pool, **kw):
     (dict(lens_host=[60, 0, 39, 5]), LS_EINVAL),
     (dict(lens_host=[60, 70, 40, 5]), LS_EINVAL),
     (dict(lens_host=[60, 0, 40, -1]), LS_EINVAL),
+    # the item-counter workspace: too small, misaligned
+    (dict(ws=F, wsb=255), LS_ENOMEM),
+    (dict(ws=F + 8, wsb=256), LS_EINVAL),
 ])
 def test_prefill_rejects_before_launch(lib, pool, kw, status):
     assert _prefill(lib, pool, **kw) == status

@@ -38,27 +38,33 @@ def _case(rng, n, c, hq, hkv, d, spare=3):
     return pool, tables, q, kn, vn
 
 
-def _run(kv, dp, q, kn, vn, n, c, tables, scale, host=False):
+def _run(kv, dp, q, kn, vn, n, c, tables, scale, host=False, queue=False):
+    """host: lengths also on the host (host-dealt schedule); queue: with the
+    item-counter workspace (XCDs take over each other's last tiles)."""
     cu = np.concatenate([[0], np.cumsum(n)]).astype(np.int32)
     out = torch.empty((q.shape[0], q.shape[1], q.shape[2]), dtype=torch.bfloat16, device="cuda")
     lens_host = np.stack([np.asarray(n), np.asarray(c)], 1) if host else None
+    ws = torch.full((kv.PREFILL_WORKSPACE_BYTES,), 0x5A, dtype=torch.uint8, device="cuda") if queue else None
     kv.paged_attn_prefill(dp.pool, 0, bf16_dev(q), i32_dev(cu), i32_dev(c), int(np.max(n)),
-                          i32_dev(tables), scale, out, bf16_dev(kn), bf16_dev(vn), lens_host=lens_host)
+                          i32_dev(tables), scale, out, bf16_dev(kn), bf16_dev(vn), lens_host=lens_host,
+                          workspace=ws)
     return out, cu
 
 
-@pytest.mark.parametrize("host", [False, True], ids=["device-lengths", "host-lengths"])
+@pytest.mark.parametrize("mode", ["device-lengths", "host-lengths", "host-lengths-counters"])
 @pytest.mark.parametrize("d,hq,hkv", [(128, 32, 4), (64, 8, 2), (128, 8, 8), (128, 16, 8),
                                       (64, 4, 1)])
-def test_prefill_ragged(kv, oracle_lib, d, hq, hkv, host):
+def test_prefill_ragged(kv, oracle_lib, d, hq, hkv, mode):
     """Turn lengths and contexts around tile and block boundaries, c = 0 included;
-    the schedule dealt in the kernel, or on the host from host lengths."""
+    the schedule dealt in the kernel, or on the host from host lengths, with or
+    without the item counters (a workspace filled with garbage first)."""
     rng = np.random.default_rng(d + hq * 3 + hkv)
     n = [1, 17, 16, 130, 37, 255, 64]
     c = [0, 5, 300, 0, 1000, 77, 16]
     pool, tables, q, kn, vn = _case(rng, n, c, hq, hkv, d)
     dp = DevicePool(kv, pool, d)
-    out, cu = _run(kv, dp, q, kn, vn, np.array(n), np.array(c), tables, 1 / math.sqrt(d), host=host)
+    out, cu = _run(kv, dp, q, kn, vn, np.array(n), np.array(c), tables, 1 / math.sqrt(d),
+                   host=mode != "device-lengths", queue=mode.endswith("counters"))
     ref, ref_pool = oracle_lib.prefill(pool, 16, d, 0, q, kn, vn, cu, c, tables, 1 / math.sqrt(d),
                                        pool_out=True)
     assert_attn_close(out, ref, "prefill D=%d G=%d" % (d, hq // hkv))
@@ -137,19 +143,22 @@ def test_prefill_host_lengths_same_result(kv):
     pool, tables, q, kn, vn = _case(rng, n, c, hq, hkv, d)
     cu = np.concatenate([[0], np.cumsum(n)]).astype(np.int32)
     outs = []
-    for lens_host in (None, np.stack([n, c], 1)):
+    ws = torch.empty(kv.PREFILL_WORKSPACE_BYTES, dtype=torch.uint8, device="cuda")
+    for lens_host, w in ((None, None), (np.stack([n, c], 1), None), (np.stack([n, c], 1), ws)):
         dp = DevicePool(kv, pool, d)
         out = torch.empty((q.shape[0], hq, d), dtype=torch.bfloat16, device="cuda")
         kv.paged_attn_prefill(dp.pool, 0, bf16_dev(q), i32_dev(cu), i32_dev(c), int(n.max()),
                               i32_dev(tables), 0.0884, out, bf16_dev(kn), bf16_dev(vn),
-                              lens_host=lens_host)
+                              lens_host=lens_host, workspace=w)
         outs.append(out)
     assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16))
+    assert torch.equal(outs[0].view(torch.int16), outs[2].view(torch.int16))
     assert kv.ls_device_errors() == 0
 
 
+@pytest.mark.parametrize("queue", [False, True], ids=["fixed", "counters"])
 @pytest.mark.parametrize("S", [64, 65])
-def test_prefill_host_plan_capacity(kv, oracle_lib, S):
+def test_prefill_host_plan_capacity(kv, oracle_lib, S, queue):
     """Host lengths with 4 KV heads: 64 sessions (256 session/KV-head pairs) fill
     the host-dealt schedule; 65 sessions (260 pairs) exceed it and the kernel
     deals the schedule itself.  Empty turns mixed in."""
@@ -161,7 +170,7 @@ def test_prefill_host_plan_capacity(kv, oracle_lib, S):
     c = rng.integers(0, 200, size=S)
     pool, tables, q, kn, vn = _case(rng, n, c, hq, hkv, d)
     dp = DevicePool(kv, pool, d)
-    out, cu = _run(kv, dp, q, kn, vn, n, c, tables, 0.125, host=True)
+    out, cu = _run(kv, dp, q, kn, vn, n, c, tables, 0.125, host=True, queue=queue)
     ref = oracle_lib.prefill(pool, 16, d, 0, q, kn, vn, cu, c, tables, 0.125)
     assert_attn_close(out, ref, "prefill, %d sessions x %d KV heads, host lengths" % (S, hkv))
     assert kv.ls_device_errors() == 0
@@ -252,7 +261,43 @@ def test_next_turn_prefill_full_sampled(kv, oracle_lib):
     assert kv.ls_device_errors() == 0
     # The timed form of the call (host lengths: schedule dealt on the host)
     # computes every row with the same arithmetic: all rows, same bits.
-    out_h, _ = _run(kv, dp, case.q, case.k_new, case.v_new, n, case.reused_lens, case.block_tables,
-                    case.scale, host=True)
-    assert torch.equal(out_h.view(torch.int16), out.view(torch.int16))
+    for queue in (False, True):
+        out_h, _ = _run(kv, dp, case.q, case.k_new, case.v_new, n, case.reused_lens, case.block_tables,
+                        case.scale, host=True, queue=queue)
+        assert torch.equal(out_h.view(torch.int16), out.view(torch.int16)), "counters=%s" % queue
+    assert kv.ls_device_errors() == 0
+
+
+def test_prefill_with_counters_captured_and_replayed(kv, oracle_lib):
+    """The call with host lengths and the counter workspace (a clearing kernel,
+    then the prefill) captured in a graph: every replay, with eager calls
+    between them, gives the eager result bit for bit."""
+    rng = np.random.default_rng(77)
+    d, hq, hkv = 128, 32, 4
+    n, c = np.array([300, 45, 129, 1, 200]), np.array([1200, 0, 400, 31, 900])
+    pool, tables, q, kn, vn = _case(rng, n, c, hq, hkv, d)
+    dp = DevicePool(kv, pool, d)
+    cu = np.concatenate([[0], np.cumsum(n)]).astype(np.int32)
+    args = [bf16_dev(q), i32_dev(cu), i32_dev(c), int(n.max()), i32_dev(tables), 0.0884]
+    kn_d, vn_d = bf16_dev(kn), bf16_dev(vn)
+    lens_host = np.stack([n, c], 1)
+    ws = torch.empty(kv.PREFILL_WORKSPACE_BYTES, dtype=torch.uint8, device="cuda")
+    eager = torch.empty((q.shape[0], hq, d), dtype=torch.bfloat16, device="cuda")
+    kv.paged_attn_prefill(dp.pool, 0, *args, eager, kn_d, vn_d, lens_host=lens_host, workspace=ws)
+    out = torch.empty_like(eager)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        kv.paged_attn_prefill(dp.pool, 0, *args, out, kn_d, vn_d, lens_host=lens_host, workspace=ws)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        out.fill_(0)
+        ws.fill_(0x77)                        # garbage counters: the replay clears them
+        kv.paged_attn_prefill(dp.pool, 0, *args, eager, kn_d, vn_d, lens_host=lens_host)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int16), eager.view(torch.int16)), "replay %d" % rep
+    ref = oracle_lib.prefill(pool, 16, d, 0, q, kn, vn, cu, c, tables, 0.0884)
+    assert_attn_close(out, ref, "prefill replayed from a graph")
     assert kv.ls_device_errors() == 0
