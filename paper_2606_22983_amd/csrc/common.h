@@ -56,6 +56,10 @@ struct DecodePlan {
 DecodePlan plan_decode(const PoolGeom &p, int32_t num_sessions, int32_t num_q_heads,
                        int32_t max_blocks_per_session);
 
+// Zeroes n (<= 64) 32-bit counters on the stream with a one-wave kernel (not
+// a memset, so that the call can be captured in a graph).
+hipError_t launch_clear_counters(uint32_t *counters, int n, hipStream_t stream);
+
 // Kernel launchers (each returns the hipError_t of its launch).
 // Copies the slabs of layers [layer_begin, layer_begin + layer_count) of blocks
 // ids[0..n): staging block i holds stage_block_slabs slabs, layer_begin's is

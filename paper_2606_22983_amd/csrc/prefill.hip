@@ -858,10 +858,13 @@ bool plan_prefill_host(int32_t S, int32_t hkv, int32_t qtok, const int32_t *lens
 
 }  // namespace
 
-// Zeroes the per-XCD item counters of a call (a kernel rather than a memset,
-// so that the call can be captured in a graph).
-__global__ void clear_queue_kernel(uint32_t *queue) {
-    if (threadIdx.x < kXcds) queue[threadIdx.x] = 0u;
+__global__ void clear_counters_kernel(uint32_t *counters, int n) {
+    if ((int)threadIdx.x < n) counters[threadIdx.x] = 0u;
+}
+
+hipError_t launch_clear_counters(uint32_t *counters, int n, hipStream_t stream) {
+    hipLaunchKernelGGL(clear_counters_kernel, dim3(1), dim3(kWave), 0, stream, counters, n);
+    return hipGetLastError();
 }
 
 hipError_t launch_prefill(const PoolGeom &p, int layer, int32_t num_sessions, int32_t num_q_heads,
@@ -896,7 +899,7 @@ hipError_t launch_prefill(const PoolGeom &p, int layer, int32_t num_sessions, in
         if (queue) {
             // Items are taken through the counters; ~10% more workgroups than
             // items let the faster XCDs take over the slower ones' last items.
-            hipLaunchKernelGGL(clear_queue_kernel, dim3(1), dim3(kWave), 0, stream, queue);
+            if (hipError_t e = launch_clear_counters(queue, kXcds, stream)) return e;
             a.queue = queue;
             int64_t items = 0;
             for (int x = 0; x < kXcds; ++x) items += plan.total[x];
