@@ -29,8 +29,8 @@
  *     ls_device_errors() returns.  A result computed with such an id is not
  *     meaningful.
  *   - Concurrency: calls on different streams may run concurrently only on
- *     disjoint sets of blocks and with their own scratch buffers (a decode
- *     workspace, a copy's staging ring); ordering between streams is the
+ *     disjoint sets of blocks and with their own scratch buffers (a decode or
+ *     prefill workspace, a copy's staging ring); ordering between streams is the
  *     caller's (events).  Blocks being restored must not be read by attention
  *     until the restore's stream has been waited on — the same rule the
  *     paper's KV manager follows before reusing preloaded KV (§5.2).

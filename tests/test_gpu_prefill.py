@@ -268,6 +268,22 @@ def test_next_turn_prefill_full_sampled(kv, oracle_lib):
     assert kv.ls_device_errors() == 0
 
 
+@pytest.mark.parametrize("n,c", [(1, 0), (700, 1500)])
+def test_prefill_counters_single_pair(kv, oracle_lib, n, c):
+    """One session and one KV head: the host deals every query tile to one XCD,
+    so with the item counters the other XCDs' workgroups take all their tiles
+    from that list (or, for a single tile, find nothing and end)."""
+    rng = np.random.default_rng(300 + n)
+    d, hq, hkv = 128, 8, 1
+    pool, tables, q, kn, vn = _case(rng, [n], [c], hq, hkv, d)
+    dp = DevicePool(kv, pool, d)
+    out, cu = _run(kv, dp, q, kn, vn, np.array([n]), np.array([c]), tables, 1 / math.sqrt(d), host=True,
+                   queue=True)
+    ref = oracle_lib.prefill(pool, 16, d, 0, q, kn, vn, cu, np.array([c]), tables, 1 / math.sqrt(d))
+    assert_attn_close(out, ref, "prefill, one pair, %d new tokens, counters" % n)
+    assert kv.ls_device_errors() == 0
+
+
 def test_prefill_with_counters_captured_and_replayed(kv, oracle_lib):
     """The call with host lengths and the counter workspace (a clearing kernel,
     then the prefill) captured in a graph: every replay, with eager calls
