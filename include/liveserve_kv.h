@@ -268,9 +268,10 @@ ls_status paged_attn_prefill(ls_kv_pool *pool, int32_t layer, int32_t num_sessio
  *                   decode (§5.2: preloads must not interfere with live requests; the
  *                   KV manager's admission divides bytes by such a rate).  It runs one
  *                   workgroup per CU, small enough to share the CU with a decode
- *                   workgroup, each copying a burst of four slabs per window of the
- *                   GPU's constant-frequency clock (at the window's start, then it
- *                   sleeps).  A rate above what that grid moves gives its maximum.
+ *                   workgroup, each copying a burst of up to 32 slabs per window of
+ *                   the GPU's constant-frequency clock (at the window's start, then
+ *                   it sleeps; windows of about a millisecond, longer at rates too
+ *                   low for one slab per workgroup in a millisecond).  A rate above what that grid moves gives its maximum.
  *                   LS_EINVAL for a negative or NaN rate.
  * Bit-exact byte copies.  n == 0 is a no-op.
  */

@@ -23,14 +23,19 @@ constexpr int kGatherWorkgroupsPerCu = 6;
 // A rate-bounded copy (a background preload beside live decode) runs one
 // workgroup per CU: with four waves (one per SIMD, 80 registers each) it fits
 // beside a decode workgroup (two waves per SIMD of 208 registers), whereas the
-// full-rate grid holds four or six workgroups per CU and keeps decode off the CU
-// until it ends.  Each workgroup copies a burst of slabs at the start of each
-// window of the GPU's constant-frequency wall clock (the same boundaries for
-// all), then sleeps until the next window.  Measured beside the thinker decode
-// at 0.5 TB/s (read + write): a steady trickle from single waves slowed the
-// decode by ~28%, one slab per window by 10.4%, four by 7.3%.
+// full-rate grid holds four or six workgroups per CU and keeps decode off the
+// CU until it ends.  Each workgroup copies a burst of slabs at the start of
+// each window of the GPU's constant-frequency wall clock (the same boundaries
+// for all), then sleeps until the next window.  Beside the thinker decode,
+// copying at 0.5-0.6 TB/s (read + write): a steady trickle from single waves,
+// or bursts staggered over the window, slowed the decode by ~28%; bursts of
+// 4, 8, 16 and 32 slabs by 9-11%, 9-10%, 9-9.5% and 7-9%.  Longer, rarer
+// bursts disturb fewer decode steps: a burst is up to 32 slabs, as many as
+// keep the window within about a millisecond (so that a small copy at a low
+// rate does not wait long for its first window), and at least one.
 constexpr int kPacedWorkgroupsPerCu = 1;
-constexpr int kPacedSlabsPerWindow = 4;
+constexpr int kPacedMaxBurst = 32;
+constexpr double kPacedWindowSeconds = 1e-3;
 
 // Persistent copy: workgroup w copies the (block i, layer) slabs
 // unit = w, w + grid, ... (unit = i * layer_count + (layer - layer_begin)) of
@@ -45,7 +50,7 @@ constexpr int kPacedSlabsPerWindow = 4;
 // to_pool: staging -> pool (restore); otherwise pool -> staging (stash).
 // ticks_per_unit > 0 (paced copies): a workgroup starts its slabs at the
 // boundaries of the global clock windows of ticks_per_unit ticks, at most
-// kPacedSlabsPerWindow per window (a workgroup that falls behind waits for the
+// `burst` slabs per window (a workgroup that falls behind waits for the
 // next boundary instead of catching up).  The first burst waits at least one whole window,
 // so that a copy of any size stays within its rate.  Every wait ends: the
 // clock only moves forward.
@@ -54,7 +59,7 @@ __global__ __launch_bounds__(kThreads) void block_copy_kernel(
     uint8_t *__restrict__ pool, const int32_t *__restrict__ ids, uint8_t *__restrict__ staging,
     int64_t num_blocks, int32_t layer_begin, int32_t layer_count, int32_t stage_block_slabs,
     int32_t stage_layer0, int64_t slab_bytes, int64_t units, int32_t to_pool, unsigned int *err,
-    uint64_t ticks_per_unit) {
+    uint64_t ticks_per_unit, int32_t burst_slabs) {
     const int64_t chunks = slab_bytes / 16;
     uint64_t next = 0;
     int burst = 0;
@@ -72,7 +77,7 @@ __global__ __launch_bounds__(kThreads) void block_copy_kernel(
                 else __builtin_amdgcn_s_sleep(2);
                 now = __builtin_amdgcn_s_memrealtime();
             }
-            if (++burst == kPacedSlabsPerWindow) {
+            if (++burst == burst_slabs) {
                 burst = 0;
                 next += ticks_per_unit;
                 if ((int64_t)(now - next) >= 0) next = (now / ticks_per_unit + 1) * ticks_per_unit;
@@ -120,16 +125,21 @@ hipError_t launch_block_copy(const PoolGeom &p, int32_t n, const int32_t *ids, u
         max_gbps > 0.0 ? kPacedWorkgroupsPerCu : (to_pool ? kCopyWorkgroupsPerCu : kGatherWorkgroupsPerCu);
     const int64_t grid = std::min<int64_t>(units, per_cu * stream_cus(p, stream));
     uint64_t ticks = 0;
+    int32_t burst = 1;
     if (max_gbps > 0.0) {
-        // grid slabs per window: the window lasts slab * grid / rate (the wall
-        // clock ticks wall_khz thousand times a second).
+        // burst * grid slabs per window: the window lasts slab * burst * grid /
+        // rate (the wall clock ticks wall_khz thousand times a second).
+        const double per_burst = (double)slab * (double)grid;
+        burst = (int32_t)std::min<double>(kPacedMaxBurst,
+                                          std::max(1.0, std::floor(max_gbps * 1e9 * kPacedWindowSeconds / per_burst)));
         const double khz = p.wall_khz > 0 ? (double)p.wall_khz : 100000.0;
-        const double secs = (double)slab * kPacedSlabsPerWindow * (double)grid / (max_gbps * 1e9);
+        const double secs = per_burst * burst / (max_gbps * 1e9);
         ticks = std::max<uint64_t>(1, (uint64_t)(secs * khz * 1e3));
     }
     hipLaunchKernelGGL(block_copy_kernel<kCopyThreads>, dim3((unsigned)grid), dim3(kCopyThreads), 0, stream,
                        reinterpret_cast<uint8_t *>(p.base), ids, staging, p.num_blocks, layer_begin,
-                       layer_count, stage_block_slabs, stage_layer0, slab, units, to_pool ? 1 : 0, err, ticks);
+                       layer_count, stage_block_slabs, stage_layer0, slab, units, to_pool ? 1 : 0, err, ticks,
+                       burst);
     return hipGetLastError();
 }
 
