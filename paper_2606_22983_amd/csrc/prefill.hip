@@ -45,7 +45,9 @@
 //
 // Scheduling: all query tiles of one (session, KV head) pair run on one XCD,
 // so they stream the same keys through its L2; pairs are dealt to XCDs
-// longest first (see the schedule in prefill_kernel).
+// longest first, by the kernel or, given the lengths on the host, by the host
+// (see the schedule in prefill_kernel).  With a counter workspace, XCDs that
+// run faster take over the slower ones' last tiles.
 #include <algorithm>
 #include <type_traits>
 
