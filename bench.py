@@ -54,7 +54,7 @@ def parse():
     ap.add_argument("--host-leg-gib", type=float, default=4.0)
     ap.add_argument("--restore-cus", type=int, default=32)
     ap.add_argument("--rates", type=lambda v: [float(x) for x in v.split(",")],
-                    default=[50.0, 100.0, 200.0, 250.0, 300.0, 400.0, 800.0, 0.0],
+                    default=[50.0, 100.0, 200.0, 250.0, 275.0, 300.0, 400.0, 800.0, 0.0],
                     help="payload GB/s caps of the bounded-restore curve (0 = full rate)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     return ap.parse_args()
