@@ -366,3 +366,20 @@ def test_schedule_rejects_bad_host_lengths(lib):
     assert _sched(lib, 2, 16, [5, 0, 7], 10)[0] == LS_EINVAL          # an empty context
     assert _sched(lib, 2, 16, [5, 0, 7], 10, appended=1)[0] == LS_OK
     assert _sched(lib, 2, 16, [5, 161, 7], 10)[0] == LS_EINVAL        # past a 10-block table
+
+
+def test_binding_constants_match_the_header(built_lib, binding):
+    """The binding's copies of the header's constants (error codes, device error
+    bits, the prefill workspace size) agree with the header."""
+    kv = binding
+    text = open(HEADER).read()
+
+    def define(name):
+        m = re.search(r"#define\s+%s\s+\(?\s*(?:\(size_t\))?\s*(0x[0-9a-fA-F]+|-?\d+)u?\s*\)?" % name, text)
+        assert m, name
+        return int(m.group(1), 0)
+
+    assert kv.PREFILL_WORKSPACE_BYTES == define("LS_PREFILL_WORKSPACE_BYTES")
+    assert kv.LS_DEVERR_BLOCK_ID == define("LS_DEVERR_BLOCK_ID")
+    assert kv.LS_DEVERR_LENGTH == define("LS_DEVERR_LENGTH")
+    assert kv.LS_DEVERR_INTERNAL == define("LS_DEVERR_INTERNAL")
