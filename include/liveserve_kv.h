@@ -146,7 +146,8 @@ size_t ls_decode_workspace_bytes(const ls_kv_pool *pool, int32_t num_sessions,
  *                  head h using KV head h / (num_q_heads / num_kv_heads)
  *   workspace      device, >= ls_decode_workspace_bytes(...) bytes
  *
- * Supported: num_q_heads / num_kv_heads in {1, 2, 4, 8}.  Errors: LS_EINVAL
+ * Supported: num_q_heads / num_kv_heads in {1, 2, 4, 8}; at most 2048 sessions
+ * and 16384 blocks (262,144 tokens) per session.  Errors: LS_EINVAL
  * (NULL pointer, layer out of range, num_q_heads not a multiple of num_kv_heads,
  * only one of k_new / v_new, a bad host length), LS_ENOMEM (workspace too
  * small), LS_EUNSUPPORTED (group size, batch limits), LS_EHIP (launch failure).

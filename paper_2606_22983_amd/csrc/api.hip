@@ -351,7 +351,7 @@ ls_status paged_attn_decode(ls_kv_pool *pool, int32_t layer, int32_t num_session
     const DecodePlan plan = plan_decode(p, num_sessions, num_q_heads, max_blocks_per_session);
     if (!plan.supported)
         return fail(LS_EUNSUPPORTED, "batch of %d sessions with %d blocks each exceeds the decode "
-                    "limits (2048 sessions, 131072 tokens)", num_sessions, max_blocks_per_session);
+                    "limits (2048 sessions, 16384 blocks per session)", num_sessions, max_blocks_per_session);
     if (workspace_bytes < plan.total())
         return fail(LS_ENOMEM, "workspace_bytes (%zu) < required (%zu)", workspace_bytes, plan.total());
     unsigned int *err = device_error_word();

@@ -120,6 +120,9 @@ def _decode(lib, pool, **kw):
     (dict(scale=0.0), LS_EINVAL),
     (dict(scale=float("nan")), LS_EINVAL),
     (dict(wsb=16), LS_ENOMEM),
+    # past the batch limits: 2049 sessions, 16385 blocks per session
+    (dict(S=2049), LS_EUNSUPPORTED),
+    (dict(maxb=16385), LS_EUNSUPPORTED),
     # host lengths: an empty context, a negative one, keys past the 8-block table
     (dict(lens_host=[5, 0, 7, 9]), LS_EINVAL),
     (dict(lens_host=[5, -1, 7, 9], kn=F, vn=F), LS_EINVAL),
@@ -383,3 +386,14 @@ def test_binding_constants_match_the_header(built_lib, binding):
     assert kv.LS_DEVERR_BLOCK_ID == define("LS_DEVERR_BLOCK_ID")
     assert kv.LS_DEVERR_LENGTH == define("LS_DEVERR_LENGTH")
     assert kv.LS_DEVERR_INTERNAL == define("LS_DEVERR_INTERNAL")
+
+
+def test_schedule_at_the_batch_limits(lib):
+    """2048 sessions and 16384-block tables are accepted; one more of either is
+    not.  A 262,144-token session is planned on the host, split into 1024-token
+    multiples of at least 2048 tokens, with the merge."""
+    assert _sched(lib, 2, 8, [1] * 2048, 16384, host=False)[0] == LS_OK
+    assert _sched(lib, 2, 8, [1] * 2049, 8, host=False)[0] == LS_EUNSUPPORTED
+    assert _sched(lib, 2, 8, [1] * 4, 16385, host=False)[0] == LS_EUNSUPPORTED
+    r, split, host, merge = _sched(lib, 1, 8, [262143, 261444, 9000], 16384, appended=1)
+    assert r == LS_OK and host and merge and split % 1024 == 0 and split >= 2048

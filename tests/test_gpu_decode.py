@@ -101,6 +101,41 @@ def test_decode_batch_sizes_and_equal_short_splits(kv, oracle_lib, num_sessions)
     assert kv.ls_device_errors() == 0
 
 
+@pytest.mark.parametrize("limit", ["sessions", "tokens"])
+def test_decode_at_the_size_limits(kv, oracle_lib, limit):
+    """The largest batch a call takes (2048 sessions) and the longest context
+    (16384 blocks, 262,144 keys: 256 splits of 1024 tokens, the merge kernel's
+    full capacity), with device lengths and with host lengths; appended rows at
+    the table's last slot included."""
+    rng = np.random.default_rng(2048 if limit == "sessions" else 262144)
+    if limit == "sessions":
+        lens = rng.integers(1, 400, size=2048)
+        lens[[0, 700, 2047]] = [5000, 4096, 1]
+        hq, hkv, append = 8, 2, False
+    else:
+        lens = np.array([262144 - 1, 262144 - 700, 9000])
+        hq, hkv, append = 8, 1, True
+    pool, tables, q, kn, vn = _synthetic(rng, lens, hq, hkv, 64, append)
+    if limit == "tokens":
+        assert tables.shape[1] == 16384
+    S = len(lens)
+    dp = DevicePool(kv, pool, 64)
+    ref, ref_pool = oracle_lib.decode(pool, 16, 64, 0, q, tables, lens, 0.125, k_new=kn, v_new=vn,
+                                      pool_out=True)
+    for host in (False, True):
+        dp.data.copy_(bf16_dev(pool))
+        ws = torch.zeros(kv.decode_workspace_bytes(dp.pool, S, hq, tables.shape[1]), dtype=torch.uint8,
+                         device="cuda")
+        out = torch.empty((S, hq, 64), dtype=torch.bfloat16, device="cuda")
+        kv.paged_attn_decode(dp.pool, 0, bf16_dev(q), i32_dev(tables), i32_dev(lens), 0.125, out, ws,
+                             None if kn is None else bf16_dev(kn), None if vn is None else bf16_dev(vn),
+                             context_lens_host=lens if host else None)
+        assert_attn_close(out, ref, "decode at the %s limit, host lengths %s" % (limit, host))
+        if append:
+            assert np.array_equal(dp.host(), ref_pool), "appended pool differs from the oracle's"
+        assert kv.ls_device_errors() == 0
+
+
 @pytest.mark.parametrize("shape", ["rising", "spike", "falling"])
 def test_decode_peaky_scores(kv, oracle_lib, shape):
     """Large, uneven scores (key norms rising along the context, one late block of
