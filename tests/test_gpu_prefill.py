@@ -219,6 +219,26 @@ def test_prefill_peaky_scores(kv, oracle_lib, shape, d, hq, hkv):
     assert kv.ls_device_errors() == 0
 
 
+@pytest.mark.parametrize("mode", ["device-lengths", "host-lengths-counters"])
+def test_prefill_over_a_262144_token_context(kv, oracle_lib, mode):
+    """A turn over the longest context a decode call takes (16384 blocks):
+    4096 key tiles per query tile, fp32 row sums over 262,144 keys; a second
+    session with an empty context beside it."""
+    rng = np.random.default_rng(16384)
+    d, hq, hkv = 64, 2, 1
+    n = np.array([16, 300])
+    c = np.array([262144 - 16, 0])
+    pool, tables, q, kn, vn = _case(rng, n, c, hq, hkv, d)
+    assert tables.shape[1] == 16384
+    dp = DevicePool(kv, pool, d)
+    out, cu = _run(kv, dp, q, kn, vn, n, c, tables, 0.125, host=mode != "device-lengths",
+                   queue=mode.endswith("counters"))
+    ref, ref_pool = oracle_lib.prefill(pool, 16, d, 0, q, kn, vn, cu, c, tables, 0.125, pool_out=True)
+    assert_attn_close(out, ref, "prefill over 262,144 keys, %s" % mode)
+    assert np.array_equal(dp.host(), ref_pool), "appended pool differs from the oracle's"
+    assert kv.ls_device_errors() == 0
+
+
 def test_prefill_chunked_equals_whole_turn(kv):
     """Two chunks (c advanced by the first) give the same rows as one call."""
     rng = np.random.default_rng(12)
