@@ -207,17 +207,20 @@ __device__ __forceinline__ void stage_barrier() {
 }
 
 // Scheduling constraint for one phase of N MFMAs: MFMA i is followed by one
-// LDS read (even i, while reads remain) and its share of the phase's
-// transcendental and other VALU instructions.
+// LDS read (even i, while reads remain), its share of the phase's plain VALU
+// instructions, then its share of the transcendental ones.  With the plain
+// ones first, the conversion of a pair of exp results issues after the next
+// MFMA instead of right behind the second exp, where it would need a wait
+// state (1.3% faster on the next-turn workload).
 template <int I, int N, int Reads, int Trans, int Valu>
 __device__ __forceinline__ void order_phase() {
     if constexpr (I < N) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         if constexpr (I % 2 == 0 && I / 2 < Reads) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         constexpr int t = (I + 1) * Trans / N - I * Trans / N;
-        if constexpr (t > 0) __builtin_amdgcn_sched_group_barrier(0x400, t, 0);
         constexpr int v = (I + 1) * Valu / N - I * Valu / N;
         if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x002, v, 0);
+        if constexpr (t > 0) __builtin_amdgcn_sched_group_barrier(0x400, t, 0);
         order_phase<I + 1, N, Reads, Trans, Valu>();
     }
 }
