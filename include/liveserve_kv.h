@@ -163,8 +163,10 @@ ls_status paged_attn_decode(ls_kv_pool *pool, int32_t layer, int32_t num_session
  * ls_decode_schedule — how paged_attn_decode will run a batch of this shape
  * on `stream`: *split_tokens tokens per split, *host_planned 1 when the
  * schedule is planned on the host from context_lens_host (0: in the kernel,
- * also when the host plan is estimated to be no faster or does not fit the
- * argument block), *merge 1 when the split merge kernel runs.  appended: 1
+ * also when the host plan is estimated to be no faster or has more items than
+ * the kernel arguments carry: 7680 for batches of at most 1024 sessions, 4 KV
+ * heads and 8 splits per session, else 3840), *merge 1 when the split merge
+ * kernel runs.  appended: 1
  * when k_new / v_new will be given.  Pure host computation; LS_EINVAL as for
  * paged_attn_decode.
  */

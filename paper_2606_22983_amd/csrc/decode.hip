@@ -37,6 +37,7 @@
 // tile built from k_new / v_new, and then writes it to the slot for the next
 // steps.
 #include <algorithm>
+#include <cstring>
 #include <cstdlib>
 #include <type_traits>
 #include <vector>
@@ -100,22 +101,30 @@ struct DecodeArgs {
 // session" 31), or, when start[kPlanMaxWg + 1] is 1, 16-bit halves of them
 // (session 0..9, KV head 10..11, split 12..14, last split 15), which holds
 // twice as many items for batches of at most 1024 sessions, 4 KV heads and 8
-// splits per session.
+// splits per session.  Plans that fit go in a ~3 KiB argument block; larger
+// batches take a ~16 KiB one (the runtime passes kernel arguments of that
+// size intact), so the common launch copies no more than it needs.
 constexpr int kPlanMaxWg = 256;
-constexpr int kPlanMaxItems = 640;                     // 32-bit items (1280 16-bit ones)
-struct DecodeHostPlan {
+constexpr int kPlanItemsSmall = 640;                   // 32-bit words: 640 or 1280 items
+constexpr int kPlanItemsLarge = 3840;                  // 32-bit words: 3840 or 7680 items
+template <int kItems>
+struct DecodeHostPlanT {
     uint16_t start[kPlanMaxWg + 2];            // [kPlanMaxWg + 1]: 1 = 16-bit items
-    uint32_t item[kPlanMaxItems];
+    uint32_t item[kItems];
 };
+using DecodeHostPlan = DecodeHostPlanT<kPlanItemsSmall>;
+using DecodeHostPlanLarge = DecodeHostPlanT<kPlanItemsLarge>;
 struct NoPlan {
     int32_t unused;
 };
-template <bool kHost>
-using PlanArg = typename std::conditional<kHost, DecodeHostPlan, NoPlan>::type;
-__device__ __forceinline__ uint32_t plan_start(const DecodeHostPlan &p, int w) { return p.start[w]; }
+template <bool kHost, int kItems>
+using PlanArg = typename std::conditional<kHost, DecodeHostPlanT<kItems>, NoPlan>::type;
+template <int kItems>
+__device__ __forceinline__ uint32_t plan_start(const DecodeHostPlanT<kItems> &p, int w) { return p.start[w]; }
 __device__ __forceinline__ uint32_t plan_start(const NoPlan &, int) { return 0; }
 // Item i in the 32-bit layout.
-__device__ __forceinline__ uint32_t plan_item(const DecodeHostPlan &p, int i) {
+template <int kItems>
+__device__ __forceinline__ uint32_t plan_item(const DecodeHostPlanT<kItems> &p, int i) {
     if (p.start[kPlanMaxWg + 1] == 0) return p.item[i];
     const uint32_t h = (p.item[i >> 1] >> ((i & 1) * 16)) & 0xFFFFu;
     return (h & 0x3FFu) | (((h >> 10) & 3u) << 12) | (((h >> 12) & 7u) << 20) | ((h >> 15) << 31);
@@ -268,8 +277,8 @@ __device__ __forceinline__ unsigned block_exclusive_scan(unsigned v, unsigned *s
 //
 // Either way each workgroup fetches the next chunk's block ids while it works
 // on the current one, and requests its first blocks before merging.
-template <int D, int kDepth, int kMaxPerWave, bool kHost>
-__global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a, PlanArg<kHost> plan) {
+template <int D, int kDepth, int kMaxPerWave, bool kHost, int kItems = kPlanItemsSmall>
+__global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a, PlanArg<kHost, kItems> plan) {
     constexpr int kChunk = kMaxPerWave * kDecWaves * kBlock;   // tokens per chunk
     __shared__ int sm_cum[kMaxBatch + 1];       // first full-split row of each session
     __shared__ int sm_len[kMaxBatch];           // attended length of each session
@@ -840,7 +849,7 @@ struct PlanRow {
 };
 
 bool plan_decode_host(int S, int num_kv_heads, const int32_t *lens_host, int appended, int W, int t_min,
-                      int t_dev, bool dev_merges, DecodeHostPlan &plan, int &t_out, bool &any_split) {
+                      int t_dev, bool dev_merges, DecodeHostPlanLarge &plan, int &t_out, bool &any_split) {
     if (W < 1 || W > kPlanMaxWg || S > 4096 || num_kv_heads > 255) return false;
     int64_t max_len = 1;
     for (int s = 0; s < S; ++s) max_len = std::max<int64_t>(max_len, (int64_t)lens_host[s] + appended);
@@ -880,7 +889,7 @@ bool plan_decode_host(int S, int num_kv_heads, const int32_t *lens_host, int app
         rows.clear();
         const int64_t ns_max = (max_len + T - 1) / T;
         compact = S <= 1024 && num_kv_heads <= 4 && ns_max <= 8;
-        const int64_t cap = compact ? 2 * kPlanMaxItems : kPlanMaxItems;
+        const int64_t cap = compact ? 2 * kPlanItemsLarge : kPlanItemsLarge;
         if (ns_max > 2047) return false;
         int64_t n_items = 0;
         for (int s = 0; s < S; ++s) {
@@ -984,11 +993,13 @@ bool plan_decode_host(int S, int num_kv_heads, const int32_t *lens_host, int app
 // neither the items nor, noticeably, their balance.
 struct CachedPlan {
     bool used = false, host = false, split = false;
+    bool large = false;                        // the plan needs the large argument block
     int S = 0, hkv = 0, appended = 0, W = 0, t_min = 0, t_dev = 0, T = 0;
     bool dev_merges = false;
     int64_t tokens = 0;
     std::vector<uint16_t> nsplits;
-    DecodeHostPlan plan;
+    DecodeHostPlanLarge plan;
+    DecodeHostPlan small;                      // the same plan, when it fits
 };
 
 const CachedPlan *cached_decode_plan(int S, int hkv, const int32_t *lens_host, int appended, int W, int t_min,
@@ -1022,6 +1033,15 @@ const CachedPlan *cached_decode_plan(int S, int hkv, const int32_t *lens_host, i
     c.dev_merges = dev_merges;
     c.tokens = tokens;
     c.host = plan_decode_host(S, hkv, lens_host, appended, W, t_min, t_dev, dev_merges, c.plan, c.T, c.split);
+    if (c.host) {
+        const int items = c.plan.start[W];
+        const int words = c.plan.start[kPlanMaxWg + 1] ? (items + 1) / 2 : items;
+        c.large = words > kPlanItemsSmall;
+        if (!c.large) {
+            std::memcpy(c.small.start, c.plan.start, sizeof c.small.start);
+            std::memcpy(c.small.item, c.plan.item, sizeof(uint32_t) * (size_t)words);
+        }
+    }
     const int T = c.host ? c.T : t_dev;
     c.nsplits.resize(S);
     for (int s = 0; s < S; ++s) {
@@ -1080,14 +1100,21 @@ hipError_t launch_decode(const PoolGeom &p, int layer, int32_t num_sessions, int
                                                  (int)resident, std::max(plan.split_tokens, 1024),
                                                  plan.split_tokens, plan.max_splits > 1);
         if (c->host) {
-            const DecodeHostPlan &hp = c->plan;
             const bool split = c->split;
             a.split_tokens = c->T;
             const dim3 grid((unsigned)resident);
-            if (p.head_dim == 128)
-                hipLaunchKernelGGL((decode_kernel<128, 2, 8, true>), grid, dim3(kDecThreads), 0, stream, a, hp);
-            else
-                hipLaunchKernelGGL((decode_kernel<64, 2, 8, true>), grid, dim3(kDecThreads), 0, stream, a, hp);
+            if (!c->large) {
+                if (p.head_dim == 128)
+                    hipLaunchKernelGGL((decode_kernel<128, 2, 8, true>), grid, dim3(kDecThreads), 0, stream, a, c->small);
+                else
+                    hipLaunchKernelGGL((decode_kernel<64, 2, 8, true>), grid, dim3(kDecThreads), 0, stream, a, c->small);
+            } else if (p.head_dim == 128) {
+                hipLaunchKernelGGL((decode_kernel<128, 2, 8, true, kPlanItemsLarge>), grid, dim3(kDecThreads), 0,
+                                   stream, a, c->plan);
+            } else {
+                hipLaunchKernelGGL((decode_kernel<64, 2, 8, true, kPlanItemsLarge>), grid, dim3(kDecThreads), 0,
+                                   stream, a, c->plan);
+            }
             hipError_t e = hipGetLastError();
             if (e != hipSuccess || !split) return e;
             if (p.head_dim == 128)

@@ -397,3 +397,15 @@ def test_schedule_at_the_batch_limits(lib):
     assert _sched(lib, 2, 8, [1] * 4, 16385, host=False)[0] == LS_EUNSUPPORTED
     r, split, host, merge = _sched(lib, 1, 8, [262143, 261444, 9000], 16384, appended=1)
     assert r == LS_OK and host and merge and split % 1024 == 0 and split >= 2048
+
+
+def test_schedule_large_batches_are_planned_on_host(lib):
+    """Batches beyond the small argument block (1280 items) take the large one:
+    512 sessions x 4 KV heads (2048 items) and 1000 sessions x 4 (4000) are
+    planned on the host; 2048 sessions x 4 KV heads (8192 32-bit items) are
+    more than either holds and run the kernel's own schedule."""
+    assert _sched(lib, 4, 32, [1536] * 512, 96)[:3] == (LS_OK, 2048, True)
+    r, split, host, _ = _sched(lib, 4, 32, [1000 + (7 * s) % 2000 for s in range(1000)], 192)
+    assert r == LS_OK and host
+    r, split, host, _ = _sched(lib, 4, 32, [1536] * 2048, 96)
+    assert r == LS_OK and not host

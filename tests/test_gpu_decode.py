@@ -136,6 +136,31 @@ def test_decode_at_the_size_limits(kv, oracle_lib, limit):
         assert kv.ls_device_errors() == 0
 
 
+@pytest.mark.parametrize("append", [False, True])
+def test_host_planned_batch_beyond_the_small_argument_block(kv, oracle_lib, append):
+    """700 sessions x 2 KV heads with contexts up to 4500 tokens: more items than
+    the small plan block holds (1280), so the plan goes in the large one."""
+    rng = np.random.default_rng(700 + append)
+    lens = rng.integers(1, 4500, size=700)
+    lens[:3] = [1, 2048, 4499]
+    pool, tables, q, kn, vn = _synthetic(rng, lens, 16, 2, 64, append)
+    dp = DevicePool(kv, pool, 64)
+    sc = _host_planned(kv, dp, 700, 16, tables.shape[1], lens, append)
+    assert sc["host_planned"], sc
+    ws = torch.zeros(kv.decode_workspace_bytes(dp.pool, 700, 16, tables.shape[1]), dtype=torch.uint8,
+                     device="cuda")
+    out = torch.empty((700, 16, 64), dtype=torch.bfloat16, device="cuda")
+    kv.paged_attn_decode(dp.pool, 0, bf16_dev(q), i32_dev(tables), i32_dev(lens), 0.125, out, ws,
+                         None if kn is None else bf16_dev(kn), None if vn is None else bf16_dev(vn),
+                         context_lens_host=lens)
+    ref, ref_pool = oracle_lib.decode(pool, 16, 64, 0, q, tables, lens, 0.125, k_new=kn, v_new=vn,
+                                      pool_out=True)
+    assert_attn_close(out, ref, "decode, 700 sessions host-planned in the large block, append=%s" % append)
+    if append:
+        assert np.array_equal(dp.host(), ref_pool)
+    assert kv.ls_device_errors() == 0
+
+
 @pytest.mark.parametrize("shape", ["rising", "spike", "falling"])
 def test_decode_peaky_scores(kv, oracle_lib, shape):
     """Large, uneven scores (key norms rising along the context, one late block of
