@@ -23,6 +23,7 @@ import json
 import math
 import os
 import sys
+import traceback
 import time
 
 import numpy as np
@@ -915,32 +916,47 @@ def main():
     legs = set(args.legs.split(","))
     log("device:", torch.cuda.get_device_name(0), "| library:", kv.version())
 
-    calib = calib_leg(torch, args) if "calib" in legs else None
+    errors = []
+
+    def secondary(name, fn):
+        """A leg beside the headline: a Python-level failure (a sampled check, a
+        missing optional runtime entry) is printed and recorded in the JSON line
+        instead of taking the headline with it."""
+        try:
+            return fn()
+        except Exception as e:                 # noqa: BLE001 - reported, not swallowed
+            traceback.print_exc()
+            errors.append("%s: %s: %s" % (name, type(e).__name__, e))
+            return {"error": "%s: %s" % (type(e).__name__, e)}
+        finally:
+            torch.cuda.empty_cache()
+
+    calib = secondary("calib", lambda: calib_leg(torch, args)) if "calib" in legs else None
     dec = decode_leg(torch, kv, W, args) if legs & {"decode", "overlap"} else None
     extra = {}
     if "prefill" in legs:
-        extra["prefill"] = prefill_leg(torch, kv, W, args)
-        torch.cuda.empty_cache()
+        extra["prefill"] = secondary("prefill", lambda: prefill_leg(torch, kv, W, args))
     if "talker" in legs:
-        extra["talker"] = talker_leg(torch, kv, W, args)
-        torch.cuda.empty_cache()
+        extra["talker"] = secondary("talker", lambda: talker_leg(torch, kv, W, args))
     if "restore" in legs:
-        extra["restore"] = restore_leg(torch, kv, W, args, dec if "overlap" in legs else None)
+        extra["restore"] = secondary("restore", lambda: restore_leg(torch, kv, W, args,
+                                                                    dec if "overlap" in legs else None))
     if "pipeline" in legs:
-        extra["restore_prefill_pipeline"] = pipeline_leg(torch, kv, W, args)
-        torch.cuda.empty_cache()
+        extra["restore_prefill_pipeline"] = secondary("pipeline", lambda: pipeline_leg(torch, kv, W, args))
     if "kvm" in legs:
-        extra["kv_manager"] = kvm_leg(W)
+        extra["kv_manager"] = secondary("kvm", lambda: kvm_leg(W))
     if "sched" in legs:
-        extra["scheduler"] = sched_leg()
+        extra["scheduler"] = secondary("sched", sched_leg)
     if calib:
         extra["calibration_copy"] = calib
+    if errors:
+        extra["leg_errors"] = errors
     if dec is None:                # a partial run (profiling one leg): no headline
         print(json.dumps({"metric": None, "value": None, "legs": extra}), flush=True)
         return
     dec_gbs = dec["alg_bytes"] / (dec["kernel_ms"] * 1e-3) / 1e9
     wall_gbs = dec["alg_bytes"] * args.steps / dec["wall_s"] / 1e9
-    cpu = None if args.no_cpu_baseline else cpu_baseline(dec, W)
+    cpu = None if args.no_cpu_baseline else secondary("cpu_baseline", lambda: cpu_baseline(dec, W))
 
     line = {
         "metric": "paged decode KV GB/s (% HBM peak); prefill TFLOP/s; restore GB/s on 1 MI355X",
