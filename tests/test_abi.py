@@ -336,13 +336,13 @@ def test_schedule_talker_batch_is_planned_on_host_without_merge(lib):
 
 def test_schedule_thinker_batch_splits_long_sessions(lib):
     """The lognormal thinker batch (64 sessions up to 16k keys): 2048-token splits
-    (856 items, in the 16-bit item form) balance better than the device's
-    1024-token snake; the merge runs.  Without host lengths: the device schedule."""
+    (856 items, in the 16-bit item form) with the merge, planned on the host;
+    without host lengths the kernel deals 2048-token splits itself."""
     from paper_2606_22983_amd import workloads as W
     lens = W.thinker_lengths()
     maxb = int(((lens + 15) // 16).max())
     assert _sched(lib, 4, 32, lens, maxb) == (LS_OK, 2048, True, True)
-    assert _sched(lib, 4, 32, lens, maxb, host=False) == (LS_OK, 1024, False, True)
+    assert _sched(lib, 4, 32, lens, maxb, host=False) == (LS_OK, 2048, False, True)
 
 
 def test_schedule_mixed_batch_splits_long_sessions(lib):
