@@ -99,7 +99,7 @@ struct DecodeArgs {
 // passed by value in the kernel arguments: workgroup w runs items
 // start[w] .. start[w + 1] - 1.  Items are 32-bit words (session in bits
 // 0..11, KV head 12..19, split 20..30, "last split the plan gives the
-// session" 31), or, when start[kPlanMaxWg + 1] is 1, 16-bit halves of them
+// session" 31), or, when the start[] entries carry kPlanCompactBit, 16-bit halves of them
 // (session 0..9, KV head 10..11, split 12..14, last split 15), which holds
 // twice as many items for batches of at most 1024 sessions, 4 KV heads and 8
 // splits per session.  Plans that fit go in a ~3 KiB argument block; larger
@@ -108,9 +108,10 @@ struct DecodeArgs {
 constexpr int kPlanMaxWg = 256;
 constexpr int kPlanItemsSmall = 640;                   // 32-bit words: 640 or 1280 items
 constexpr int kPlanItemsLarge = 3840;                  // 32-bit words: 3840 or 7680 items
+constexpr uint32_t kPlanCompactBit = 0x8000u;          // in every start[] entry: 16-bit items
 template <int kItems>
 struct DecodeHostPlanT {
-    uint16_t start[kPlanMaxWg + 2];            // [kPlanMaxWg + 1]: 1 = 16-bit items
+    uint16_t start[kPlanMaxWg + 2];            // | kPlanCompactBit: 16-bit items; [kPlanMaxWg + 1]: unused
     uint32_t item[kItems];
 };
 using DecodeHostPlan = DecodeHostPlanT<kPlanItemsSmall>;
@@ -120,14 +121,32 @@ struct NoPlan {
 };
 template <bool kHost, int kItems>
 using PlanArg = typename std::conditional<kHost, DecodeHostPlanT<kItems>, NoPlan>::type;
+// Items [first, end) of workgroup w and the item width: start[w] and
+// start[w + 1], read as the two aligned 32-bit words from start[w & ~1] on, in
+// one scalar load (those need 4-byte alignment).  Every entry carries the
+// width flag, so no other load is needed before the first item's.
 template <int kItems>
-__device__ __forceinline__ uint32_t plan_start(const DecodeHostPlanT<kItems> &p, int w) { return p.start[w]; }
-__device__ __forceinline__ uint32_t plan_start(const NoPlan &, int) { return 0; }
-// Item i in the 32-bit layout.
+__device__ __forceinline__ void plan_range(const DecodeHostPlanT<kItems> &p, int w, int &first, int &end,
+                                           bool &compact) {
+    uint32_t word[2];
+    __builtin_memcpy(word, &p.start[w & ~1], sizeof word);
+    const uint32_t lo = (w & 1) ? word[0] >> 16 : word[0] & 0xFFFFu;
+    const uint32_t hi = (w & 1) ? word[1] & 0xFFFFu : word[0] >> 16;
+    first = (int)(lo & ~kPlanCompactBit);
+    end = (int)(hi & ~kPlanCompactBit);
+    compact = (lo & kPlanCompactBit) != 0;
+}
+__device__ __forceinline__ void plan_range(const NoPlan &, int, int &first, int &end, bool &compact) {
+    first = end = 0;
+    compact = false;
+}
+// Item i in the 32-bit layout: one load either way (the word index is
+// selected, not branched on).
 template <int kItems>
-__device__ __forceinline__ uint32_t plan_item(const DecodeHostPlanT<kItems> &p, int i) {
-    if (p.start[kPlanMaxWg + 1] == 0) return p.item[i];
-    const uint32_t h = (p.item[i >> 1] >> ((i & 1) * 16)) & 0xFFFFu;
+__device__ __forceinline__ uint32_t plan_item(const DecodeHostPlanT<kItems> &p, int i, bool compact) {
+    const uint32_t word = p.item[compact ? i >> 1 : i];
+    if (!compact) return word;
+    const uint32_t h = (word >> ((i & 1) * 16)) & 0xFFFFu;
     return (h & 0x3FFu) | (((h >> 10) & 3u) << 12) | (((h >> 12) & 7u) << 20) | ((h >> 15) << 31);
 }
 
@@ -308,13 +327,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a, PlanA
         sm_merged[tid] = 0;
     }
     int full_rows = 0, total_rows = 0;
-    if constexpr (kHost) {
-        // The schedule came with the arguments: only the lengths are needed.
-        for (int s = tid; s < S; s += kDecThreads) {
-            sm_len[s] = attended_len(a, s, blockIdx.x == 0);
-            sm_own[s] = a.appended && a.lens[s] >= 0 && a.lens[s] + 1 <= a.max_blocks * kBlock;
-        }
-    } else {
+    if constexpr (!kHost) {
         constexpr int kMaskWords = kDecThreads / 64;
         for (int i = tid; i < kKeyBins * kMaskWords; i += kDecThreads) sm_kmask[i / kMaskWords][i % kMaskWords] = 0ull;
         // ---- work rows: full splits per session (prefix sum) and short splits.
@@ -427,12 +440,14 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a, PlanA
     };
     // This workgroup's k-th item: (session, KV head, split, last split the
     // plan gives the session), or false past its last item.
-    const int host_base = kHost ? (int)plan_start(plan, blockIdx.x) : 0;
-    const int host_count = kHost ? (int)plan_start(plan, blockIdx.x + 1) - host_base : 0;
+    int host_base, host_end;
+    bool host_compact;
+    plan_range(plan, (int)blockIdx.x, host_base, host_end, host_compact);
+    const int host_count = host_end - host_base;
     auto item_at = [&](int k, int &s_out, int &g_out, int &split_out, bool &last_out) -> bool {
         if constexpr (kHost) {
             if (k >= host_count) return false;
-            const uint32_t e = plan_item(plan, host_base + k);
+            const uint32_t e = plan_item(plan, host_base + k, host_compact);
             s_out = (int)(e & 0xFFFu);
             g_out = (int)((e >> 12) & 0xFFu);
             split_out = (int)((e >> 20) & 0x7FFu);
@@ -499,7 +514,16 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeArgs a, PlanA
     bool have = item_at(0, s, g, split, last_planned);
     int ids_pre = have ? fetch_ids(s, split, 0) : -1;
     if (have) load_q(s, g, qop);
-    if constexpr (kHost) __syncthreads();      // the lengths are in LDS
+    if constexpr (kHost) {
+        // The schedule came with the arguments, so only the lengths are needed.
+        // They are loaded after the first item's block ids and q, whose loads
+        // are then already in flight.
+        for (int i = tid; i < S; i += kDecThreads) {
+            sm_len[i] = attended_len(a, i, blockIdx.x == 0);
+            sm_own[i] = a.appended && a.lens[i] >= 0 && a.lens[i] + 1 <= a.max_blocks * kBlock;
+        }
+        __syncthreads();
+    }
     if (have) {
         if (lane < kMaxSplitTokens / kBlock) sm_ids[wave][0][lane] = ids_pre;
         const int nb = chunk_blocks(sm_len[s], split, 0);
@@ -936,8 +960,8 @@ bool plan_decode_host(int S, int num_kv_heads, const int32_t *lens_host, int app
         int count[kPlanMaxWg + 1] = {0};
         for (uint32_t o : order) ++count[(o >> 16) + 1];
         for (int w = 0; w < W; ++w) count[w + 1] += count[w];
-        for (int w = 0; w <= W; ++w) plan.start[w] = (uint16_t)count[w];
-        plan.start[kPlanMaxWg + 1] = compact ? 1 : 0;
+        for (int w = 0; w <= W; ++w) plan.start[w] = (uint16_t)(count[w] | (compact ? kPlanCompactBit : 0u));
+        plan.start[kPlanMaxWg + 1] = 0;
         for (int w = 0; w < W; ++w) slot_of[w] = count[w];
         size_t i = 0;
         for (const PlanRow &r : rows) {
@@ -1044,8 +1068,8 @@ const CachedPlan *cached_decode_plan(int S, int hkv, const int32_t *lens_host, i
     c.tokens = tokens;
     c.host = plan_decode_host(S, hkv, lens_host, appended, W, t_min, t_dev, dev_merges, c.plan, c.T, c.split);
     if (c.host) {
-        const int items = c.plan.start[W];
-        const int words = c.plan.start[kPlanMaxWg + 1] ? (items + 1) / 2 : items;
+        const int items = c.plan.start[W] & ~kPlanCompactBit;
+        const int words = (c.plan.start[W] & kPlanCompactBit) ? (items + 1) / 2 : items;
         c.large = words > kPlanItemsSmall;
         if (!c.large) {
             std::memcpy(c.small.start, c.plan.start, sizeof c.small.start);
