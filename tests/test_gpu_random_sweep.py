@@ -1,7 +1,7 @@
 """Seeded random sweep of the three entry points against the oracle.
 
-Each case draws its own geometry (head_dim 64 or 128, 1-8 KV heads, groups
-1-8, 1-3 layers with a random layer attended), batch shape (a length profile,
+Each case draws its own geometry (head_dim 64 or 128, 1-8 KV heads and groups
+1-8, or 16-32 KV heads and groups 1-4; 1-3 layers with a random layer attended), batch shape (a length profile,
 table widths wider than needed) and call mode (append or not, device or host
 lengths, the static-scratch decode, prefill with or without the turn's K/V
 and with or without the item counters), so that combinations the targeted
@@ -32,10 +32,12 @@ def kv():
     return kv_mod
 
 
-def _geometry(rng):
+def _geometry(rng, wide=False):
+    """head_dim, KV heads, query heads, layers, attended layer.  ``wide``: 16 or
+    32 KV heads (multi-head-like models), groups of 1, 2 or 4."""
     d = int(rng.choice([64, 128]))
-    hkv = int(rng.choice([1, 2, 4, 8]))
-    g = int(rng.choice([1, 2, 4, 8]))
+    hkv = int(rng.choice([16, 32] if wide else [1, 2, 4, 8]))
+    g = int(rng.choice([1, 2, 4] if wide else [1, 2, 4, 8]))
     nl = int(rng.integers(1, 4))
     return d, hkv, g * hkv, nl, int(rng.integers(0, nl))
 
@@ -71,10 +73,10 @@ def _decode_lengths(rng, append):
     return profile, lens.astype(np.int64)
 
 
-def decode_inputs(oracle_lib, seed):
+def decode_inputs(oracle_lib, seed, wide=False):
     """One seeded decode case and the oracle's result for it."""
-    rng = np.random.default_rng(8100 + seed)
-    d, hkv, hq, nl, layer = _geometry(rng)
+    rng = np.random.default_rng((8600 if wide else 8100) + seed)
+    d, hkv, hq, nl, layer = _geometry(rng, wide)
     append = bool(rng.random() < 0.5)
     host = bool(rng.random() < 0.5)
     static = bool(rng.random() < 0.25)
@@ -103,7 +105,15 @@ def decode_inputs(oracle_lib, seed):
 
 @pytest.mark.parametrize("seed", range(64))
 def test_decode_random(kv, oracle_lib, seed):
-    x = decode_inputs(oracle_lib, seed)
+    _check_decode(kv, decode_inputs(oracle_lib, seed))
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_decode_random_many_kv_heads(kv, oracle_lib, seed):
+    _check_decode(kv, decode_inputs(oracle_lib, seed, wide=True))
+
+
+def _check_decode(kv, x):
     what, d, hq, layer, lens, tables, kn, vn, scale = (x[k] for k in ("what", "d", "hq", "layer", "lens",
                                                                       "tables", "kn", "vn", "scale"))
     S = len(lens)
@@ -136,10 +146,10 @@ def _prefill_lengths(rng):
     return n.astype(np.int64), c.astype(np.int64)
 
 
-def prefill_inputs(oracle_lib, seed):
+def prefill_inputs(oracle_lib, seed, wide=False):
     """One seeded prefill case and the oracle's result for it."""
-    rng = np.random.default_rng(9100 + seed)
-    d, hkv, hq, nl, layer = _geometry(rng)
+    rng = np.random.default_rng((9600 if wide else 9100) + seed)
+    d, hkv, hq, nl, layer = _geometry(rng, wide)
     mode = str(rng.choice(["device-lengths", "host-lengths", "host-lengths-counters"]))
     with_kv = bool(rng.random() < 0.8)
     n, c = _prefill_lengths(rng)
@@ -180,7 +190,15 @@ def prefill_inputs(oracle_lib, seed):
 
 @pytest.mark.parametrize("seed", range(48))
 def test_prefill_random(kv, oracle_lib, seed):
-    x = prefill_inputs(oracle_lib, seed)
+    _check_prefill(kv, prefill_inputs(oracle_lib, seed))
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_prefill_random_many_kv_heads(kv, oracle_lib, seed):
+    _check_prefill(kv, prefill_inputs(oracle_lib, seed, wide=True))
+
+
+def _check_prefill(kv, x):
     what, d, hq, layer, mode, with_kv, n, c, cu, tables, kn, vn = (
         x[k] for k in ("what", "d", "hq", "layer", "mode", "with_kv", "n", "c", "cu", "tables", "kn", "vn"))
     total = int(n.sum())
