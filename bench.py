@@ -904,7 +904,7 @@ def calib_leg(torch, args):
 def main():
     args = parse()
     if args.gpus != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (sessions would be "
+        print("bench.py measures one GPU: the library has no multi-GPU path (sessions would be "
               "sharded across GPUs with no exchange inside attention); run with --gpus 1",
               file=sys.stderr)
         sys.exit(2)
