@@ -499,16 +499,21 @@ def restore_leg(torch, kv, W, args, dec):
             if n_dec % 16 == 0:
                 dec_stream.synchronize()
         torch.cuda.synchronize()
+        calls = np.array([a.elapsed_time(b) for a, b in dtimer.pairs]) * 1e3
         return {"steps": n_dec, "makespan": time.perf_counter() - t0,
                 "side_ms": round(ev_side_start.elapsed_time(ev_side_end), 3),
-                "us": round(dtimer.mean_ms() * 1e3, 2) if n_dec else float("nan")}
+                "us": round(float(calls.mean()), 2) if n_dec else float("nan"),
+                "p50": round(float(np.median(calls)), 1) if n_dec else float("nan"),
+                "p99": round(float(np.percentile(calls, 99)), 1) if n_dec else float("nan")}
 
     curve, best, part, dev_overlap = [], None, {}, {}
     if overlaps:
         # Decode alone, timed the same way (one event pair per call, a sync every
         # 16 calls): the reference for every slowdown below.
-        dec_alone_ms = overlap_decode(None, alone=True)["us"] * 1e-3
-        log("decode alone, single calls: %.1f us" % (dec_alone_ms * 1e3))
+        alone = overlap_decode(None, alone=True)
+        dec_alone_ms = alone["us"] * 1e-3
+        log("decode alone, single calls: %.1f us (p50 %.1f, p99 %.1f us)" % (dec_alone_ms * 1e3, alone["p50"],
+                                                                             alone["p99"]))
         ov = overlap_decode(lambda st: kv.kv_blocks_restore(pool, b, staging, stream=st))
         n_dec, side_ms, dec_conc_ms = ov["steps"], ov["side_ms"], ov["us"] * 1e-3
         agg = (2.0 * payload + n_dec * dec["alg_bytes"]) / ov["makespan"] / 1e9
@@ -516,6 +521,7 @@ def restore_leg(torch, kv, W, args, dec):
             side_ms, n_dec, dec_conc_ms * 1e3, dec_alone_ms * 1e3))
         dev_overlap = {"restore_side_stream_ms": round(side_ms, 3), "decode_steps": n_dec,
                        "decode_us_alone": round(dec_alone_ms * 1e3, 2),
+                       "decode_us_alone_p50": alone["p50"], "decode_us_alone_p99": alone["p99"],
                        "decode_us_concurrent": round(dec_conc_ms * 1e3, 2),
                        "decode_slowdown_pct": round(100 * (dec_conc_ms / dec_alone_ms - 1), 1),
                        "aggregate_gbs": round(agg, 1)}
@@ -531,10 +537,12 @@ def restore_leg(torch, kv, W, args, dec):
             gbs_b = 2.0 * nb_b * per_block / (pt["side_ms"] * 1e-3) / 1e9
             curve.append({"max_gbps_payload": gbps, "blocks": nb_b, "restore_ms": pt["side_ms"],
                           "restore_gbs_2n": round(gbs_b, 1), "decode_steps": pt["steps"],
-                          "decode_us_concurrent": pt["us"],
+                          "decode_us_concurrent": pt["us"], "decode_us_p50": pt["p50"],
+                          "decode_us_p99": pt["p99"],
                           "decode_slowdown_pct": round(100 * (pt["us"] * 1e-3 / dec_alone_ms - 1), 1)})
-            log("paced restore: cap %s GB/s payload, %.0f GB/s (2N) over %.1f ms, decode %.1f us (+%.1f%%)" % (
-                gbps or "none", gbs_b, pt["side_ms"], pt["us"], curve[-1]["decode_slowdown_pct"]))
+            log("paced restore: cap %s GB/s payload, %.0f GB/s (2N) over %.1f ms, decode %.1f us (+%.1f%%; "
+                "per call p50 %.1f, p99 %.1f us)" % (gbps or "none", gbs_b, pt["side_ms"], pt["us"],
+                                                     curve[-1]["decode_slowdown_pct"], pt["p50"], pt["p99"]))
         within = [p for p in curve if p["decode_slowdown_pct"] <= 10.0]
         best = max(within, key=lambda p: p["restore_gbs_2n"]) if within else None
 
